@@ -1,0 +1,345 @@
+// C ABI of the MoE decode library: argument validation, workspace carve-up and the
+// launch sequence of one decode step.  Declared in include/moe_decode.h.
+#include <hip/hip_runtime.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <new>
+
+#include "../../include/moe_decode.h"
+#include "moe_internal.h"
+
+namespace moe {
+
+static size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+size_t carve_workspace(int H, int E, int I, int kmax, int Tmax, void *base, Workspace *ws)
+{
+    const size_t P = (size_t)Tmax * kmax;  // (token, choice) pairs = slots
+    const MetaIdx mi{E};
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        size_t o = off;
+        off += align256(bytes);
+        return (char *)base + o;
+    };
+    Workspace w;
+    w.logits = (float *)take(sizeof(float) * (size_t)Tmax * E);
+    w.ids = (int32_t *)take(sizeof(int32_t) * P);
+    w.wts = (float *)take(sizeof(float) * P);
+    w.meta = (int32_t *)take(sizeof(int32_t) * (size_t)mi.words());
+    w.slot_of = (int32_t *)take(sizeof(int32_t) * P);
+    w.tok_of = (int32_t *)take(sizeof(int32_t) * P);
+    w.h = (float *)take(sizeof(float) * P * I);
+    w.o = (float *)take(sizeof(float) * P * H);
+    w.fb = (int32_t *)take(sizeof(int32_t) * (size_t)Tmax * E);
+    w.bytes = off;
+    if (ws) *ws = w;
+    return off;
+}
+
+}  // namespace moe
+
+using namespace moe;
+
+struct moe_decode_s {
+    moe_decode_config cfg;
+    Layer L;
+    Workspace ws;
+    int mstar;  // MFMA threshold in tokens per expert (<= 0: GEMV only)
+    hipStream_t last_stream;
+    int last_T;
+    char err[256];
+    // profiler
+    int prof_cap, prof_n;
+    hipEvent_t *prof_ev;  // [prof_cap][MOE_N_STAGES + 1]
+};
+
+static thread_local char g_init_err[256];
+
+#define FAIL(buf, code, ...)            \
+    do {                                \
+        snprintf(buf, 256, __VA_ARGS__); \
+        return code;                    \
+    } while (0)
+
+static moe_status check_config(const moe_decode_config *c, char *err)
+{
+    if (!c) FAIL(err, MOE_ERR_INVALID, "config is NULL");
+    for (int i = 0; i < 7; ++i)
+        if (c->reserved[i] != 0) FAIL(err, MOE_ERR_INVALID, "config.reserved[%d] must be zero", i);
+    if (c->wfmt != MOE_WFMT_FP8_E4M3_B128 && c->wfmt != MOE_WFMT_MXFP4_E2M1_B32)
+        FAIL(err, MOE_ERR_INVALID, "unknown weight format %d", c->wfmt);
+    const int q = c->wfmt == MOE_WFMT_FP8_E4M3_B128 ? 128 : 256;
+    if (c->hidden <= 0 || c->hidden % q) FAIL(err, MOE_ERR_INVALID, "hidden=%d must be a positive multiple of %d", c->hidden, q);
+    if (c->inter <= 0 || c->inter % q) FAIL(err, MOE_ERR_INVALID, "inter=%d must be a positive multiple of %d", c->inter, q);
+    if (c->n_experts < 1 || c->n_experts > 1024) FAIL(err, MOE_ERR_INVALID, "n_experts=%d outside 1..1024", c->n_experts);
+    const int kcap = c->n_experts < 64 ? c->n_experts : 64;
+    if (c->max_topk < 1 || c->max_topk > kcap) FAIL(err, MOE_ERR_INVALID, "max_topk=%d outside 1..%d", c->max_topk, kcap);
+    if (c->max_tokens < 1 || c->max_tokens > 1024) FAIL(err, MOE_ERR_INVALID, "max_tokens=%d outside 1..1024", c->max_tokens);
+    if ((long)c->n_experts * ((c->max_tokens + 31) / 32) > 8192)
+        FAIL(err, MOE_ERR_INVALID, "n_experts * ceil(max_tokens/32) = %ld exceeds 8192",
+             (long)c->n_experts * ((c->max_tokens + 31) / 32));
+    if (c->act_dtype != MOE_DTYPE_F32 && c->act_dtype != MOE_DTYPE_BF16)
+        FAIL(err, MOE_ERR_INVALID, "unknown act_dtype %d", c->act_dtype);
+    if (c->router_dtype != MOE_DTYPE_F32 && c->router_dtype != MOE_DTYPE_BF16)
+        FAIL(err, MOE_ERR_INVALID, "unknown router_dtype %d", c->router_dtype);
+    {
+        // The GEMV path stages 4 activation rows of max(H, I) elements in LDS.
+        const long stage = 4L * (c->hidden > c->inter ? c->hidden : c->inter) * (c->act_dtype == MOE_DTYPE_BF16 ? 2 : 4);
+        if (stage > 65536)
+            FAIL(err, MOE_ERR_UNSUPPORTED, "activation staging of %ld bytes exceeds 64 KiB of LDS", stage);
+    }
+    if (c->mfma_min_tokens > 0) FAIL(err, MOE_ERR_UNSUPPORTED, "MFMA expert tiles are not available in this build (mfma_min_tokens=%d)", c->mfma_min_tokens);
+    return MOE_OK;
+}
+
+extern "C" {
+
+size_t moe_decode_workspace_bytes(const moe_decode_config *cfg)
+{
+    char err[256];
+    if (check_config(cfg, err) != MOE_OK) return 0;
+    return carve_workspace(cfg->hidden, cfg->n_experts, cfg->inter, cfg->max_topk, cfg->max_tokens, nullptr, nullptr);
+}
+
+size_t moe_decode_expert_weight_bytes(const moe_decode_config *cfg)
+{
+    char err[256];
+    if (check_config(cfg, err) != MOE_OK) return 0;
+    const size_t H = cfg->hidden, I = cfg->inter;
+    return cfg->wfmt == MOE_WFMT_FP8_E4M3_B128 ? 3 * H * I : 3 * H * I / 2;
+}
+
+size_t moe_decode_expert_scale_bytes(const moe_decode_config *cfg)
+{
+    char err[256];
+    if (check_config(cfg, err) != MOE_OK) return 0;
+    const size_t H = cfg->hidden, I = cfg->inter;
+    return cfg->wfmt == MOE_WFMT_FP8_E4M3_B128 ? 4 * 3 * (H / 128) * (I / 128) : 3 * H * I / 32;
+}
+
+moe_status moe_decode_init(const moe_decode_config *cfg, void *workspace, size_t workspace_bytes, moe_decode_t *out)
+{
+    g_init_err[0] = 0;
+    if (!out) FAIL(g_init_err, MOE_ERR_INVALID, "out is NULL");
+    *out = nullptr;
+    moe_status s = check_config(cfg, g_init_err);
+    if (s != MOE_OK) return s;
+    const size_t need = moe_decode_workspace_bytes(cfg);
+    if (!workspace) FAIL(g_init_err, MOE_ERR_WORKSPACE, "workspace is NULL");
+    if ((uintptr_t)workspace % 256) FAIL(g_init_err, MOE_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+    if (workspace_bytes < need)
+        FAIL(g_init_err, MOE_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+    moe_decode_s *h = new (std::nothrow) moe_decode_s();
+    if (!h) FAIL(g_init_err, MOE_ERR_INVALID, "out of host memory");
+    h->cfg = *cfg;
+    h->L.H = cfg->hidden;
+    h->L.E = cfg->n_experts;
+    h->L.I = cfg->inter;
+    h->L.wfmt = cfg->wfmt;
+    h->L.act_bf16 = cfg->act_dtype == MOE_DTYPE_BF16;
+    h->L.router_bf16 = cfg->router_dtype == MOE_DTYPE_BF16;
+    h->L.expert_w_bytes = moe_decode_expert_weight_bytes(cfg);
+    h->L.expert_s_bytes = moe_decode_expert_scale_bytes(cfg);
+    carve_workspace(cfg->hidden, cfg->n_experts, cfg->inter, cfg->max_topk, cfg->max_tokens, workspace, &h->ws);
+    h->mstar = 0;  // GEMV only
+    h->last_stream = nullptr;
+    h->last_T = -1;
+    h->err[0] = 0;
+    h->prof_cap = h->prof_n = 0;
+    h->prof_ev = nullptr;
+    *out = h;
+    return MOE_OK;
+}
+
+static moe_status check_ptr(moe_decode_t h, const void *p, const char *name, int align, bool nullable)
+{
+    if (!p) {
+        if (nullable) return MOE_OK;
+        FAIL(h->err, MOE_ERR_INVALID, "%s is NULL", name);
+    }
+    if ((uintptr_t)p % align) FAIL(h->err, MOE_ERR_INVALID, "%s is not %d-byte aligned", name, align);
+    return MOE_OK;
+}
+
+#define CHECK(expr)                     \
+    do {                                \
+        moe_status _s = (expr);         \
+        if (_s != MOE_OK) return _s;    \
+    } while (0)
+
+#define HIPCHECK(h, expr)                                                                  \
+    do {                                                                                   \
+        hipError_t _e = (expr);                                                            \
+        if (_e != hipSuccess) FAIL((h)->err, MOE_ERR_HIP, "%s: %s", #expr, hipGetErrorString(_e)); \
+    } while (0)
+
+static moe_status check_common(moe_decode_t h, const void *x, int32_t T, const void *router_w, const float *bias,
+                               int32_t topk, const int32_t *ids, const float *wts)
+{
+    if (!h) return MOE_ERR_INVALID;
+    h->err[0] = 0;
+    if (T < 0 || T > h->cfg.max_tokens)
+        FAIL(h->err, MOE_ERR_INVALID, "n_tokens=%d outside 0..%d", T, h->cfg.max_tokens);
+    if (topk < 1 || topk > h->cfg.max_topk)
+        FAIL(h->err, MOE_ERR_INVALID, "topk=%d outside 1..%d", topk, h->cfg.max_topk);
+    CHECK(check_ptr(h, x, "x", 16, false));
+    CHECK(check_ptr(h, router_w, "router_w", 16, false));
+    CHECK(check_ptr(h, bias, "router_bias", 4, true));
+    CHECK(check_ptr(h, ids, "topk_ids", 4, true));
+    CHECK(check_ptr(h, wts, "topk_weights", 4, true));
+    return MOE_OK;
+}
+
+static void prof_mark(moe_decode_t h, int stage_boundary, hipStream_t st)
+{
+    if (h->prof_n < h->prof_cap) hipEventRecord(h->prof_ev[h->prof_n * (MOE_N_STAGES + 1) + stage_boundary], st);
+}
+
+moe_status moe_decode_route(moe_decode_t h, void *stream, const void *x, int32_t n_tokens, const void *router_w,
+                            const float *router_bias, int32_t topk, float *logits, int32_t *topk_ids,
+                            float *topk_weights)
+{
+    CHECK(check_common(h, x, n_tokens, router_w, router_bias, topk, topk_ids, topk_weights));
+    CHECK(check_ptr(h, logits, "logits", 4, true));
+    if (n_tokens == 0) return MOE_OK;
+    hipStream_t st = (hipStream_t)stream;
+    const Workspace &w = h->ws;
+    HIPCHECK(h, launch_router(h->L, x, n_tokens, router_w, router_bias, w.logits, w.fb, st));
+    HIPCHECK(h, launch_topk(h->L, w.logits, n_tokens, topk, w.ids, w.wts, topk_ids, topk_weights, st));
+    if (logits)
+        HIPCHECK(h, hipMemcpyAsync(logits, w.logits, sizeof(float) * (size_t)n_tokens * h->L.E,
+                                   hipMemcpyDeviceToDevice, st));
+    return MOE_OK;
+}
+
+moe_status moe_decode_forward(moe_decode_t h, void *stream, const void *x, int32_t n_tokens, const void *router_w,
+                              const float *router_bias, const void *expert_w, const void *scales, int32_t topk,
+                              void *y, int32_t *topk_ids, float *topk_weights)
+{
+    CHECK(check_common(h, x, n_tokens, router_w, router_bias, topk, topk_ids, topk_weights));
+    CHECK(check_ptr(h, expert_w, "expert_w", 16, false));
+    CHECK(check_ptr(h, scales, "scales", 4, false));
+    CHECK(check_ptr(h, y, "y", 16, false));
+    if (y == x) FAIL(h->err, MOE_ERR_INVALID, "y must not alias x");
+    hipStream_t st = (hipStream_t)stream;
+    h->last_stream = st;
+    h->last_T = n_tokens;
+    if (n_tokens == 0) return MOE_OK;
+    const Workspace &w = h->ws;
+    const Layer &L = h->L;
+    const int T = n_tokens, k = topk;
+    const bool prof = h->prof_n < h->prof_cap;
+    if (prof) prof_mark(h, 0, st);
+    HIPCHECK(h, launch_router(L, x, T, router_w, router_bias, w.logits, w.fb, st));
+    HIPCHECK(h, launch_topk(L, w.logits, T, k, w.ids, w.wts, topk_ids, topk_weights, st));
+    HIPCHECK(h, launch_group(L, w.ids, T, k, h->mstar, w.meta, w.slot_of, w.tok_of, w.fb, st));
+    if (prof) prof_mark(h, 1, st);
+    HIPCHECK(h, launch_w13(L, expert_w, scales, x, T, k, w.meta, w.tok_of, w.h, st));
+    if (prof) prof_mark(h, 2, st);
+    HIPCHECK(h, launch_w2(L, expert_w, scales, T, k, w.meta, w.h, w.o, st));
+    if (prof) prof_mark(h, 3, st);
+    HIPCHECK(h, launch_combine(L, T, k, w.slot_of, w.wts, w.o, y, st));
+    if (prof) {
+        prof_mark(h, 4, st);
+        h->prof_n++;
+    }
+    return MOE_OK;
+}
+
+moe_status moe_decode_get_stats(moe_decode_t h, moe_decode_stats *out, int32_t *counts_host)
+{
+    if (!h) return MOE_ERR_INVALID;
+    if (!out) FAIL(h->err, MOE_ERR_INVALID, "out is NULL");
+    memset(out, 0, sizeof *out);
+    if (h->last_T < 0) FAIL(h->err, MOE_ERR_INVALID, "no forward call on this handle yet");
+    out->n_tokens = h->last_T;
+    if (h->last_T == 0) {
+        if (counts_host) memset(counts_host, 0, sizeof(int32_t) * h->L.E);
+        return MOE_OK;
+    }
+    HIPCHECK(h, hipStreamSynchronize(h->last_stream));
+    const MetaIdx mi{h->L.E};
+    int32_t head[8];
+    HIPCHECK(h, hipMemcpy(head, h->ws.meta, sizeof head, hipMemcpyDeviceToHost));
+    out->n_active = head[mi.n_active()];
+    out->n_active_mfma = head[mi.n_mfma()];
+    out->n_fallback = head[mi.n_fallback()];
+    out->active_weight_bytes = (int64_t)out->n_active * (int64_t)(h->L.expert_w_bytes + h->L.expert_s_bytes);
+    if (counts_host)
+        HIPCHECK(h, hipMemcpy(counts_host, h->ws.meta + mi.counts(), sizeof(int32_t) * h->L.E, hipMemcpyDeviceToHost));
+    return MOE_OK;
+}
+
+static void prof_release(moe_decode_t h)
+{
+    if (h->prof_ev) {
+        for (int i = 0; i < h->prof_cap * (MOE_N_STAGES + 1); ++i)
+            if (h->prof_ev[i]) hipEventDestroy(h->prof_ev[i]);
+        free(h->prof_ev);
+    }
+    h->prof_ev = nullptr;
+    h->prof_cap = h->prof_n = 0;
+}
+
+moe_status moe_decode_profile_enable(moe_decode_t h, int32_t max_calls)
+{
+    if (!h) return MOE_ERR_INVALID;
+    prof_release(h);
+    if (max_calls <= 0) return MOE_OK;
+    const int n = max_calls * (MOE_N_STAGES + 1);
+    h->prof_ev = (hipEvent_t *)calloc((size_t)n, sizeof(hipEvent_t));
+    if (!h->prof_ev) FAIL(h->err, MOE_ERR_INVALID, "out of host memory");
+    h->prof_cap = max_calls;
+    for (int i = 0; i < n; ++i) {
+        hipError_t e = hipEventCreate(&h->prof_ev[i]);
+        if (e != hipSuccess) {
+            prof_release(h);
+            FAIL(h->err, MOE_ERR_HIP, "hipEventCreate: %s", hipGetErrorString(e));
+        }
+    }
+    return MOE_OK;
+}
+
+moe_status moe_decode_profile_read(moe_decode_t h, float *stage_ms, int32_t *n_calls)
+{
+    if (!h) return MOE_ERR_INVALID;
+    if (!n_calls) FAIL(h->err, MOE_ERR_INVALID, "n_calls is NULL");
+    *n_calls = h->prof_n;
+    for (int c = 0; c < h->prof_n; ++c) {
+        hipEvent_t *ev = h->prof_ev + c * (MOE_N_STAGES + 1);
+        HIPCHECK(h, hipEventSynchronize(ev[MOE_N_STAGES]));
+        for (int s = 0; s < MOE_N_STAGES; ++s) {
+            float ms = 0.f;
+            HIPCHECK(h, hipEventElapsedTime(&ms, ev[s], ev[s + 1]));
+            if (stage_ms) stage_ms[c * MOE_N_STAGES + s] = ms;
+        }
+    }
+    h->prof_n = 0;
+    return MOE_OK;
+}
+
+void moe_decode_free(moe_decode_t h)
+{
+    if (!h) return;
+    prof_release(h);
+    delete h;
+}
+
+const char *moe_decode_status_string(moe_status s)
+{
+    switch (s) {
+    case MOE_OK: return "ok";
+    case MOE_ERR_INVALID: return "invalid argument";
+    case MOE_ERR_UNSUPPORTED: return "unsupported configuration";
+    case MOE_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case MOE_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+const char *moe_decode_last_error(moe_decode_t h) { return h ? h->err : g_init_err; }
+
+}  // extern "C"

@@ -1,0 +1,158 @@
+"""The C-ABI library loads, exports every symbol of include/moe_decode.h, and rejects
+invalid arguments before enqueuing anything (runs without a GPU: nothing here
+reaches a HIP call)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moe_decode.h")
+
+
+@pytest.fixture(scope="module")
+def B():
+    from paper_2609_11133_amd import binding
+
+    if not os.path.exists(binding.LIB_PATH):
+        from paper_2609_11133_amd import build
+
+        build.build(force=True)
+    binding.lib()
+    return binding
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(moe_decode_\w+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported(B):
+    names = declared_functions()
+    assert len(names) >= 10
+    lib = ctypes.CDLL(B.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_no_oracle_or_generator_symbols_in_library(B):
+    out = os.popen(f"nm -D --defined-only {B.LIB_PATH}").read()
+    assert "oracle_" not in out and "synth_" not in out
+
+
+def cfg(B, **kw):
+    base = dict(hidden=512, n_experts=16, inter=256, max_topk=4, max_tokens=32)
+    base.update(kw)
+    return B.make_config(**base)
+
+
+def test_workspace_bytes_and_sizes(B):
+    c = cfg(B)
+    assert B.moe_decode_workspace_bytes(c) > 0
+    assert B.moe_decode_expert_weight_bytes(c) == 3 * 512 * 256
+    assert B.moe_decode_expert_scale_bytes(c) == 4 * 3 * 4 * 2
+    c4 = cfg(B, wfmt=B.MOE_WFMT_MXFP4_E2M1_B32)
+    assert B.moe_decode_expert_weight_bytes(c4) == 3 * 512 * 256 // 2
+    assert B.moe_decode_expert_scale_bytes(c4) == 3 * 512 * 256 // 32
+
+
+@pytest.mark.parametrize(
+    "kw,code",
+    [
+        (dict(hidden=500), -1),
+        (dict(hidden=0), -1),
+        (dict(inter=100), -1),
+        (dict(hidden=128, wfmt=1), -1),  # MXFP4 needs multiples of 256
+        (dict(n_experts=0), -1),
+        (dict(n_experts=2000), -1),
+        (dict(max_topk=17), -1),
+        (dict(max_topk=0), -1),
+        (dict(max_tokens=0), -1),
+        (dict(max_tokens=4096), -1),
+        (dict(act_dtype=7), -1),
+        (dict(wfmt=3), -1),
+    ],
+)
+def test_invalid_configs_rejected(B, kw, code):
+    c = cfg(B, **kw)
+    assert B.moe_decode_workspace_bytes(c) == 0
+    with pytest.raises(B.MoEDecodeError) as ei:
+        B.moe_decode_init(c, 1 << 20, 1 << 30)
+    assert ei.value.status == code
+    assert B.moe_decode_last_error(None)
+
+
+def test_reserved_must_be_zero(B):
+    c = cfg(B)
+    c.reserved[3] = 1
+    assert B.moe_decode_workspace_bytes(c) == 0
+
+
+def test_workspace_checks(B):
+    c = cfg(B)
+    need = B.moe_decode_workspace_bytes(c)
+    for ws, nb in [(None, need), (4096 + 16, need), (4096, need - 1)]:
+        with pytest.raises(B.MoEDecodeError) as ei:
+            B.moe_decode_init(c, ws, nb)
+        assert ei.value.status == B.MOE_ERR_WORKSPACE
+
+
+FAKE = 1 << 32  # a 256-aligned address; nothing dereferences it in these tests
+
+
+def make_handle(B):
+    c = cfg(B)
+    return B.moe_decode_init(c, FAKE, B.moe_decode_workspace_bytes(c))
+
+
+@pytest.mark.parametrize(
+    "change,needle",
+    [
+        (dict(n_tokens=33), "n_tokens"),
+        (dict(n_tokens=-1), "n_tokens"),
+        (dict(topk=5), "topk"),
+        (dict(topk=0), "topk"),
+        (dict(x=None), "x is NULL"),
+        (dict(x=FAKE + 8), "x is not 16-byte aligned"),
+        (dict(router_w=FAKE + 4), "router_w"),
+        (dict(expert_w=None), "expert_w"),
+        (dict(scales=FAKE + 2), "scales"),
+        (dict(y=None), "y is NULL"),
+        (dict(y=FAKE), "alias"),
+        (dict(router_bias=FAKE + 1), "router_bias"),
+        (dict(topk_ids=FAKE + 2), "topk_ids"),
+    ],
+)
+def test_forward_validates_before_launch(B, change, needle):
+    h = make_handle(B)
+    args = dict(stream=None, x=FAKE, n_tokens=4, router_w=FAKE + 4096, router_bias=None, expert_w=FAKE + 8192,
+                scales=FAKE + 12288, topk=2, y=FAKE + 16384, topk_ids=None, topk_weights=None)
+    args.update(change)
+    with pytest.raises(B.MoEDecodeError) as ei:
+        B.moe_decode_forward(h, **args)
+    assert ei.value.status == B.MOE_ERR_INVALID
+    assert needle in str(ei.value)
+    B.moe_decode_free(h)
+
+
+def test_zero_tokens_is_a_no_op(B):
+    h = make_handle(B)
+    B.moe_decode_forward(h, None, FAKE, 0, FAKE + 4096, None, FAKE + 8192, FAKE + 12288, 2, FAKE + 16384)
+    st, counts = B.moe_decode_get_stats(h, 16)
+    assert st.n_tokens == 0 and st.n_active == 0 and counts == [0] * 16
+    B.moe_decode_free(h)
+
+
+def test_stats_before_forward_is_an_error(B):
+    h = make_handle(B)
+    with pytest.raises(B.MoEDecodeError):
+        B.moe_decode_get_stats(h, 16)
+    B.moe_decode_free(h)
+
+
+def test_status_strings(B):
+    for s in (0, -1, -2, -3, -4):
+        assert B.moe_decode_status_string(s)
+    B.lib().moe_decode_free(None)  # NULL is ignored

@@ -1,0 +1,272 @@
+"""Parity of the HIP decode layer (through the C ABI) with the fp64 oracle.
+
+Routing must match bit-exactly (canonical logits and expert ids, ties to the lower
+index); routing weights within 1e-6; outputs within max|err| <= 2e-2 * max|ref|.
+Small layers are compared on every token; the full-size 235B/480B-shaped layers on
+every token's routing and on sampled tokens' outputs (the oracle computes tokens
+independently)."""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_11133_amd import configs as C
+from paper_2609_11133_amd import workload as W
+from paper_2609_11133_amd.configs import LayerConfig
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+THREADS = min(16, os.cpu_count() or 1)
+TOL = 2e-2
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_11133_amd import binding as B
+
+    B.lib()  # fails loudly if the library is missing
+    return torch.device("cuda:0")
+
+
+class Run:
+    def __init__(self, cfg, hl, dev, max_tokens, mfma_min_tokens=0):
+        from paper_2609_11133_amd import binding as B
+
+        self.cfg, self.hl, self.dev = cfg, hl, dev
+        self.m = B.MoEDecode(W.binding_config(cfg, max_tokens, mfma_min_tokens), device=dev)
+        self.rw = W.to_device(hl.router_w, dev)
+        self.bias = W.to_device(hl.bias, dev)
+        self.ew = W.to_device(hl.expert_w, dev)
+        self.sc = W.to_device(hl.scales, dev)
+
+    def forward(self, x, topk=None):
+        k = topk or self.cfg.topk
+        T = x.shape[0]
+        xd = W.to_device(x, self.dev)
+        y = W.empty_y(self.cfg, T, self.dev)
+        ids = torch.full((T, k), -1, dtype=torch.int32, device=self.dev)
+        wts = torch.zeros((T, k), dtype=torch.float32, device=self.dev)
+        self.m.forward(xd, T, self.rw, self.bias, self.ew, self.sc, k, y, ids, wts)
+        torch.cuda.synchronize(self.dev)
+        return ids.cpu().numpy(), wts.cpu().numpy(), W.y_to_f64(y)
+
+    def route(self, x, topk=None):
+        k = topk or self.cfg.topk
+        T = x.shape[0]
+        xd = W.to_device(x, self.dev)
+        lg = torch.empty((T, self.cfg.n_experts), dtype=torch.float32, device=self.dev)
+        ids = torch.empty((T, k), dtype=torch.int32, device=self.dev)
+        wts = torch.empty((T, k), dtype=torch.float32, device=self.dev)
+        self.m.route(xd, T, self.rw, self.bias, k, lg, ids, wts)
+        torch.cuda.synchronize(self.dev)
+        return lg.cpu().numpy(), ids.cpu().numpy(), wts.cpu().numpy()
+
+
+def check_layer(run, x, tokens=None, topk=None, label=""):
+    cfg, hl = run.cfg, run.hl
+    k = topk or cfg.topk
+    say(f"[parity] {label} T={x.shape[0]} k={k} tokens={'all' if tokens is None else list(tokens)}")
+    ids, wts, y = run.forward(x, topk=k)
+    lo, io, wo, yo = oracle.forward(x, hl.router_w, hl.bias, hl.expert_w, hl.scales, k, cfg.inter, cfg.wfmt_id,
+                                    tokens=tokens, threads=THREADS)
+    sel = slice(None) if tokens is None else np.asarray(tokens)
+    assert np.array_equal(ids[sel], io), f"{label}: expert selection differs"
+    assert np.abs(wts[sel] - wo).max() <= 1e-6, f"{label}: routing weights differ"
+    ref = yo
+    err = np.abs(y[sel] - ref).max()
+    scale = np.abs(ref).max()
+    say(f"[parity] {label}: max|err|/max|ref| = {err / scale if scale else err:.3e}")
+    if scale == 0:
+        assert err == 0
+    else:
+        assert err <= TOL * scale, f"{label}: max|err| {err} > {TOL} * {scale}"
+    return ids, wts, y
+
+
+def check_routing(run, x, topk=None, label=""):
+    cfg, hl = run.cfg, run.hl
+    k = topk or cfg.topk
+    say(f"[routing] {label} T={x.shape[0]} k={k}")
+    lg, ids, wts = run.route(x, topk=k)
+    for t in range(x.shape[0]):
+        l_o, i_o, w_o, _ = oracle.route_token(x[t], hl.router_w, hl.bias, k)
+        assert np.array_equal(lg[t].view(np.uint32), l_o.view(np.uint32)), f"{label}: logits of token {t} differ"
+        assert np.array_equal(ids[t], i_o), f"{label}: selection of token {t} differs"
+        assert np.abs(wts[t] - w_o).max() <= 1e-6
+    return lg, ids, wts
+
+
+# ---------------------------------------------------------------- small layers, every token
+
+SMALL_FP8 = LayerConfig("small-fp8", 512, 16, 4, 256, "bf16", "bf16", "fp8", "normal:0.5", [])
+SMALL_MX = LayerConfig("small-mxfp4", 512, 16, 4, 512, "bf16", "bf16", "mxfp4", "zipf:1.1", [])
+SMALL_F32_MX = LayerConfig("small-f32-mxfp4", 256, 8, 2, 256, "f32", "f32", "mxfp4", None, [])
+
+
+@pytest.mark.parametrize("T", [1, 5, 13, 32])
+def test_small_fp8_layer(dev, T):
+    hl = W.host_layer(SMALL_FP8, seed=501)
+    run = Run(SMALL_FP8, hl, dev, max_tokens=32)
+    check_layer(run, W.host_x(SMALL_FP8, T, seed=501), label=f"small-fp8 T={T}")
+
+
+@pytest.mark.parametrize("T", [3, 13])
+def test_small_mxfp4_layer(dev, T):
+    hl = W.host_layer(SMALL_MX, seed=502)
+    run = Run(SMALL_MX, hl, dev, max_tokens=16)
+    check_layer(run, W.host_x(SMALL_MX, T, seed=502), label=f"small-mxfp4 T={T}")
+
+
+def test_tiny_config(dev):
+    cfg = C.TINY
+    hl = W.host_layer(cfg)
+    run = Run(cfg, hl, dev, max_tokens=4)
+    check_layer(run, W.host_x(cfg, 4), label="tiny")
+    check_routing(run, W.host_x(cfg, 4), label="tiny")
+
+
+def test_fp32_mxfp4_layer(dev):
+    hl = W.host_layer(SMALL_F32_MX, seed=503)
+    run = Run(SMALL_F32_MX, hl, dev, max_tokens=8)
+    check_layer(run, W.host_x(SMALL_F32_MX, 6, seed=503), label="f32-mxfp4")
+
+
+def test_small_routing_bitwise(dev):
+    hl = W.host_layer(SMALL_FP8, seed=504)
+    run = Run(SMALL_FP8, hl, dev, max_tokens=32)
+    check_routing(run, W.host_x(SMALL_FP8, 32, seed=504), label="small-fp8")
+
+
+@pytest.mark.parametrize("k", [1, 16])
+def test_topk_extremes(dev, k):
+    cfg = LayerConfig("k-extreme", 512, 16, 16, 256, "bf16", "bf16", "fp8", None, [])
+    hl = W.host_layer(cfg, seed=505)
+    run = Run(cfg, hl, dev, max_tokens=8)
+    check_layer(run, W.host_x(cfg, 5, seed=505), topk=k, label=f"k={k}")
+
+
+def test_zero_input_and_ties(dev):
+    """x = 0, no bias: every logit is +0, the selection is experts 0..k-1 with equal
+    weights, and y = 0.  Duplicate router rows tie; the lower index wins."""
+    hl = W.host_layer(SMALL_FP8, seed=506)
+    hl.bias = None
+    hl.router_w[9] = hl.router_w[2]
+    hl.router_w[11] = hl.router_w[2]
+    run = Run(SMALL_FP8, hl, dev, max_tokens=8)
+    x = W.host_x(SMALL_FP8, 8, seed=506)
+    x[3] = 0
+    ids, wts, y = check_layer(run, x, label="zero+ties")
+    assert list(ids[3]) == [0, 1, 2, 3] and np.all(wts[3] == 0.25) and np.all(y[3] == 0)
+    check_routing(run, x, label="zero+ties")
+
+
+def test_exact_fallback_path(dev):
+    """Logits whose exact value sits on (or within 2^-80 of) an fp32 rounding midpoint
+    must take the double-double path and still equal the oracle bit for bit."""
+    from paper_2609_11133_amd import binding as B
+
+    cfg = LayerConfig("midpoint", 512, 16, 4, 256, "bf16", "bf16", "fp8", None, [])
+    hl = W.host_layer(cfg, seed=507)
+    one, tiny24, tiny80 = 0x3F80, 0x3380, 0x1780  # 1.0, 2^-24, 2^-80 in bf16
+    hl.router_w[:] = 0
+    hl.router_w[:, 0] = one
+    hl.router_w[5, 1] = tiny24          # l = 1 + 2^-24: tie -> 1.0
+    hl.router_w[6, 1] = tiny24          # l = 1 + 2^-24 + 2^-80: above the tie -> 1 + 2^-23
+    hl.router_w[6, 2] = tiny80
+    x = np.zeros((4, cfg.hidden), np.uint16)
+    x[:, 0] = one
+    x[:, 1] = one
+    x[:, 2] = one
+    run = Run(cfg, hl, dev, max_tokens=8)
+    lg, ids, _ = check_routing(run, x, label="midpoint")
+    assert lg[0, 5] == np.float32(1.0) and lg[0, 6] == np.float32(1.0 + 2.0**-23)
+    assert ids[0, 0] == 6
+    check_layer(run, x, label="midpoint")
+    st, _ = run.m.stats()
+    assert st.n_fallback >= 4
+
+
+def test_bitwise_repeatable_and_permutation_equivariant(dev):
+    hl = W.host_layer(SMALL_FP8, seed=508)
+    run = Run(SMALL_FP8, hl, dev, max_tokens=32)
+    x = W.host_x(SMALL_FP8, 29, seed=508)
+    a = run.forward(x)
+    for _ in range(3):
+        b = run.forward(x)
+        assert all(np.array_equal(p, q) for p, q in zip(a, b))
+    perm = np.random.default_rng(0).permutation(29)
+    c = run.forward(x[perm])
+    assert np.array_equal(c[0], a[0][perm]) and np.array_equal(c[2], a[2][perm])
+
+
+def test_zero_tokens_leaves_output_untouched(dev):
+    hl = W.host_layer(SMALL_FP8, seed=509)
+    run = Run(SMALL_FP8, hl, dev, max_tokens=8)
+    y = torch.full((1, SMALL_FP8.hidden), 7.0, dtype=torch.bfloat16, device=dev)
+    xd = torch.zeros((1, SMALL_FP8.hidden), dtype=torch.int16, device=dev)
+    run.m.forward(xd, 0, run.rw, run.bias, run.ew, run.sc, 4, y)
+    torch.cuda.synchronize(dev)
+    assert torch.all(y == 7.0)
+
+
+def test_max_tokens(dev):
+    cfg = LayerConfig("maxT", 512, 16, 4, 256, "bf16", "bf16", "fp8", "normal:0.5", [])
+    hl = W.host_layer(cfg, seed=510)
+    run = Run(cfg, hl, dev, max_tokens=1024)
+    check_layer(run, W.host_x(cfg, 1024, seed=510), tokens=[0, 511, 1023], label="T=1024")
+
+
+# ---------------------------------------------------------------- full-size layers
+
+@pytest.fixture(scope="module")
+def full_235b(dev):
+    say("[gen] qwen3-235b-a22b layer")
+    return W.host_layer(C.QWEN3_235B)
+
+
+@pytest.fixture(scope="module")
+def full_480b(dev):
+    say("[gen] qwen3-coder-480b-a35b layer")
+    return W.host_layer(C.QWEN3_480B)
+
+
+def _full(run, cfg, T, batch):
+    x = W.host_x(cfg, T, batch=batch)
+    tokens = sorted({0, T // 2, T - 1})
+    ids, wts, y = check_layer(run, x, tokens=tokens, label=f"{cfg.name} T={T}")
+    # routing of every token
+    io = np.stack([oracle.route_token(x[t], run.hl.router_w, run.hl.bias, cfg.topk)[1] for t in range(T)])
+    assert np.array_equal(ids, io)
+
+
+@pytest.mark.parametrize("T", C.QWEN3_235B.tokens)
+def test_full_235b(dev, full_235b, T):
+    run = Run(C.QWEN3_235B, full_235b, dev, max_tokens=max(C.QWEN3_235B.tokens))
+    _full(run, C.QWEN3_235B, T, batch=T)
+
+
+@pytest.mark.parametrize("T", C.QWEN3_480B.tokens)
+def test_full_480b(dev, full_480b, T):
+    run = Run(C.QWEN3_480B, full_480b, dev, max_tokens=max(C.QWEN3_480B.tokens))
+    _full(run, C.QWEN3_480B, T, batch=T)
+
+
+def test_full_235b_mxfp4_zipf(dev):
+    cfg = C.QWEN3_235B_MXFP4
+    say("[gen] qwen3-235b-a22b mxfp4 layer")
+    hl = W.host_layer(cfg)
+    run = Run(cfg, hl, dev, max_tokens=256)
+    _full(run, cfg, 256, batch=0)
+    st, counts = run.m.stats()
+    say(f"[zipf] active={st.n_active} max tokens/expert={max(counts)}")
+    assert max(counts) > 4 * (256 * cfg.topk / st.n_active)  # skewed popularity
