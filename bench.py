@@ -1,0 +1,287 @@
+"""Benchmark of the MoE decode layer on one MI355X.
+
+A step is one decode step of one MoE layer (router, top-k, grouping, grouped
+experts, combine) over one batch of T synthetic tokens, with all inputs resident in
+HBM.  The default workload is the Qwen3-235B-A22B-shaped layer (hidden 4096, 128
+experts, top-8, SwiGLU intermediate 1536, FP8-E4M3 weights with 128x128 fp32 block
+scales, bf16 activations) at T = 64, the largest decode batch of its sweep.
+
+Cold-cache protocol: steps cycle over L copies of the layer's expert weights at
+distinct HBM addresses and over a pool of 16 token batches, so consecutive steps
+stream weights that are not resident in the 256 MB MALL or the L2s, as in a model
+whose layers follow each other.
+
+Printed: one JSON line with tokens/s (value), the layer-level HBM rate of the
+unique activated-expert bytes, the sweep over the layer's batch sizes, the roofline
+of the dominant kernel (gate/up projection, from HIP events around it on the
+launch stream inside the timed region), board power where readable, and the fp64
+CPU oracle timed on this host's cores on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import statistics
+import sys
+import threading
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, published
+METRIC = "MoE decode-layer tokens/s and achieved HBM GB/s (% of peak) vs batch size"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="qwen3-235b-a22b")
+    ap.add_argument("--tokens", type=int, default=None, help="T of the headline line (default: largest T <= 64)")
+    ap.add_argument("--copies", type=int, default=0, help="weight copies cycled (0: enough for 8 GB)")
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-power", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU work of the oracle sample")
+    ap.add_argument("--mstar", type=int, default=0,
+                    help="tokens per expert from which MFMA tiles are used (0: library default, -1: GEMV only)")
+    return ap.parse_args()
+
+
+class PowerSampler:
+    """Board power via amdsmi every 100 ms (None where unreadable)."""
+
+    def __init__(self):
+        self.samples = []
+        self.ok = False
+        try:
+            import amdsmi
+
+            amdsmi.amdsmi_init()
+            self.amdsmi = amdsmi
+            self.h = amdsmi.amdsmi_get_processor_handles()[0]
+            self.read()
+            self.ok = True
+        except Exception as e:  # noqa: BLE001
+            self.err = repr(e)
+
+    def read(self):
+        info = self.amdsmi.amdsmi_get_power_info(self.h)
+        for key in ("socket_power", "current_socket_power", "average_socket_power"):
+            v = info.get(key)
+            if isinstance(v, (int, float)) and v > 0:
+                return float(v)
+        raise RuntimeError(f"no power field in {info}")
+
+    def run(self, stop: threading.Event):
+        while not stop.is_set():
+            try:
+                self.samples.append((time.perf_counter(), self.read()))
+            except Exception:  # noqa: BLE001
+                pass
+            stop.wait(0.1)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; multi-GPU sharding is a design note only",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2609_11133_amd import binding as B
+    from paper_2609_11133_amd import configs as C
+    from paper_2609_11133_amd import workload as W
+
+    if not os.path.exists(B.LIB_PATH):
+        import __graft_entry__
+
+        __graft_entry__.build()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    cfg = C.BY_NAME[args.config]
+    T_main = args.tokens or max(t for t in cfg.tokens if t <= 64)
+    sweep_T = sorted(set(cfg.tokens) | {T_main}) if not args.no_sweep else [T_main]
+    Tmax = max(sweep_T)
+    layer_bytes = cfg.n_experts * (cfg.expert_weight_bytes() + cfg.expert_scale_bytes())
+    copies = args.copies or max(2, math.ceil(8e9 / layer_bytes))
+
+    t0 = time.time()
+    hl = W.host_layer(cfg)
+    pool = 16
+    xs = {T: [W.to_device(W.host_x(cfg, T, batch=b), dev) for b in range(pool)] for T in sweep_T}
+    rw, bias = W.to_device(hl.router_w, dev), W.to_device(hl.bias, dev)
+    ew0, sc0 = W.to_device(hl.expert_w, dev), W.to_device(hl.scales, dev)
+    ews = [ew0] + [ew0.clone() for _ in range(copies - 1)]
+    scs = [sc0] + [sc0.clone() for _ in range(copies - 1)]
+    setup_s = time.time() - t0
+
+    m = B.MoEDecode(W.binding_config(cfg, Tmax, args.mstar), device=dev)
+    stream = torch.cuda.current_stream(dev)
+    Be = cfg.expert_bytes()
+    results = {}
+
+    for T in sweep_T:
+        ys = [W.empty_y(cfg, T, dev) for _ in range(2)]
+        # unique activated experts of each pooled batch (deterministic per batch)
+        n_act = []
+        for b in range(pool):
+            m.forward(xs[T][b], T, rw, bias, ews[0], scs[0], cfg.topk, ys[0])
+            n_act.append(m.stats()[0].n_active)
+
+        def step(i):
+            c = i % copies
+            m.forward(xs[T][i % pool], T, rw, bias, ews[c], scs[c], cfg.topk, ys[i & 1])
+
+        for i in range(args.warmup):
+            step(i)
+        torch.cuda.synchronize(dev)
+        # timed region: K steps between two events on the launch stream, with the
+        # library's stage events recording each step's kernels on the same stream
+        B.moe_decode_profile_enable(m.handle, args.steps)
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize(dev)
+        start.record(stream)
+        for i in range(args.steps):
+            step(i)
+        end.record(stream)
+        torch.cuda.synchronize(dev)
+        ms = start.elapsed_time(end) / args.steps
+        stages = B.moe_decode_profile_read(m.handle, args.steps)
+        B.moe_decode_profile_enable(m.handle, 0)
+        acts = [n_act[i % pool] for i in range(args.steps)]
+        bytes_step = statistics.mean(acts) * Be
+        st_ms = [statistics.mean(s[j] for s in stages) for j in range(B.MOE_N_STAGES)]
+        w13_bytes = statistics.mean(a * cfg.w13_bytes() for a in acts)
+        w2_bytes = statistics.mean(a * cfg.w2_bytes() for a in acts)
+        w13_gbs = w13_bytes / (st_ms[B.MOE_STAGE_W13] * 1e-3) / 1e9
+        w2_gbs = w2_bytes / (st_ms[B.MOE_STAGE_W2] * 1e-3) / 1e9
+        exp_gbs = (w13_bytes + w2_bytes) / ((st_ms[1] + st_ms[2]) * 1e-3) / 1e9
+        results[T] = dict(
+            tokens_per_s=T / (ms * 1e-3),
+            ms_per_step=ms,
+            n_active_mean=statistics.mean(acts),
+            bytes_per_step=bytes_step,
+            layer_GBs=bytes_step / (ms * 1e-3) / 1e9,
+            layer_frac=bytes_step / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS,
+            stage_ms={n: v for n, v in zip(B.STAGE_NAMES, st_ms)},
+            w13_GBs=w13_gbs,
+            w2_GBs=w2_gbs,
+            experts_GBs=exp_gbs,
+            experts_frac=exp_gbs / PEAK_HBM_GBS,
+            w13_bytes_per_launch=w13_bytes,
+        )
+        print(f"[bench] T={T}: {results[T]['tokens_per_s']:.0f} tok/s, {ms * 1e3:.1f} us/step, layer "
+              f"{results[T]['layer_GBs']:.0f} GB/s, experts {exp_gbs:.0f} GB/s, stages(us) "
+              + " ".join(f"{n}={v * 1e3:.1f}" for n, v in zip(B.STAGE_NAMES, st_ms)), file=sys.stderr, flush=True)
+
+    # board power over a steady ~4 s loop at the headline batch size
+    power = None
+    if not args.no_power:
+        ps = PowerSampler()
+        if ps.ok:
+            ys = [W.empty_y(cfg, T_main, dev) for _ in range(2)]
+            stop = threading.Event()
+            th = threading.Thread(target=ps.run, args=(stop,), daemon=True)
+            th.start()
+            n, tp0 = 0, time.perf_counter()
+            while time.perf_counter() - tp0 < 4.0:
+                for _ in range(50):
+                    c = n % copies
+                    m.forward(xs[T_main][n % pool], T_main, rw, bias, ews[c], scs[c], cfg.topk, ys[n & 1])
+                    n += 1
+                torch.cuda.synchronize(dev)
+            dt = time.perf_counter() - tp0
+            stop.set()
+            th.join()
+            watts = [w for _, w in ps.samples]
+            if watts:
+                pw = statistics.mean(watts)
+                power = dict(board_W=pw, samples=len(watts), tokens_per_J=(n * T_main / dt) / pw)
+        if power is None:
+            power = dict(board_W=None, note="amdsmi power unreadable: " + getattr(ps, "err", "no samples"))
+
+    # the fp64 oracle on this host's cores, on a bounded sample of the headline batch
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+
+        threads = len(os.sched_getaffinity(0))
+        threads = max(1, min(threads, 16))
+        x_host = W.host_x(cfg, T_main, batch=0)
+        tp = time.perf_counter()
+        oracle.forward(x_host, hl.router_w, hl.bias, hl.expert_w, hl.scales, cfg.topk, cfg.inter, cfg.wfmt_id,
+                       tokens=[0], threads=threads)
+        t1 = time.perf_counter() - tp
+        n_tok = max(1, min(T_main, int(args.cpu_seconds / max(t1, 1e-3))))
+        tokens = list(range(n_tok))
+        tp = time.perf_counter()
+        oracle.forward(x_host, hl.router_w, hl.bias, hl.expert_w, hl.scales, cfg.topk, cfg.inter, cfg.wfmt_id,
+                       tokens=tokens, threads=threads)
+        dt = time.perf_counter() - tp
+        cpu = dict(value=n_tok / dt, unit="tokens/s", cores=threads, kind="oracle",
+                   sample=f"first {n_tok} of the {T_main} tokens of batch 0: full layer in fp64 (exact router "
+                          f"logits, top-{cfg.topk}, {cfg.topk} dequantised experts per token, combine); "
+                          f"{dt:.1f} s wall")
+
+    R = results[T_main]
+    line = {
+        "metric": METRIC,
+        "value": R["tokens_per_s"],
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": R["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{cfg.name} MoE decode layer: hidden {cfg.hidden}, {cfg.n_experts} experts, top-{cfg.topk}, "
+                        f"SwiGLU intermediate {cfg.inter}, {cfg.wfmt} weights, {cfg.act} activations, "
+                        f"T={T_main} tokens per step",
+            "tokens_per_step": T_main,
+            "weights": "fp8-e4m3, fp32 scale per 128x128 block" if cfg.wfmt == "fp8" else "mxfp4 (e2m1 + e8m0/32)",
+            "activations": cfg.act,
+            "cold_cache": f"{copies} weight copies x 16 token batches cycled",
+        },
+        "hbm": {
+            "bytes_per_step": R["bytes_per_step"],
+            "layer_GBs": R["layer_GBs"],
+            "layer_frac_of_peak": R["layer_frac"],
+            "experts_GBs": R["experts_GBs"],
+            "experts_frac_of_peak": R["experts_frac"],
+            "n_active_mean": R["n_active_mean"],
+        },
+        "roofline": {
+            "kernel": "w13 (grouped gate/up + SiLU-gate)",
+            "bound": "hbm",
+            "achieved": R["w13_GBs"],
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": R["w13_GBs"] / PEAK_HBM_GBS,
+            "traffic": None,
+            "avg_launch_us": R["stage_ms"]["w13"] * 1e3,
+            "bytes_per_launch": R["w13_bytes_per_launch"],
+        },
+        "sweep": {str(T): {k: (v if not isinstance(v, float) else round(v, 4)) for k, v in r.items()}
+                  for T, r in results.items()},
+        "power": power,
+        "cpu_baseline": cpu,
+        "setup_s": round(setup_s, 1),
+    }
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

@@ -9,7 +9,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmoe_decode.so")
-SOURCES = ["route.hip", "expert.hip", "api.hip"]
+PROBE = os.path.join(PKG, "stream_probe")
+SOURCES = ["route.hip", "expert.hip", "mfma.hip", "api.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
@@ -47,7 +48,19 @@ def build(force: bool = True) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
     os.replace(tmp, LIB)
+    build_probe()
     return LIB
+
+
+def build_probe() -> str:
+    """The HBM streaming reference executable (roofline ceiling and PMC scaling)."""
+    tmp = PROBE + ".tmp"
+    r = subprocess.run([HIPCC, *FLAGS, os.path.join(CSRC, "stream_probe.hip"), "-o", tmp], capture_output=True,
+                       text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed for stream_probe.hip:\n{r.stderr}")
+    os.replace(tmp, PROBE)
+    return PROBE
 
 
 if __name__ == "__main__":

@@ -17,7 +17,7 @@ static size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 size_t carve_workspace(int H, int E, int I, int kmax, int Tmax, void *base, Workspace *ws)
 {
     const size_t P = (size_t)Tmax * kmax;  // (token, choice) pairs = slots
-    const MetaIdx mi{E};
+    const MetaIdx mi{E, max_mfma_chunks(E, Tmax, kmax)};
     size_t off = 0;
     auto take = [&](size_t bytes) {
         size_t o = off;
@@ -33,7 +33,15 @@ size_t carve_workspace(int H, int E, int I, int kmax, int Tmax, void *base, Work
     w.tok_of = (int32_t *)take(sizeof(int32_t) * P);
     w.h = (float *)take(sizeof(float) * P * I);
     w.o = (float *)take(sizeof(float) * P * H);
-    w.fb = (int32_t *)take(sizeof(int32_t) * (size_t)Tmax * E);
+    w.sync = (int32_t *)take(sizeof(int32_t) * ((size_t)Tmax + 2));
+    w.xs_hi = (uint8_t *)take((size_t)Tmax * H);
+    w.xs_lo = (uint8_t *)take((size_t)Tmax * H);
+    w.xe_hi = (uint8_t *)take((size_t)Tmax * H / 32);
+    w.xe_lo = (uint8_t *)take((size_t)Tmax * H / 32);
+    w.hs_hi = (uint8_t *)take(P * I);
+    w.hs_lo = (uint8_t *)take(P * I);
+    w.he_hi = (uint8_t *)take(P * I / 32);
+    w.he_lo = (uint8_t *)take(P * I / 32);
     w.bytes = off;
     if (ws) *ws = w;
     return off;
@@ -48,6 +56,7 @@ struct moe_decode_s {
     Layer L;
     Workspace ws;
     int mstar;  // MFMA threshold in tokens per expert (<= 0: GEMV only)
+    int synced;  // routing counters zeroed (by the first call on this handle)
     hipStream_t last_stream;
     int last_T;
     char err[256];
@@ -57,6 +66,9 @@ struct moe_decode_s {
 };
 
 static thread_local char g_init_err[256];
+
+// Experts with at least this many tokens in a step run on MFMA tiles by default.
+static const int kDefaultMfmaMinTokens = 3;
 
 #define FAIL(buf, code, ...)            \
     do {                                \
@@ -91,7 +103,6 @@ static moe_status check_config(const moe_decode_config *c, char *err)
         if (stage > 65536)
             FAIL(err, MOE_ERR_UNSUPPORTED, "activation staging of %ld bytes exceeds 64 KiB of LDS", stage);
     }
-    if (c->mfma_min_tokens > 0) FAIL(err, MOE_ERR_UNSUPPORTED, "MFMA expert tiles are not available in this build (mfma_min_tokens=%d)", c->mfma_min_tokens);
     return MOE_OK;
 }
 
@@ -144,7 +155,8 @@ moe_status moe_decode_init(const moe_decode_config *cfg, void *workspace, size_t
     h->L.expert_w_bytes = moe_decode_expert_weight_bytes(cfg);
     h->L.expert_s_bytes = moe_decode_expert_scale_bytes(cfg);
     carve_workspace(cfg->hidden, cfg->n_experts, cfg->inter, cfg->max_topk, cfg->max_tokens, workspace, &h->ws);
-    h->mstar = 0;  // GEMV only
+    h->mstar = cfg->mfma_min_tokens == 0 ? kDefaultMfmaMinTokens : (cfg->mfma_min_tokens < 0 ? 0 : cfg->mfma_min_tokens);
+    h->synced = 0;
     h->last_stream = nullptr;
     h->last_T = -1;
     h->err[0] = 0;
@@ -198,6 +210,46 @@ static void prof_mark(moe_decode_t h, int stage_boundary, hipStream_t st)
     if (h->prof_n < h->prof_cap) hipEventRecord(h->prof_ev[h->prof_n * (MOE_N_STAGES + 1) + stage_boundary], st);
 }
 
+static moe_status ensure_synced(moe_decode_t h, hipStream_t st)
+{
+    if (!h->synced) {
+        HIPCHECK(h, launch_zero(h->ws.sync, h->cfg.max_tokens + 2, st));
+        h->synced = 1;
+    }
+    return MOE_OK;
+}
+
+static RouteParams route_params(moe_decode_t h, const void *x, int T, int k, const void *router_w, const float *bias,
+                                int32_t *ids_user, float *wts_user, bool split, bool group)
+{
+    const Workspace &w = h->ws;
+    RouteParams P;
+    P.x = x;
+    P.T = T;
+    P.k = k;
+    P.router_w = router_w;
+    P.bias = bias;
+    P.logits = w.logits;
+    P.ids = w.ids;
+    P.ids_user = ids_user;
+    P.wts = w.wts;
+    P.wts_user = wts_user;
+    P.meta = w.meta;
+    P.slot_of = w.slot_of;
+    P.tok_of = w.tok_of;
+    P.cnt_tok = w.sync;
+    P.cnt_all = w.sync + h->cfg.max_tokens;
+    P.fb_acc = w.sync + h->cfg.max_tokens + 1;
+    P.xs_hi = split ? w.xs_hi : nullptr;
+    P.xs_lo = w.xs_lo;
+    P.xe_hi = w.xe_hi;
+    P.xe_lo = w.xe_lo;
+    P.mstar = h->mstar;
+    P.do_group = group ? 1 : 0;
+    P.max_chunks = max_mfma_chunks(h->L.E, h->cfg.max_tokens, h->cfg.max_topk);
+    return P;
+}
+
 moe_status moe_decode_route(moe_decode_t h, void *stream, const void *x, int32_t n_tokens, const void *router_w,
                             const float *router_bias, int32_t topk, float *logits, int32_t *topk_ids,
                             float *topk_weights)
@@ -206,11 +258,11 @@ moe_status moe_decode_route(moe_decode_t h, void *stream, const void *x, int32_t
     CHECK(check_ptr(h, logits, "logits", 4, true));
     if (n_tokens == 0) return MOE_OK;
     hipStream_t st = (hipStream_t)stream;
-    const Workspace &w = h->ws;
-    HIPCHECK(h, launch_router(h->L, x, n_tokens, router_w, router_bias, w.logits, w.fb, st));
-    HIPCHECK(h, launch_topk(h->L, w.logits, n_tokens, topk, w.ids, w.wts, topk_ids, topk_weights, st));
+    CHECK(ensure_synced(h, st));
+    const RouteParams P = route_params(h, x, n_tokens, topk, router_w, router_bias, topk_ids, topk_weights, false, false);
+    HIPCHECK(h, launch_route(h->L, P, st));
     if (logits)
-        HIPCHECK(h, hipMemcpyAsync(logits, w.logits, sizeof(float) * (size_t)n_tokens * h->L.E,
+        HIPCHECK(h, hipMemcpyAsync(logits, h->ws.logits, sizeof(float) * (size_t)n_tokens * h->L.E,
                                    hipMemcpyDeviceToDevice, st));
     return MOE_OK;
 }
@@ -232,14 +284,20 @@ moe_status moe_decode_forward(moe_decode_t h, void *stream, const void *x, int32
     const Layer &L = h->L;
     const int T = n_tokens, k = topk;
     const bool prof = h->prof_n < h->prof_cap;
+    // Expert paths this step can use: MFMA tiles for experts with >= mstar tokens
+    // (impossible when T < mstar), the GEMV path for the others (none when mstar <= 1).
+    const bool mfma = h->mstar > 0 && T >= h->mstar;
+    const bool gemv = h->mstar != 1;
+    CHECK(ensure_synced(h, st));
     if (prof) prof_mark(h, 0, st);
-    HIPCHECK(h, launch_router(L, x, T, router_w, router_bias, w.logits, w.fb, st));
-    HIPCHECK(h, launch_topk(L, w.logits, T, k, w.ids, w.wts, topk_ids, topk_weights, st));
-    HIPCHECK(h, launch_group(L, w.ids, T, k, h->mstar, w.meta, w.slot_of, w.tok_of, w.fb, st));
+    const RouteParams P = route_params(h, x, T, k, router_w, router_bias, topk_ids, topk_weights, mfma, true);
+    HIPCHECK(h, launch_route(L, P, st));
     if (prof) prof_mark(h, 1, st);
-    HIPCHECK(h, launch_w13(L, expert_w, scales, x, T, k, w.meta, w.tok_of, w.h, st));
+    if (gemv) HIPCHECK(h, launch_w13(L, expert_w, scales, x, T, k, w.meta, w.tok_of, w.h, st));
+    if (mfma) HIPCHECK(h, launch_w13_mfma(L, expert_w, scales, T, k, w.meta, w.tok_of, w, st));
     if (prof) prof_mark(h, 2, st);
-    HIPCHECK(h, launch_w2(L, expert_w, scales, T, k, w.meta, w.h, w.o, st));
+    if (gemv) HIPCHECK(h, launch_w2(L, expert_w, scales, T, k, w.meta, w.h, w.o, st));
+    if (mfma) HIPCHECK(h, launch_w2_mfma(L, expert_w, scales, T, k, w.meta, w, st));
     if (prof) prof_mark(h, 3, st);
     HIPCHECK(h, launch_combine(L, T, k, w.slot_of, w.wts, w.o, y, st));
     if (prof) {
@@ -261,7 +319,7 @@ moe_status moe_decode_get_stats(moe_decode_t h, moe_decode_stats *out, int32_t *
         return MOE_OK;
     }
     HIPCHECK(h, hipStreamSynchronize(h->last_stream));
-    const MetaIdx mi{h->L.E};
+    const MetaIdx mi{h->L.E, max_mfma_chunks(h->L.E, h->cfg.max_tokens, h->cfg.max_topk)};
     int32_t head[8];
     HIPCHECK(h, hipMemcpy(head, h->ws.meta, sizeof head, hipMemcpyDeviceToHost));
     out->n_active = head[mi.n_active()];

@@ -5,6 +5,14 @@
 // the few tokens routed to it, so these kernels are bound by HBM bandwidth (the
 // weight-read-dominated decode of the paper's Background section).  Weights stay in
 // their stored format in HBM and are dequantised in registers.
+//
+// GEMV path layout.  A work item is a tile of rows of one activated expert.  Each
+// wave owns 8 row groups of 8 lanes; a row group streams two weight rows (gate row i
+// and up row i for the gate/up projection, rows n and n+8 for the down projection),
+// lane c of the group taking one 16-byte load per block of 128 FP8 (256 E2M1)
+// inputs.  Weight loads are issued in chunks of kD blocks, double-buffered in
+// registers, and the first chunk is in flight while the expert's tokens are staged
+// in LDS.  Each weight is converted once and reused for every token of the pass.
 #include <hip/hip_runtime.h>
 #include <math.h>
 
@@ -16,9 +24,19 @@ namespace {
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kMC = 4;  // tokens per pass over a weight tile (GEMV path)
+constexpr int kD = 2;     // weight blocks per prefetch chunk
+constexpr int kMaxM = 4;  // tokens per pass over a weight tile (larger groups run on MFMA tiles)
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ inline bf16x2 as_bf16x2(uint32_t u) { return __builtin_bit_cast(bf16x2, u); }
+
+// Streaming 16-byte weight load (non-temporal: each weight is read once per step).
+__device__ inline uint4 load_stream16(const uint8_t *p)
+{
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
 
 __device__ inline uint32_t f32_to_bf16_rne(float f)
 {
@@ -30,166 +48,242 @@ __device__ inline uint32_t f32_to_bf16_rne(float f)
 // E8M0 code -> fp32 power of two (codes 0 and 255 are outside the contract).
 __device__ inline float e8m0_to_f32(uint32_t code) { return __uint_as_float(code << 23); }
 
-// 16 FP8-E4M3 weights . 16 bf16 activations -> fp32.  Conversion to bf16 is exact.
-__device__ inline float dot16_fp8_bf16(const uint4 &w, const uint4 &xa, const uint4 &xb, float p)
-{
-    const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
-    const uint32_t xd[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
+// Wait for this wave's LDS traffic, then a workgroup barrier.  Global loads still in
+// flight (the prefetched weights) are not waited for.
+__device__ inline void block_sync_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// ------------------------------------------------------------------ per-format block math
+//
+// A "block" is one lane's 16-byte load: 16 FP8 or 32 E2M1 weights.  cvt() turns it
+// into bf16 pairs (exact: E4M3 and scaled E2M1 values fit bf16) or fp32 pairs;
+// dot() multiplies the converted block with the matching staged activations.
+
+template <int FMT>
+struct Blk;
+
+template <>
+struct Blk<0> {  // FP8 E4M3, fp32 block scale applied to the partial dot
+    static constexpr int kCols = 16;
+    static constexpr int kPairs = 8;
+    __device__ static inline void cvt_bf16(const uint4 &w, float /*sc*/, uint32_t (&o)[kPairs])
+    {
+        const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        p = __builtin_amdgcn_fdot2_f32_bf16(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(wd[i], 1.0f, false),
-                                            as_bf16x2(xd[2 * i]), p, false);
-        p = __builtin_amdgcn_fdot2_f32_bf16(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(wd[i], 1.0f, true),
-                                            as_bf16x2(xd[2 * i + 1]), p, false);
+        for (int i = 0; i < 4; ++i) {
+            o[2 * i] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(wd[i], 1.0f, false));
+            o[2 * i + 1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(wd[i], 1.0f, true));
+        }
+    }
+    __device__ static inline void cvt_f32(const uint4 &w, float /*sc*/, f32x2 (&o)[kPairs])
+    {
+        const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            o[2 * i] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wd[i], 1.0f, false);
+            o[2 * i + 1] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wd[i], 1.0f, true);
+        }
+    }
+};
+
+template <>
+struct Blk<1> {  // MXFP4: E2M1 pairs, E8M0 scale applied exactly in the conversion
+    static constexpr int kCols = 32;
+    static constexpr int kPairs = 16;
+    __device__ static inline void cvt_bf16(const uint4 &w, float sc, uint32_t (&o)[kPairs])
+    {
+        const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            o[4 * i + 0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(wd[i], sc, 0));
+            o[4 * i + 1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(wd[i], sc, 1));
+            o[4 * i + 2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(wd[i], sc, 2));
+            o[4 * i + 3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(wd[i], sc, 3));
+        }
+    }
+    __device__ static inline void cvt_f32(const uint4 &w, float sc, f32x2 (&o)[kPairs])
+    {
+        const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            o[4 * i + 0] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wd[i], sc, 0);
+            o[4 * i + 1] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wd[i], sc, 1);
+            o[4 * i + 2] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wd[i], sc, 2);
+            o[4 * i + 3] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wd[i], sc, 3);
+        }
+    }
+};
+
+// Converted block . staged activations of one token (bf16 pairs in LDS).
+template <int NP>
+__device__ inline float dot_bf16(const uint32_t (&wc)[NP], const uint4 *xp)
+{
+    float p = 0.f;
+#pragma unroll
+    for (int q = 0; q < NP / 4; ++q) {
+        const uint4 xv = xp[q];
+        p = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(wc[4 * q + 0]), as_bf16x2(xv.x), p, false);
+        p = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(wc[4 * q + 1]), as_bf16x2(xv.y), p, false);
+        p = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(wc[4 * q + 2]), as_bf16x2(xv.z), p, false);
+        p = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(wc[4 * q + 3]), as_bf16x2(xv.w), p, false);
     }
     return p;
 }
 
-// 32 E2M1 weights (low nibble first) times 2^(scale) . 32 bf16 activations -> fp32.
-// The conversion applies the power-of-two scale exactly.
-__device__ inline float dot32_fp4_bf16(const uint4 &w, float sc, const uint4 (&x)[4], float p)
+// Converted block . staged activations of one token (fp32 in LDS).
+template <int NP>
+__device__ inline float dot_f32(const f32x2 (&wc)[NP], const uint4 *xp)
 {
-    const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+    float p = 0.f;
+    const float4 *x4 = reinterpret_cast<const float4 *>(xp);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const uint4 xv = x[i];
-        p = __builtin_amdgcn_fdot2_f32_bf16(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(wd[i], sc, 0), as_bf16x2(xv.x),
-                                            p, false);
-        p = __builtin_amdgcn_fdot2_f32_bf16(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(wd[i], sc, 1), as_bf16x2(xv.y),
-                                            p, false);
-        p = __builtin_amdgcn_fdot2_f32_bf16(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(wd[i], sc, 2), as_bf16x2(xv.z),
-                                            p, false);
-        p = __builtin_amdgcn_fdot2_f32_bf16(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(wd[i], sc, 3), as_bf16x2(xv.w),
-                                            p, false);
+    for (int q = 0; q < NP / 2; ++q) {
+        const float4 xv = x4[q];
+        p = fmaf(wc[2 * q].x, xv.x, p);
+        p = fmaf(wc[2 * q].y, xv.y, p);
+        p = fmaf(wc[2 * q + 1].x, xv.z, p);
+        p = fmaf(wc[2 * q + 1].y, xv.w, p);
     }
     return p;
 }
 
-__device__ inline float fma4(const f32x2 &a, const f32x2 &b, const float4 &x, float p)
-{
-    p = fmaf(a.x, x.x, p);
-    p = fmaf(a.y, x.y, p);
-    p = fmaf(b.x, x.z, p);
-    return fmaf(b.y, x.w, p);
-}
+// ------------------------------------------------------------------ two-row streaming GEMV
+//
+// State of one row group's pass over two weight rows of K inputs.
+template <int FMT>
+struct TwoRows {
+    const uint8_t *r0, *r1;  // row starts (bytes)
+    const float *fs0, *fs1;  // FP8: per-128-input scale rows (uniform over the wave)
+    const uint8_t *es0, *es1;  // MXFP4: per-32-input E8M0 rows
+    int nblk;                // K / (16*8) FP8 or K / (32*8) MXFP4 blocks per lane
+    int c;                   // lane within the row group
+};
 
-// 16 FP8 weights . 16 fp32 activations.
-__device__ inline float dot16_fp8_f32(const uint4 &w, const float4 *x, float p)
-{
-    const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-        p = fma4(__builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wd[i], 1.0f, false),
-                 __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(wd[i], 1.0f, true), x[i], p);
-    return p;
-}
+template <int FMT>
+struct Chunk {
+    uint4 w[kD][2];
+    uint32_t e[kD][2];  // MXFP4 scale codes
+};
 
-// 32 E2M1 weights times 2^(scale) . 32 fp32 activations.
-__device__ inline float dot32_fp4_f32(const uint4 &w, float sc, const float4 *x, float p)
+template <int FMT>
+__device__ inline void load_chunk(const TwoRows<FMT> &R, int b0, Chunk<FMT> &C)
 {
-    const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+    constexpr int kStride = Blk<FMT>::kCols * 8 / (FMT == 0 ? 1 : 2);  // bytes per block row-step
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        p = fma4(__builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wd[i], sc, 0),
-                 __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wd[i], sc, 1), x[2 * i], p);
-        p = fma4(__builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wd[i], sc, 2),
-                 __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(wd[i], sc, 3), x[2 * i + 1], p);
+    for (int d = 0; d < kD; ++d) {
+        const int b = min(b0 + d, R.nblk - 1);  // clamped: tail blocks are loaded, not used
+        const size_t off = (size_t)b * kStride + (size_t)R.c * 16;
+        C.w[d][0] = load_stream16(R.r0 + off);
+        C.w[d][1] = load_stream16(R.r1 + off);
+        if constexpr (FMT == 1) {
+            C.e[d][0] = R.es0[b * 8 + R.c];
+            C.e[d][1] = R.es1[b * 8 + R.c];
+        }
     }
-    return p;
 }
 
-// Two weight rows (r0, r1) of length K against up to kMC activation rows staged in
-// LDS (`xs`, row stride K elements).  A row is split over the 8 lanes of a row
-// group: lane c takes 16 FP8 (or 32 E2M1) weights = one 16-byte load per block of
-// 128 (256) inputs.  FP8 block scales are per 128 inputs and uniform over the row
-// pair (same 128-row block); E8M0 scales are per lane.
+// Apply one chunk (blocks b0 .. b0+kD-1, those below nblk) to M staged tokens.
+template <int FMT, bool AF32, int M>
+__device__ inline void apply_chunk(const TwoRows<FMT> &R, int b0, const Chunk<FMT> &C, const uint4 *xs, int xq,
+                                   float (&a0)[kMaxM], float (&a1)[kMaxM])
+{
+    constexpr int NP = Blk<FMT>::kPairs;
+    constexpr int XQ_PER_BLK = AF32 ? Blk<FMT>::kCols / 4 : Blk<FMT>::kCols / 8;  // uint4 of activations
+#pragma unroll
+    for (int d = 0; d < kD; ++d) {
+        const int b = b0 + d;
+        if (b < R.nblk) {
+            const int xoff = (b * 8 + R.c) * XQ_PER_BLK;
+            float s0 = 1.f, s1 = 1.f;
+            if constexpr (FMT == 0) {
+                s0 = R.fs0[b];
+                s1 = R.fs1[b];
+            }
+            if constexpr (AF32) {
+                f32x2 c0[NP], c1[NP];
+                Blk<FMT>::cvt_f32(C.w[d][0], FMT == 1 ? e8m0_to_f32(C.e[d][0]) : 1.f, c0);
+                Blk<FMT>::cvt_f32(C.w[d][1], FMT == 1 ? e8m0_to_f32(C.e[d][1]) : 1.f, c1);
+#pragma unroll
+                for (int m = 0; m < M; ++m) {
+                    const uint4 *xp = xs + m * xq + xoff;
+                    a0[m] = fmaf(s0, dot_f32<NP>(c0, xp), a0[m]);
+                    a1[m] = fmaf(s1, dot_f32<NP>(c1, xp), a1[m]);
+                }
+            } else {
+                uint32_t c0[NP], c1[NP];
+                Blk<FMT>::cvt_bf16(C.w[d][0], FMT == 1 ? e8m0_to_f32(C.e[d][0]) : 1.f, c0);
+                Blk<FMT>::cvt_bf16(C.w[d][1], FMT == 1 ? e8m0_to_f32(C.e[d][1]) : 1.f, c1);
+#pragma unroll
+                for (int m = 0; m < M; ++m) {
+                    const uint4 *xp = xs + m * xq + xoff;
+                    a0[m] = fmaf(s0, dot_bf16<NP>(c0, xp), a0[m]);
+                    a1[m] = fmaf(s1, dot_bf16<NP>(c1, xp), a1[m]);
+                }
+            }
+        }
+    }
+}
+
+// Stream both rows over all K for M staged tokens.  `A` holds chunk 0 on entry.
+template <int FMT, bool AF32, int M>
+__device__ inline void stream_rows(const TwoRows<FMT> &R, Chunk<FMT> &A, const uint4 *xs, int xq,
+                                   float (&a0)[kMaxM], float (&a1)[kMaxM])
+{
+    Chunk<FMT> Bc;
+    const int nch = (R.nblk + kD - 1) / kD;
+    for (int ch = 0; ch < nch; ch += 2) {
+        if (ch + 1 < nch) load_chunk<FMT>(R, (ch + 1) * kD, Bc);
+        apply_chunk<FMT, AF32, M>(R, ch * kD, A, xs, xq, a0, a1);
+        if (ch + 1 >= nch) break;
+        if (ch + 2 < nch) load_chunk<FMT>(R, (ch + 2) * kD, A);
+        apply_chunk<FMT, AF32, M>(R, (ch + 1) * kD, Bc, xs, xq, a0, a1);
+    }
+}
+
 template <int FMT, bool AF32>
-__device__ inline void gemv_rows(const uint8_t *__restrict__ r0, const uint8_t *__restrict__ r1, const void *s0p,
-                                 const void *s1p, const uint4 *__restrict__ xs, int K, int c, int mc,
-                                 float (&a0)[kMC], float (&a1)[kMC])
+__device__ inline void stream_rows_m(int m, const TwoRows<FMT> &R, Chunk<FMT> &A, const uint4 *xs, int xq,
+                                     float (&a0)[kMaxM], float (&a1)[kMaxM])
 {
-    const int xq = AF32 ? K / 4 : K / 8;  // uint4 per staged activation row
-    if constexpr (FMT == 0) {
-        const float *s0 = (const float *)s0p, *s1 = (const float *)s1p;
-        const int KB = K / 128;
-#pragma unroll 4
-        for (int kb = 0; kb < KB; ++kb) {
-            const int col = kb * 128 + c * 16;
-            const uint4 w0 = *reinterpret_cast<const uint4 *>(r0 + col);
-            const uint4 w1 = *reinterpret_cast<const uint4 *>(r1 + col);
-            const float sc0 = s0[kb], sc1 = s1[kb];
+    switch (m) {
+    case 1: stream_rows<FMT, AF32, 1>(R, A, xs, xq, a0, a1); break;
+    case 2: stream_rows<FMT, AF32, 2>(R, A, xs, xq, a0, a1); break;
+    case 3: stream_rows<FMT, AF32, 3>(R, A, xs, xq, a0, a1); break;
+    default: stream_rows<FMT, AF32, 4>(R, A, xs, xq, a0, a1); break;
+    }
+}
+
+__device__ inline void reduce_row_group(float (&a)[kMaxM], int m)
+{
 #pragma unroll
-            for (int m = 0; m < kMC; ++m) {
-                if (m < mc) {
-                    float p0, p1;
-                    if constexpr (AF32) {
-                        const float4 *xv = reinterpret_cast<const float4 *>(xs + m * xq + col / 4);
-                        p0 = dot16_fp8_f32(w0, xv, 0.f);
-                        p1 = dot16_fp8_f32(w1, xv, 0.f);
-                    } else {
-                        const uint4 xa = xs[m * xq + col / 8], xb = xs[m * xq + col / 8 + 1];
-                        p0 = dot16_fp8_bf16(w0, xa, xb, 0.f);
-                        p1 = dot16_fp8_bf16(w1, xa, xb, 0.f);
-                    }
-                    a0[m] = fmaf(sc0, p0, a0[m]);
-                    a1[m] = fmaf(sc1, p1, a1[m]);
-                }
-            }
-        }
-    } else {
-        const uint8_t *s0 = (const uint8_t *)s0p, *s1 = (const uint8_t *)s1p;
-        const int KB = K / 256;
-#pragma unroll 4
-        for (int kb = 0; kb < KB; ++kb) {
-            const int col = kb * 256 + c * 32;
-            const uint4 w0 = *reinterpret_cast<const uint4 *>(r0 + col / 2);
-            const uint4 w1 = *reinterpret_cast<const uint4 *>(r1 + col / 2);
-            const float sc0 = e8m0_to_f32(s0[kb * 8 + c]), sc1 = e8m0_to_f32(s1[kb * 8 + c]);
-#pragma unroll
-            for (int m = 0; m < kMC; ++m) {
-                if (m < mc) {
-                    if constexpr (AF32) {
-                        const float4 *xv = reinterpret_cast<const float4 *>(xs + m * xq + col / 4);
-                        a0[m] = dot32_fp4_f32(w0, sc0, xv, a0[m]);
-                        a1[m] = dot32_fp4_f32(w1, sc1, xv, a1[m]);
-                    } else {
-                        const uint4 xv[4] = {xs[m * xq + col / 8], xs[m * xq + col / 8 + 1],
-                                             xs[m * xq + col / 8 + 2], xs[m * xq + col / 8 + 3]};
-                        a0[m] = dot32_fp4_bf16(w0, sc0, xv, a0[m]);
-                        a1[m] = dot32_fp4_bf16(w1, sc1, xv, a1[m]);
-                    }
-                }
-            }
+    for (int j = 0; j < kMaxM; ++j) {
+        if (j < m) {
+            a[j] += __shfl_xor(a[j], 1);
+            a[j] += __shfl_xor(a[j], 2);
+            a[j] += __shfl_xor(a[j], 4);
         }
     }
 }
 
-__device__ inline void reduce_row_group(float (&a)[kMC])
-{
-#pragma unroll
-    for (int m = 0; m < kMC; ++m) {
-        a[m] += __shfl_xor(a[m], 1);
-        a[m] += __shfl_xor(a[m], 2);
-        a[m] += __shfl_xor(a[m], 4);
-    }
-}
+constexpr int kXR = 4;   // activation uint4 held per thread while the weights are in flight
 
 // ------------------------------------------------------------------ gate/up + SiLU-gate
 //
-// Work item = (active expert, tile of 32 consecutive intermediate rows).  A 256-thread
-// workgroup = 4 waves x 8 row groups; row group rg of wave w owns intermediate row
-// i = 32*tile + 8*w + rg and streams both its gate row and its up row, so the epilogue
-// h_i = silu(g_i) * u_i needs no data exchange.  Tokens are staged in LDS kMC at a
-// time.  Items are spread over the grid with a grid stride.
-template <int FMT, bool AF32>
-__global__ __launch_bounds__(256) void w13_gemv_kernel(const uint8_t *__restrict__ ew, const uint8_t *__restrict__ es,
-                                                       const void *__restrict__ x, const int32_t *__restrict__ meta,
-                                                       const int32_t *__restrict__ tok_of, float *__restrict__ hbuf,
-                                                       int H, int I, int E, size_t ewb, size_t esb)
+// Work item = (active expert, tile of 8*WAVES intermediate rows).  Row group rg of
+// wave w owns row i = tile*8*WAVES + 8w + rg and streams its gate and up rows, so the
+// epilogue h_i = silu(g_i) * u_i needs no data exchange.
+template <int FMT, bool AF32, int WAVES>
+__global__ __launch_bounds__(WAVES * 64) void w13_gemv_kernel(const uint8_t *__restrict__ ew,
+                                                              const uint8_t *__restrict__ es,
+                                                              const void *__restrict__ x,
+                                                              const int32_t *__restrict__ meta,
+                                                              const int32_t *__restrict__ tok_of,
+                                                              float *__restrict__ hbuf, int H, int I, int E,
+                                                              size_t ewb, size_t esb, int mmax)
 {
+    constexpr int NTH = WAVES * 64;
+    constexpr int ROWS = 8 * WAVES;
     extern __shared__ uint4 lds4[];
     const MetaIdx mi{E};
-    const int tiles = I / 32;
+    const int tiles = I / ROWS;
     const int n_items = meta[mi.n_gemv()] * tiles;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63, rg = lane >> 3, c = lane & 7;
@@ -198,41 +292,64 @@ __global__ __launch_bounds__(256) void w13_gemv_kernel(const uint8_t *__restrict
     const size_t rowb = FMT == 0 ? (size_t)H : (size_t)H / 2;
 
     for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
-        const int e = meta[mi.act_gemv() + item / tiles];
+        const int4 rec = reinterpret_cast<const int4 *>(meta + mi.gemv_rec())[item / tiles];
+        const int e = rec.x, s0 = rec.y, M = rec.z;
         const int tile = item % tiles;
-        const int s0 = meta[mi.offsets() + e];
-        const int M = meta[mi.offsets() + e + 1] - s0;
-        const int ibase = tile * 32 + wave * 8;
+        const int ibase = tile * ROWS + wave * 8;
         const int i = ibase + rg;
         const uint8_t *we = ew + (size_t)e * ewb;
         const uint8_t *se = es + (size_t)e * esb;
-        const uint8_t *r0 = we + (size_t)i * rowb;
-        const uint8_t *r1 = we + (size_t)(I + i) * rowb;
-        const void *sg, *su;
+        TwoRows<FMT> R;
+        R.r0 = we + (size_t)i * rowb;
+        R.r1 = we + (size_t)(I + i) * rowb;
+        R.c = c;
+        R.nblk = FMT == 0 ? H / 128 : H / 256;
         if constexpr (FMT == 0) {
-            const float *sf = (const float *)se + (size_t)(ibase / 128) * (H / 128);
-            sg = sf;
-            su = sf + (size_t)(I / 128) * (H / 128);
+            R.fs0 = (const float *)se + (size_t)(ibase / 128) * (H / 128);
+            R.fs1 = R.fs0 + (size_t)(I / 128) * (H / 128);
         } else {
-            sg = se + (size_t)i * (H / 32);
-            su = se + (size_t)(I + i) * (H / 32);
+            R.es0 = se + (size_t)i * (H / 32);
+            R.es1 = se + (size_t)(I + i) * (H / 32);
         }
-        for (int m0 = 0; m0 < M; m0 += kMC) {
-            const int mc = min(kMC, M - m0);
-            __syncthreads();
-            for (int q = threadIdx.x; q < mc * xq; q += blockDim.x) {
-                const int m = q / xq, qq = q % xq;
-                const int t = tok_of[s0 + m0 + m];
-                lds4[q] = reinterpret_cast<const uint4 *>((const uint8_t *)x + (size_t)t * H * act_bytes)[qq];
+        for (int m0 = 0; m0 < M; m0 += mmax) {
+            const int mc = min(mmax, M - m0);
+            // token rows of this pass (uniform scalar loads), then their activations
+            // into registers, then the first weight chunk, then LDS: the activation
+            // wait leaves the weight loads in flight.
+            int tk[kMaxM];
+#pragma unroll
+            for (int m = 0; m < kMaxM; ++m) tk[m] = m < mc ? tok_of[s0 + m0 + m] : 0;
+            const int total = mc * xq;
+            Chunk<FMT> A;
+            for (int r0 = 0; r0 < total; r0 += kXR * NTH) {
+                uint4 xv[kXR];
+#pragma unroll
+                for (int u = 0; u < kXR; ++u) {
+                    const int q = r0 + u * NTH + (int)threadIdx.x;
+                    if (q < total) {
+                        const int m = q / xq;
+                        int t = tk[0];
+#pragma unroll
+                        for (int j = 1; j < kMaxM; ++j) t = m == j ? tk[j] : t;
+                        xv[u] = reinterpret_cast<const uint4 *>((const uint8_t *)x + (size_t)t * H * act_bytes)[q - m * xq];
+                    }
+                }
+                if (r0 == 0) load_chunk<FMT>(R, 0, A);
+                block_sync_lds();  // the previous pass is done reading LDS
+#pragma unroll
+                for (int u = 0; u < kXR; ++u) {
+                    const int q = r0 + u * NTH + (int)threadIdx.x;
+                    if (q < total) lds4[q] = xv[u];
+                }
             }
-            __syncthreads();
-            float a0[kMC] = {}, a1[kMC] = {};
-            gemv_rows<FMT, AF32>(r0, r1, sg, su, lds4, H, c, mc, a0, a1);
-            reduce_row_group(a0);
-            reduce_row_group(a1);
+            block_sync_lds();
+            float a0[kMaxM] = {}, a1[kMaxM] = {};
+            stream_rows_m<FMT, AF32>(mc, R, A, lds4, xq, a0, a1);
+            reduce_row_group(a0, mc);
+            reduce_row_group(a1, mc);
             if (c == 0) {
 #pragma unroll
-                for (int m = 0; m < kMC; ++m)
+                for (int m = 0; m < kMaxM; ++m)
                     if (m < mc) {
                         const float g = a0[m], u = a1[m];
                         hbuf[(size_t)(s0 + m0 + m) * I + i] = g / (1.0f + expf(-g)) * u;
@@ -244,18 +361,22 @@ __global__ __launch_bounds__(256) void w13_gemv_kernel(const uint8_t *__restrict
 
 // ------------------------------------------------------------------ down projection
 //
-// Work item = (active expert, tile of 64 output rows).  Row group rg of wave w owns
-// rows n0 = 64*tile + 16*w + rg and n0 + 8.  The expert's SwiGLU activations are
-// staged in LDS (rounded to bf16 for bf16 layers, fp32 otherwise).
-template <int FMT, bool AF32>
-__global__ __launch_bounds__(256) void w2_gemv_kernel(const uint8_t *__restrict__ ew, const uint8_t *__restrict__ es,
-                                                      const int32_t *__restrict__ meta,
-                                                      const float *__restrict__ hbuf, float *__restrict__ obuf, int H,
-                                                      int I, int E, size_t ewb, size_t esb)
+// Work item = (active expert, tile of 16*WAVES output rows).  Row group rg of wave w
+// owns rows n0 = tile*16*WAVES + 16w + rg and n0 + 8.  The expert's SwiGLU
+// activations are staged in LDS (rounded to bf16 for bf16 layers, fp32 otherwise).
+template <int FMT, bool AF32, int WAVES>
+__global__ __launch_bounds__(WAVES * 64) void w2_gemv_kernel(const uint8_t *__restrict__ ew,
+                                                             const uint8_t *__restrict__ es,
+                                                             const int32_t *__restrict__ meta,
+                                                             const float *__restrict__ hbuf,
+                                                             float *__restrict__ obuf, int H, int I, int E, size_t ewb,
+                                                             size_t esb, int mmax)
 {
+    constexpr int NTH = WAVES * 64;
+    constexpr int ROWS = 16 * WAVES;
     extern __shared__ uint4 lds4[];
     const MetaIdx mi{E};
-    const int tiles = H / 64;
+    const int tiles = H / ROWS;
     const int n_items = meta[mi.n_gemv()] * tiles;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63, rg = lane >> 3, c = lane & 7;
@@ -264,51 +385,71 @@ __global__ __launch_bounds__(256) void w2_gemv_kernel(const uint8_t *__restrict_
     const size_t w2off = FMT == 0 ? (size_t)2 * I * H : (size_t)I * H;
 
     for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
-        const int e = meta[mi.act_gemv() + item / tiles];
+        const int4 rec = reinterpret_cast<const int4 *>(meta + mi.gemv_rec())[item / tiles];
+        const int e = rec.x, s0 = rec.y, M = rec.z;
         const int tile = item % tiles;
-        const int s0 = meta[mi.offsets() + e];
-        const int M = meta[mi.offsets() + e + 1] - s0;
-        const int nbase = tile * 64 + wave * 16;
+        const int nbase = tile * ROWS + wave * 16;
         const int n0 = nbase + rg, n1 = n0 + 8;
         const uint8_t *we = ew + (size_t)e * ewb + w2off;
         const uint8_t *se = es + (size_t)e * esb;
-        const uint8_t *r0 = we + (size_t)n0 * rowb;
-        const uint8_t *r1 = we + (size_t)n1 * rowb;
-        const void *sa, *sb;
+        TwoRows<FMT> R;
+        R.r0 = we + (size_t)n0 * rowb;
+        R.r1 = we + (size_t)n1 * rowb;
+        R.c = c;
+        R.nblk = FMT == 0 ? I / 128 : I / 256;
         if constexpr (FMT == 0) {
-            const float *sf = (const float *)se + (size_t)2 * (I / 128) * (H / 128) + (size_t)(nbase / 128) * (I / 128);
-            sa = sf;
-            sb = sf;
+            R.fs0 = (const float *)se + (size_t)2 * (I / 128) * (H / 128) + (size_t)(nbase / 128) * (I / 128);
+            R.fs1 = R.fs0;
         } else {
             const uint8_t *sd = se + (size_t)2 * I * (H / 32);
-            sa = sd + (size_t)n0 * (I / 32);
-            sb = sd + (size_t)n1 * (I / 32);
+            R.es0 = sd + (size_t)n0 * (I / 32);
+            R.es1 = sd + (size_t)n1 * (I / 32);
         }
-        for (int m0 = 0; m0 < M; m0 += kMC) {
-            const int mc = min(kMC, M - m0);
-            __syncthreads();
-            for (int q = threadIdx.x; q < mc * xq; q += blockDim.x) {
-                const int m = q / xq, qq = q % xq;
-                const float *hr = hbuf + (size_t)(s0 + m0 + m) * I;
-                if constexpr (AF32) {
-                    lds4[q] = reinterpret_cast<const uint4 *>(hr)[qq];
-                } else {
-                    const float4 a = reinterpret_cast<const float4 *>(hr)[2 * qq];
-                    const float4 b = reinterpret_cast<const float4 *>(hr)[2 * qq + 1];
-                    lds4[q] = make_uint4(f32_to_bf16_rne(a.x) | (f32_to_bf16_rne(a.y) << 16),
-                                         f32_to_bf16_rne(a.z) | (f32_to_bf16_rne(a.w) << 16),
-                                         f32_to_bf16_rne(b.x) | (f32_to_bf16_rne(b.y) << 16),
-                                         f32_to_bf16_rne(b.z) | (f32_to_bf16_rne(b.w) << 16));
+        for (int m0 = 0; m0 < M; m0 += mmax) {
+            const int mc = min(mmax, M - m0);
+            const float *hb = hbuf + (size_t)(s0 + m0) * I;  // the pass's slots are consecutive
+            const int total = mc * xq;
+            Chunk<FMT> A;
+            for (int r0 = 0; r0 < total; r0 += (kXR / 2) * NTH) {
+                float4 hv[kXR];  // AF32: one float4 per staged uint4; bf16: two
+#pragma unroll
+                for (int u = 0; u < kXR / 2; ++u) {
+                    const int q = r0 + u * NTH + (int)threadIdx.x;
+                    if (q < total) {
+                        if constexpr (AF32) {
+                            hv[u] = reinterpret_cast<const float4 *>(hb)[q];
+                        } else {
+                            hv[2 * u] = reinterpret_cast<const float4 *>(hb)[2 * q];
+                            hv[2 * u + 1] = reinterpret_cast<const float4 *>(hb)[2 * q + 1];
+                        }
+                    }
+                }
+                if (r0 == 0) load_chunk<FMT>(R, 0, A);
+                block_sync_lds();
+#pragma unroll
+                for (int u = 0; u < kXR / 2; ++u) {
+                    const int q = r0 + u * NTH + (int)threadIdx.x;
+                    if (q < total) {
+                        if constexpr (AF32) {
+                            lds4[q] = __builtin_bit_cast(uint4, hv[u]);
+                        } else {
+                            const float4 a = hv[2 * u], b = hv[2 * u + 1];
+                            lds4[q] = make_uint4(f32_to_bf16_rne(a.x) | (f32_to_bf16_rne(a.y) << 16),
+                                                 f32_to_bf16_rne(a.z) | (f32_to_bf16_rne(a.w) << 16),
+                                                 f32_to_bf16_rne(b.x) | (f32_to_bf16_rne(b.y) << 16),
+                                                 f32_to_bf16_rne(b.z) | (f32_to_bf16_rne(b.w) << 16));
+                        }
+                    }
                 }
             }
-            __syncthreads();
-            float a0[kMC] = {}, a1[kMC] = {};
-            gemv_rows<FMT, AF32>(r0, r1, sa, sb, lds4, I, c, mc, a0, a1);
-            reduce_row_group(a0);
-            reduce_row_group(a1);
+            block_sync_lds();
+            float a0[kMaxM] = {}, a1[kMaxM] = {};
+            stream_rows_m<FMT, AF32>(mc, R, A, lds4, xq, a0, a1);
+            reduce_row_group(a0, mc);
+            reduce_row_group(a1, mc);
             if (c == 0) {
 #pragma unroll
-                for (int m = 0; m < kMC; ++m)
+                for (int m = 0; m < kMaxM; ++m)
                     if (m < mc) {
                         obuf[(size_t)(s0 + m0 + m) * H + n0] = a0[m];
                         obuf[(size_t)(s0 + m0 + m) * H + n1] = a1[m];
@@ -349,7 +490,18 @@ __global__ __launch_bounds__(256) void combine_kernel(int k, int H, const int32_
     }
 }
 
-int grid_for(int items_upper_bound) { return items_upper_bound < 1 ? 1 : (items_upper_bound > 16384 ? 16384 : items_upper_bound); }
+int grid_for(long items) { return items < 1 ? 1 : (items > 65535 ? 65535 : (int)items); }
+
+// Tokens per pass: as many as fit 64 KiB of LDS, at most kMaxM.
+int tokens_per_pass(int K, int act_bytes)
+{
+    int m = 65536 / (K * act_bytes);
+    return m < 1 ? 1 : (m > kMaxM ? kMaxM : m);
+}
+
+// Two waves per item while few tokens share an expert (more, smaller items balance
+// the CUs when only a handful of experts is active), four otherwise.
+int waves_for(int T, int k, int E) { return (long)T * k <= 2L * E ? 2 : 4; }
 
 }  // namespace
 
@@ -357,16 +509,20 @@ hipError_t launch_w13(const Layer &L, const void *expert_w, const void *scales, 
                       const int32_t *meta, const int32_t *tok_of, float *h, hipStream_t st)
 {
     const int max_active = T * k < L.E ? T * k : L.E;
-    dim3 grid(grid_for(max_active * (L.I / 32))), block(256);
-    const size_t lds = (size_t)kMC * L.H * (L.act_bf16 ? 2 : 4);
+    const int ab = L.act_bf16 ? 2 : 4;
+    const int mmax = tokens_per_pass(L.H, ab);
+    const size_t lds = (size_t)mmax * L.H * ab;
     const uint8_t *ew = (const uint8_t *)expert_w, *es = (const uint8_t *)scales;
-#define W13(F, A) \
-    w13_gemv_kernel<F, A><<<grid, block, lds, st>>>(ew, es, x, meta, tok_of, h, L.H, L.I, L.E, L.expert_w_bytes, \
-                                                     L.expert_s_bytes)
+    const int waves = waves_for(T, k, L.E);
+#define W13(F, A, WV)                                                                                        \
+    w13_gemv_kernel<F, A, WV><<<grid_for((long)max_active * (L.I / (8 * WV))), WV * 64, lds, st>>>(          \
+        ew, es, x, meta, tok_of, h, L.H, L.I, L.E, L.expert_w_bytes, L.expert_s_bytes, mmax)
+#define W13W(F, A) (waves == 2 ? (W13(F, A, 2)) : (W13(F, A, 4)))
     if (L.wfmt == 0)
-        L.act_bf16 ? W13(0, false) : W13(0, true);
+        L.act_bf16 ? W13W(0, false) : W13W(0, true);
     else
-        L.act_bf16 ? W13(1, false) : W13(1, true);
+        L.act_bf16 ? W13W(1, false) : W13W(1, true);
+#undef W13W
 #undef W13
     return hipGetLastError();
 }
@@ -375,15 +531,20 @@ hipError_t launch_w2(const Layer &L, const void *expert_w, const void *scales, i
                      const float *h, float *o, hipStream_t st)
 {
     const int max_active = T * k < L.E ? T * k : L.E;
-    dim3 grid(grid_for(max_active * (L.H / 64))), block(256);
-    const size_t lds = (size_t)kMC * L.I * (L.act_bf16 ? 2 : 4);
+    const int ab = L.act_bf16 ? 2 : 4;
+    const int mmax = tokens_per_pass(L.I, ab);
+    const size_t lds = (size_t)mmax * L.I * ab;
     const uint8_t *ew = (const uint8_t *)expert_w, *es = (const uint8_t *)scales;
-#define W2(F, A) \
-    w2_gemv_kernel<F, A><<<grid, block, lds, st>>>(ew, es, meta, h, o, L.H, L.I, L.E, L.expert_w_bytes, L.expert_s_bytes)
+    const int waves = waves_for(T, k, L.E);
+#define W2(F, A, WV)                                                                                          \
+    w2_gemv_kernel<F, A, WV><<<grid_for((long)max_active * (L.H / (16 * WV))), WV * 64, lds, st>>>(           \
+        ew, es, meta, h, o, L.H, L.I, L.E, L.expert_w_bytes, L.expert_s_bytes, mmax)
+#define W2W(F, A) (waves == 2 ? (W2(F, A, 2)) : (W2(F, A, 4)))
     if (L.wfmt == 0)
-        L.act_bf16 ? W2(0, false) : W2(0, true);
+        L.act_bf16 ? W2W(0, false) : W2W(0, true);
     else
-        L.act_bf16 ? W2(1, false) : W2(1, true);
+        L.act_bf16 ? W2W(1, false) : W2W(1, true);
+#undef W2W
 #undef W2
     return hipGetLastError();
 }

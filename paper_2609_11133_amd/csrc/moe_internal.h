@@ -15,25 +15,38 @@ struct Workspace {
     int32_t *meta;     // Meta block, see MetaIdx
     int32_t *slot_of;  // [Tmax*kmax] slot of pair (t, j)
     int32_t *tok_of;   // [Tmax*kmax] token of slot
-    float *h;          // [Tmax*kmax][I] SwiGLU activations per slot
+    float *h;          // [Tmax*kmax][I] SwiGLU activations per slot (GEMV path)
     float *o;          // [Tmax*kmax][H] expert outputs per slot
-    int32_t *fb;       // [Tmax][E] 1 where a router logit took the exact fallback path
+    int32_t *sync;     // [Tmax + 2] routing counters (zero between launches)
+    uint8_t *xs_hi, *xs_lo;  // [Tmax][H] 2-term FP8 split of x (MFMA path)
+    uint8_t *xe_hi, *xe_lo;  // [Tmax][H/32] E8M0 exponents of the split
+    uint8_t *hs_hi, *hs_lo;  // [Tmax*kmax][I] 2-term FP8 split of h (MFMA path)
+    uint8_t *he_hi, *he_lo;  // [Tmax*kmax][I/32]
     size_t bytes;
 };
 
-// Layout of the meta block (int32 words).  Offsets depend on E.
+// Layout of the meta block (int32 words).  Records are int4 and start on 16-byte
+// boundaries: GEMV records {expert, first slot, tokens, 0}; MFMA chunk records
+// {expert, first slot of the chunk, tokens in the chunk (<= 32), 0}, one per 32
+// tokens of an MFMA expert.
 struct MetaIdx {
     int E;
+    int max_chunks;  // E + ceil(Tmax * kmax / 32) bounds the number of MFMA chunks
     __host__ __device__ int n_active() const { return 0; }
     __host__ __device__ int n_gemv() const { return 1; }
     __host__ __device__ int n_mfma() const { return 2; }
     __host__ __device__ int n_fallback() const { return 3; }
-    __host__ __device__ int counts() const { return 8; }                 // [E]
-    __host__ __device__ int offsets() const { return 8 + E; }            // [E+1]
-    __host__ __device__ int act_gemv() const { return 8 + 2 * E + 1; }   // [E]
-    __host__ __device__ int act_mfma() const { return 8 + 3 * E + 1; }   // [E]
-    __host__ __device__ int words() const { return 8 + 4 * E + 1; }
+    __host__ __device__ int n_mfma_chunks() const { return 4; }
+    __host__ __device__ int counts() const { return 8; }        // [E]
+    __host__ __device__ int offsets() const { return 8 + E; }   // [E+1]
+    __host__ __device__ int gemv_rec() const { return ((8 + 2 * E + 1) + 3) & ~3; }  // int4 [E]
+    __host__ __device__ int chunk_rec() const { return gemv_rec() + 4 * E; }         // int4 [max_chunks]
+    __host__ __device__ int words() const { return chunk_rec() + 4 * max_chunks; }
 };
+
+__host__ __device__ inline int max_mfma_chunks(int E, int Tmax, int kmax) { return E + (Tmax * kmax + 31) / 32; }
+
+constexpr int kMfmaChunk = 32;  // tokens per MFMA pass (two 16-column tiles)
 
 size_t carve_workspace(int H, int E, int I, int kmax, int Tmax, void *base, Workspace *ws);
 
@@ -47,17 +60,33 @@ struct Layer {
     size_t expert_s_bytes;  // per expert
 };
 
+struct RouteParams {
+    const void *x;
+    int T, k;
+    const void *router_w;
+    const float *bias;
+    float *logits;
+    int32_t *ids, *ids_user;
+    float *wts, *wts_user;
+    int32_t *meta, *slot_of, *tok_of;
+    int32_t *cnt_tok, *cnt_all, *fb_acc;
+    uint8_t *xs_hi, *xs_lo, *xe_hi, *xe_lo;  // NULL: no activation split
+    int mstar;
+    int do_group;
+    int max_chunks;
+};
+
 // ---- launchers (all enqueue on `st`, return hipGetLastError())
-hipError_t launch_router(const Layer &L, const void *x, int T, const void *router_w, const float *bias,
-                         float *logits, int32_t *fb_flags, hipStream_t st);
-hipError_t launch_topk(const Layer &L, const float *logits, int T, int k, int32_t *ids, float *wts,
-                       int32_t *ids_user, float *wts_user, hipStream_t st);
-hipError_t launch_group(const Layer &L, const int32_t *ids, int T, int k, int mstar, int32_t *meta,
-                        int32_t *slot_of, int32_t *tok_of, const int32_t *fb_flags, hipStream_t st);
+hipError_t launch_zero(int32_t *p, int n, hipStream_t st);
+hipError_t launch_route(const Layer &L, const RouteParams &P, hipStream_t st);
 hipError_t launch_w13(const Layer &L, const void *expert_w, const void *scales, const void *x, int T, int k,
                       const int32_t *meta, const int32_t *tok_of, float *h, hipStream_t st);
 hipError_t launch_w2(const Layer &L, const void *expert_w, const void *scales, int T, int k, const int32_t *meta,
                      const float *h, float *o, hipStream_t st);
+hipError_t launch_w13_mfma(const Layer &L, const void *expert_w, const void *scales, int T, int k,
+                           const int32_t *meta, const int32_t *tok_of, const Workspace &ws, hipStream_t st);
+hipError_t launch_w2_mfma(const Layer &L, const void *expert_w, const void *scales, int T, int k,
+                          const int32_t *meta, const Workspace &ws, hipStream_t st);
 hipError_t launch_combine(const Layer &L, int T, int k, const int32_t *slot_of, const float *wts, const float *o,
                           void *y, hipStream_t st);
 

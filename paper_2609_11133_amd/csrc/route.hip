@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <math.h>
 
+#include "fp8split.h"
 #include "moe_internal.h"
 
 namespace moe {
@@ -91,78 +92,61 @@ __device__ inline void load8<float>(const float *p, double (&v)[8])
     v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
 }
 
-// One wave per (token, group of `epw` experts).
+// Canonical logit of token row xr against router row wrow, computed by one wave.
+// Every lane returns the same value; *fallback is set when the exact path ran.
 template <typename XT, typename WT>
-__global__ __launch_bounds__(256) void router_logits_kernel(const XT *__restrict__ x, const WT *__restrict__ wr,
-                                                            const float *__restrict__ bias, float *__restrict__ logits,
-                                                            int32_t *__restrict__ fb_flags, int T, int E, int H,
-                                                            int epw)
+__device__ inline float wave_logit(const XT *__restrict__ xr, const WT *__restrict__ wrow, const float *bias_e, int H,
+                                   int lane, int &fallback)
 {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
-    const int groups = (E + epw - 1) / epw;
-    const int t = wave / groups;
-    if (t >= T) return;
-    const int e0 = (wave % groups) * epw;
-    const int e1 = min(E, e0 + epw);
-    const XT *xr = x + (size_t)t * H;
     const int per_lane = ((H + 511) / 512) * 8;
     const double gamma = (double)(per_lane + 6 + 1 + 2) * 0x1p-52;  // >= 2 gamma_D
-
-    for (int e = e0; e < e1; ++e) {
-        const WT *wrow = wr + (size_t)e * H;
-        double s = 0.0, a = 0.0;
+    double s = 0.0, a = 0.0;
+    for (int h = lane * 8; h < H; h += 512) {
+        double xv[8], wv[8];
+        load8<XT>(xr + h, xv);
+        load8<WT>(wrow + h, wv);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            s = fma(xv[i], wv[i], s);
+            a = fma(fabs(xv[i]), fabs(wv[i]), a);
+        }
+    }
+#pragma unroll
+    for (int o = kWave / 2; o >= 1; o >>= 1) {
+        s += __shfl_xor(s, o);
+        a += __shfl_xor(a, o);
+    }
+    const double b = bias_e ? (double)*bias_e : 0.0;
+    float r;
+    fallback = 0;
+    if (!certain_f32(s + b, gamma * (a + fabs(b)), r)) {
+        // Exact path: error-free accumulation of the same (exact) products.
+        double hi = 0.0, lo = 0.0;
         for (int h = lane * 8; h < H; h += 512) {
             double xv[8], wv[8];
             load8<XT>(xr + h, xv);
             load8<WT>(wrow + h, wv);
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                s = fma(xv[i], wv[i], s);
-                a = fma(fabs(xv[i]), fabs(wv[i]), a);
+                double p = xv[i] * wv[i], ss, ee;
+                two_sum(hi, p, ss, ee);
+                hi = ss;
+                lo += ee;
             }
         }
+        double nh = hi + lo;  // normalise the lane's pair before combining
+        lo = lo - (nh - hi);
+        hi = nh;
 #pragma unroll
         for (int o = kWave / 2; o >= 1; o >>= 1) {
-            s += __shfl_xor(s, o);
-            a += __shfl_xor(a, o);
+            double h2 = __shfl_xor(hi, o), l2 = __shfl_xor(lo, o);
+            dd_add(hi, lo, h2, l2);
         }
-        const double b = bias ? (double)bias[e] : 0.0;
-        const double v = s + b;
-        float r;
-        int fallback = 0;
-        if (!certain_f32(v, gamma * (a + fabs(b)), r)) {
-            // Exact path: error-free accumulation of the same (exact) products.
-            double hi = 0.0, lo = 0.0;
-            for (int h = lane * 8; h < H; h += 512) {
-                double xv[8], wv[8];
-                load8<XT>(xr + h, xv);
-                load8<WT>(wrow + h, wv);
-#pragma unroll
-                for (int i = 0; i < 8; ++i) {
-                    double p = xv[i] * wv[i], ss, ee;
-                    two_sum(hi, p, ss, ee);
-                    hi = ss;
-                    lo += ee;
-                }
-            }
-            double nh = hi + lo;  // normalise the lane's pair before combining
-            lo = lo - (nh - hi);
-            hi = nh;
-#pragma unroll
-            for (int o = kWave / 2; o >= 1; o >>= 1) {
-                double h2 = __shfl_xor(hi, o), l2 = __shfl_xor(lo, o);
-                dd_add(hi, lo, h2, l2);
-            }
-            dd_add(hi, lo, b, 0.0);
-            r = round_dd_to_f32(hi, lo);
-            fallback = 1;
-        }
-        if (lane == 0) {
-            logits[(size_t)t * E + e] = r + 0.0f;  // -0 -> +0
-            if (fb_flags) fb_flags[(size_t)t * E + e] = fallback;
-        }
+        dd_add(hi, lo, b, 0.0);
+        r = round_dd_to_f32(hi, lo);
+        fallback = 1;
     }
+    return r + 0.0f;  // -0 -> +0
 }
 
 // ------------------------------------------------------------------ top-k softmax
@@ -184,31 +168,26 @@ __device__ inline float from_ordered(uint32_t o) { return __uint_as_float((o & 0
 
 constexpr int kMaxKeysPerLane = 16;  // E <= 1024
 
-__global__ __launch_bounds__(256) void topk_softmax_kernel(const float *__restrict__ logits, int T, int E, int k,
-                                                           int32_t *__restrict__ ids, float *__restrict__ wts,
-                                                           int32_t *__restrict__ ids_user, float *__restrict__ wts_user)
+__device__ inline void wave_topk(const float *__restrict__ l, int E, int k, int lane, int32_t *ids, float *wts,
+                                 int32_t *ids_user, float *wts_user)
 {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int t = blockIdx.x * (blockDim.x / kWave) + (threadIdx.x / kWave);
-    if (t >= T) return;
-    const float *l = logits + (size_t)t * E;
     uint64_t key[kMaxKeysPerLane];
     const int nk = (E + kWave - 1) / kWave;
 #pragma unroll
     for (int c = 0; c < kMaxKeysPerLane; ++c) {
-        int e = lane + c * kWave;
+        const int e = lane + c * kWave;
         key[c] = (c < nk && e < E) ? (((uint64_t)ordered_bits(l[e]) << 32) | (uint32_t)(~(uint32_t)e)) : 0ull;
     }
-    float top_l = 0.f, denom = 0.f;
-    float my_l = 0.f;
+    float top_l = 0.f, denom = 0.f, my_p = 0.f;
     int my_e = 0;
     for (int j = 0; j < k; ++j) {
         uint64_t best = 0;
 #pragma unroll
-        for (int c = 0; c < kMaxKeysPerLane; ++c) best = key[c] > best ? key[c] : best;
+        for (int c = 0; c < kMaxKeysPerLane; ++c)
+            if (c < nk) best = key[c] > best ? key[c] : best;
 #pragma unroll
         for (int o = kWave / 2; o >= 1; o >>= 1) {
-            uint64_t other = __shfl_xor(best, o);
+            const uint64_t other = __shfl_xor(best, o);
             best = other > best ? other : best;
         }
         const int e = (int)(~(uint32_t)best);
@@ -223,132 +202,316 @@ __global__ __launch_bounds__(256) void topk_softmax_kernel(const float *__restri
         denom += p;  // same order (j ascending) in every lane
         if (lane == j) {
             my_e = e;
-            my_l = p;
+            my_p = p;
         }
     }
     if (lane < k) {
-        const float w = my_l / denom;
-        ids[(size_t)t * k + lane] = my_e;
-        wts[(size_t)t * k + lane] = w;
-        if (ids_user) ids_user[(size_t)t * k + lane] = my_e;
-        if (wts_user) wts_user[(size_t)t * k + lane] = w;
+        const float w = my_p / denom;
+        ids[lane] = my_e;
+        wts[lane] = w;
+        if (ids_user) ids_user[lane] = my_e;
+        if (wts_user) wts_user[lane] = w;
     }
 }
 
-// ------------------------------------------------------------------ grouping
-//
-// One workgroup.  LDS holds one bit per (expert, token): expert e's tokens in token
-// order.  counts[e] = popcount of its row, offsets = exclusive prefix sum, and the
-// slot of pair (t, j) choosing e is offsets[e] + (number of earlier tokens that chose
-// e).  Every result is independent of thread timing.  Experts with at least `mstar`
-// tokens go to the MFMA list, the others to the GEMV list, each in expert order.
+template <typename XT>
+__device__ inline void load32_f32(const XT *p, float (&v)[32]);
 
-__global__ __launch_bounds__(1024) void group_kernel(const int32_t *__restrict__ ids, int T, int k, int E, int mstar,
-                                                     int32_t *__restrict__ meta, int32_t *__restrict__ slot_of,
-                                                     int32_t *__restrict__ tok_of,
-                                                     const int32_t *__restrict__ fb_flags)
+template <>
+__device__ inline void load32_f32<uint16_t>(const uint16_t *p, float (&v)[32])
+{
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const uint4 u = reinterpret_cast<const uint4 *>(p)[q];
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            v[8 * q + 2 * i] = __uint_as_float(w[i] << 16);
+            v[8 * q + 2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+        }
+    }
+}
+
+template <>
+__device__ inline void load32_f32<float>(const float *p, float (&v)[32])
+{
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        const float4 u = reinterpret_cast<const float4 *>(p)[q];
+        v[4 * q] = u.x;
+        v[4 * q + 1] = u.y;
+        v[4 * q + 2] = u.z;
+        v[4 * q + 3] = u.w;
+    }
+}
+
+// ------------------------------------------------------------------ block scan
+
+// Exclusive prefix sums of four counters over the 256 threads of a workgroup.
+__device__ inline void block_exscan4(int (&v)[4], int (&tot)[4], int *sh /* [4 waves][4] */)
+{
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int inc[4] = {v[0], v[1], v[2], v[3]};
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int y = __shfl_up(inc[c], o);
+            if (lane >= o) inc[c] += y;
+        }
+    }
+    if (lane == 63)
+        for (int c = 0; c < 4; ++c) sh[wave * 4 + c] = inc[c];
+    __syncthreads();
+    for (int c = 0; c < 4; ++c) {
+        int before = 0, all = 0;
+        for (int w = 0; w < 4; ++w) {
+            const int s = sh[w * 4 + c];
+            if (w < wave) before += s;
+            all += s;
+        }
+        tot[c] = all;
+        v[c] = before + inc[c] - v[c];
+    }
+    __syncthreads();
+}
+
+// ------------------------------------------------------------------ fused routing kernel
+//
+// Grid = T x bpt workgroups of 4 waves.  Workgroup (t, q) computes the logits of token
+// t for experts [4*q*epw, 4*(q+1)*epw).  The last workgroup of token t to finish (a
+// device-scope counter) runs that token's top-k softmax and, when the MFMA path is
+// enabled, its 2-term FP8 activation split.  The last token to finish then groups all
+// (token, choice) pairs by expert.  The counters are reset by the workgroup that
+// consumes them, so they read zero at the start of every launch.
+
+// Device-scope release / acquire fences (the agent is the whole GPU: its XCDs have
+// separate L2 caches, so publishing writes them back and consuming invalidates).
+__device__ inline void release_agent() { __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent"); }
+__device__ inline void acquire_agent() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
+
+struct RouteArgs {
+    const void *x;
+    const void *wr;
+    const float *bias;
+    float *logits;
+    int32_t *ids, *ids_user;
+    float *wts, *wts_user;
+    int32_t *meta, *slot_of, *tok_of;
+    int32_t *cnt_tok;  // [Tmax]
+    int32_t *cnt_all;  // [1]
+    int32_t *fb_acc;   // [1]
+    uint8_t *xs_hi, *xs_lo, *xe_hi, *xe_lo;  // activation split (NULL: MFMA path off)
+    int T, E, H, k, epw, bpt, mstar, do_group, max_chunks;
+};
+
+template <typename XT, typename WT>
+__global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
 {
     extern __shared__ uint32_t lds[];
-    const int W = (T + 31) / 32;
-    uint32_t *mask = lds;                  // [E][W]
-    int32_t *offs = (int32_t *)(lds + E * W);  // [E+1]
-    __shared__ int32_t fb_total;
-    const MetaIdx mi{E};
-    const int tid = threadIdx.x, nth = blockDim.x;
+    __shared__ int s_flag;
+    __shared__ int s_scan[16];
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+    const int t = blockIdx.x / A.bpt;
+    const int q = blockIdx.x % A.bpt;
+    const int E = A.E, H = A.H;
+    const XT *xr = (const XT *)A.x + (size_t)t * H;
 
-    for (int i = tid; i < E * W; i += nth) mask[i] = 0u;
-    if (tid == 0) fb_total = 0;
-    __syncthreads();
-    for (int p = tid; p < T * k; p += nth) {
-        const int t = p / k;
-        atomicOr(&mask[ids[p] * W + t / 32], 1u << (t % 32));
+    // 1. logits of this workgroup's experts
+    {
+        const int e0 = (q * 4 + wave) * A.epw;
+        const int e1 = min(E, e0 + A.epw);
+        int nfb = 0;
+        for (int e = e0; e < e1; ++e) {
+            int fb;
+            const float r = wave_logit<XT, WT>(xr, (const WT *)A.wr + (size_t)e * H, A.bias ? A.bias + e : nullptr,
+                                               H, lane, fb);
+            nfb += fb;
+            if (lane == 0) A.logits[(size_t)t * E + e] = r;
+        }
+        if (lane == 0 && nfb) atomicAdd(A.fb_acc, nfb);
     }
-    int fb = 0;
-    if (fb_flags)
-        for (int i = tid; i < T * E; i += nth) fb += fb_flags[i];
+    // Publish this workgroup's logits (release: write back, no invalidate), count it;
+    // only the last workgroup of the token acquires (invalidates its caches).
+    release_agent();
     __syncthreads();
-    for (int e = tid; e < E; e += nth) {
-        int c = 0;
-        for (int w = 0; w < W; ++w) c += __popc(mask[e * W + w]);
-        meta[mi.counts() + e] = c;
-        offs[e] = c;  // counts for the scan below
+    if (threadIdx.x == 0) s_flag = atomicAdd(&A.cnt_tok[t], 1) == A.bpt - 1;
+    __syncthreads();
+    if (!s_flag) return;
+    acquire_agent();
+
+    // 2. last workgroup of token t: top-k softmax and the activation split
+    if (wave == 0)
+        wave_topk(A.logits + (size_t)t * E, E, A.k, lane, A.ids + (size_t)t * A.k, A.wts + (size_t)t * A.k,
+                  A.ids_user ? A.ids_user + (size_t)t * A.k : nullptr,
+                  A.wts_user ? A.wts_user + (size_t)t * A.k : nullptr);
+    if (A.xs_hi) {
+        for (int g = threadIdx.x; g < H / 32; g += blockDim.x) {
+            float v[32], res[32];
+            uint32_t qh[8], ql[8];
+            load32_f32<XT>(xr + g * 32, v);
+            const int ch = exp_for_group(amax_of(v));
+            split_hi(v, ch, qh, res);
+            const int cl = exp_for_group(amax_of(res));
+            split_lo(res, cl, ql);
+            const size_t o = (size_t)t * H + g * 32;
+            reinterpret_cast<uint4 *>(A.xs_hi + o)[0] = make_uint4(qh[0], qh[1], qh[2], qh[3]);
+            reinterpret_cast<uint4 *>(A.xs_hi + o)[1] = make_uint4(qh[4], qh[5], qh[6], qh[7]);
+            reinterpret_cast<uint4 *>(A.xs_lo + o)[0] = make_uint4(ql[0], ql[1], ql[2], ql[3]);
+            reinterpret_cast<uint4 *>(A.xs_lo + o)[1] = make_uint4(ql[4], ql[5], ql[6], ql[7]);
+            A.xe_hi[(size_t)t * (H / 32) + g] = (uint8_t)ch;
+            A.xe_lo[(size_t)t * (H / 32) + g] = (uint8_t)cl;
+        }
     }
-    if (fb) atomicAdd(&fb_total, fb);
+    if (threadIdx.x == 0) A.cnt_tok[t] = 0;
+    if (!A.do_group) return;
+    release_agent();
     __syncthreads();
-    if (tid == 0) {
-        int run = 0, na = 0, ng = 0, nm = 0;
-        for (int e = 0; e < E; ++e) {
-            const int c = offs[e];
-            offs[e] = run;
-            meta[mi.offsets() + e] = run;
-            run += c;
+    if (threadIdx.x == 0) s_flag = atomicAdd(A.cnt_all, 1) == A.T - 1;
+    __syncthreads();
+    if (!s_flag) return;
+    acquire_agent();
+
+    // 3. last token: group the T*k (token, choice) pairs by expert.  LDS holds one bit
+    // per (expert, token): expert e's tokens in token order.  counts = popcounts,
+    // offsets = exclusive prefix sum, slot of pair (t, j) choosing e = offsets[e] +
+    // (number of earlier tokens that chose e).  Experts with at least `mstar` tokens
+    // go to the MFMA list, the others to the GEMV list, each in expert order.
+    const int T = A.T, k = A.k;
+    const int W = (T + 31) / 32;
+    uint32_t *mask = lds;                        // [E][W]
+    int32_t *offs = (int32_t *)(lds + E * W);    // [E]
+    const MetaIdx mi{E, A.max_chunks};
+    for (int i = threadIdx.x; i < E * W; i += blockDim.x) mask[i] = 0u;
+    __syncthreads();
+    for (int p = threadIdx.x; p < T * k; p += blockDim.x) {
+        const int tt = p / k;
+        atomicOr(&mask[A.ids[p] * W + tt / 32], 1u << (tt % 32));
+    }
+    __syncthreads();
+    // each thread owns up to 4 consecutive experts
+    const int per = (E + 255) / 256;
+    const int eb = threadIdx.x * per;
+    int cnt[4] = {0, 0, 0, 0};
+    int v[4] = {0, 0, 0, 0};  // tokens, gemv experts, mfma experts, mfma token chunks
+    for (int j = 0; j < per; ++j) {
+        const int e = eb + j;
+        if (e < E) {
+            int c = 0;
+            for (int w = 0; w < W; ++w) c += __popc(mask[e * W + w]);
+            cnt[j] = c;
+            v[0] += c;
             if (c > 0) {
-                ++na;
-                if (mstar > 0 && c >= mstar)
-                    meta[mi.act_mfma() + nm++] = e;
-                else
-                    meta[mi.act_gemv() + ng++] = e;
+                if (A.mstar > 0 && c >= A.mstar) {
+                    v[2]++;
+                    v[3] += (c + kMfmaChunk - 1) / kMfmaChunk;
+                } else {
+                    v[1]++;
+                }
             }
         }
-        offs[E] = run;
-        meta[mi.offsets() + E] = run;
-        meta[mi.n_active()] = na;
-        meta[mi.n_gemv()] = ng;
-        meta[mi.n_mfma()] = nm;
-        meta[mi.n_fallback()] = fb_total;
+    }
+    int tot[4];
+    block_exscan4(v, tot, s_scan);
+    for (int j = 0; j < per; ++j) {
+        const int e = eb + j;
+        if (e < E) {
+            const int c = cnt[j];
+            offs[e] = v[0];
+            A.meta[mi.counts() + e] = c;
+            A.meta[mi.offsets() + e] = v[0];
+            if (c > 0) {
+                if (A.mstar > 0 && c >= A.mstar) {
+                    int4 *cr = reinterpret_cast<int4 *>(A.meta + mi.chunk_rec());
+                    for (int m0 = 0; m0 < c; m0 += kMfmaChunk)
+                        cr[v[3]++] = make_int4(e, v[0] + m0, min(kMfmaChunk, c - m0), 0);
+                    v[2]++;
+                } else {
+                    reinterpret_cast<int4 *>(A.meta + mi.gemv_rec())[v[1]++] = make_int4(e, v[0], c, 0);
+                }
+            }
+            v[0] += c;
+        }
+    }
+    if (threadIdx.x == 0) {
+        A.meta[mi.offsets() + E] = tot[0];
+        A.meta[mi.n_active()] = tot[1] + tot[2];
+        A.meta[mi.n_gemv()] = tot[1];
+        A.meta[mi.n_mfma()] = tot[2];
+        A.meta[mi.n_fallback()] = atomicExch(A.fb_acc, 0);
+        A.meta[mi.n_mfma_chunks()] = tot[3];
+        *A.cnt_all = 0;
     }
     __syncthreads();
-    for (int p = tid; p < T * k; p += nth) {
-        const int t = p / k, e = ids[p];
-        int rank = __popc(mask[e * W + t / 32] & ((1u << (t % 32)) - 1u));
-        for (int w = 0; w < t / 32; ++w) rank += __popc(mask[e * W + w]);
+    for (int p = threadIdx.x; p < T * k; p += blockDim.x) {
+        const int tt = p / k, e = A.ids[p];
+        int rank = __popc(mask[e * W + tt / 32] & ((1u << (tt % 32)) - 1u));
+        for (int w = 0; w < tt / 32; ++w) rank += __popc(mask[e * W + w]);
         const int slot = offs[e] + rank;
-        slot_of[p] = slot;
-        tok_of[slot] = t;
+        A.slot_of[p] = slot;
+        A.tok_of[slot] = tt;
     }
+}
+
+__global__ void zero_kernel(int32_t *p, int n)
+{
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
 }
 
 }  // namespace
 
-hipError_t launch_router(const Layer &L, const void *x, int T, const void *router_w, const float *bias,
-                         float *logits, int32_t *fb_flags, hipStream_t st)
+hipError_t launch_zero(int32_t *p, int n, hipStream_t st)
+{
+    zero_kernel<<<(n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024, 256, 0, st>>>(p, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_route(const Layer &L, const RouteParams &P, hipStream_t st)
 {
     // Experts per wave: enough waves to cover the GPU, few experts per wave at small T.
     const int target_waves = 4096;
-    int epw = (T * L.E + target_waves - 1) / target_waves;
+    int epw = (P.T * L.E + target_waves - 1) / target_waves;
     epw = epw < 1 ? 1 : (epw > 16 ? 16 : epw);
-    const int groups = (L.E + epw - 1) / epw;
-    const int waves = T * groups;
-    dim3 grid((waves + 3) / 4), block(256);
+    const int bpt = (L.E + 4 * epw - 1) / (4 * epw);
+    RouteArgs A;
+    A.x = P.x;
+    A.wr = P.router_w;
+    A.bias = P.bias;
+    A.logits = P.logits;
+    A.ids = P.ids;
+    A.ids_user = P.ids_user;
+    A.wts = P.wts;
+    A.wts_user = P.wts_user;
+    A.meta = P.meta;
+    A.slot_of = P.slot_of;
+    A.tok_of = P.tok_of;
+    A.cnt_tok = P.cnt_tok;
+    A.cnt_all = P.cnt_all;
+    A.fb_acc = P.fb_acc;
+    A.xs_hi = P.xs_hi;
+    A.xs_lo = P.xs_lo;
+    A.xe_hi = P.xe_hi;
+    A.xe_lo = P.xe_lo;
+    A.T = P.T;
+    A.E = L.E;
+    A.H = L.H;
+    A.k = P.k;
+    A.epw = epw;
+    A.bpt = bpt;
+    A.mstar = P.mstar;
+    A.do_group = P.do_group;
+    A.max_chunks = P.max_chunks;
+    const int W = (P.T + 31) / 32;
+    const size_t lds = P.do_group ? sizeof(uint32_t) * ((size_t)L.E * W + L.E) : 0;
+    dim3 grid(P.T * bpt), block(256);
     if (L.act_bf16 && L.router_bf16)
-        router_logits_kernel<uint16_t, uint16_t><<<grid, block, 0, st>>>(
-            (const uint16_t *)x, (const uint16_t *)router_w, bias, logits, fb_flags, T, L.E, L.H, epw);
+        route_kernel<uint16_t, uint16_t><<<grid, block, lds, st>>>(A);
     else if (L.act_bf16)
-        router_logits_kernel<uint16_t, float><<<grid, block, 0, st>>>(
-            (const uint16_t *)x, (const float *)router_w, bias, logits, fb_flags, T, L.E, L.H, epw);
+        route_kernel<uint16_t, float><<<grid, block, lds, st>>>(A);
     else if (L.router_bf16)
-        router_logits_kernel<float, uint16_t><<<grid, block, 0, st>>>(
-            (const float *)x, (const uint16_t *)router_w, bias, logits, fb_flags, T, L.E, L.H, epw);
+        route_kernel<float, uint16_t><<<grid, block, lds, st>>>(A);
     else
-        router_logits_kernel<float, float><<<grid, block, 0, st>>>((const float *)x, (const float *)router_w, bias,
-                                                                   logits, fb_flags, T, L.E, L.H, epw);
-    return hipGetLastError();
-}
-
-hipError_t launch_topk(const Layer &L, const float *logits, int T, int k, int32_t *ids, float *wts,
-                       int32_t *ids_user, float *wts_user, hipStream_t st)
-{
-    dim3 grid((T + 3) / 4), block(256);
-    topk_softmax_kernel<<<grid, block, 0, st>>>(logits, T, L.E, k, ids, wts, ids_user, wts_user);
-    return hipGetLastError();
-}
-
-hipError_t launch_group(const Layer &L, const int32_t *ids, int T, int k, int mstar, int32_t *meta,
-                        int32_t *slot_of, int32_t *tok_of, const int32_t *fb_flags, hipStream_t st)
-{
-    const int W = (T + 31) / 32;
-    const size_t lds = sizeof(uint32_t) * ((size_t)L.E * W + L.E + 1);
-    group_kernel<<<1, 1024, lds, st>>>(ids, T, k, L.E, mstar, meta, slot_of, tok_of, fb_flags);
+        route_kernel<float, float><<<grid, block, lds, st>>>(A);
     return hipGetLastError();
 }
 

@@ -1,0 +1,136 @@
+// HBM streaming reference for the roofline: how fast this GPU reads (and copies)
+// large buffers with the access shapes the expert kernels use.  Not part of the
+// library; built as a separate executable and used by the measurement scripts.
+//
+//   stream_probe <mode> <MiB> <iters>
+//   modes: read      grid-stride 16-byte loads over a contiguous buffer
+//          read_nt   the same with non-temporal loads
+//          tiles     16-row x 128-byte tiles of 4096-byte rows, each lane two 16-byte
+//                    pieces (the FP8 MFMA operand shape), rows streamed in K order
+//          tiles_nt  the same with non-temporal loads
+//          copy      contiguous 16-byte copy (reads and writes MiB each)
+// Prints one line: mode, bytes moved per launch, mean ms, GB/s.
+#include <hip/hip_runtime.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <bool NT>
+__device__ inline u32x4 ld(const u32x4 *p)
+{
+    if constexpr (NT)
+        return __builtin_nontemporal_load(p);
+    else
+        return *p;
+}
+
+template <bool NT>
+__global__ __launch_bounds__(256) void read_kernel(const u32x4 *__restrict__ a, size_t n, uint32_t *__restrict__ sink)
+{
+    u32x4 acc = {0, 0, 0, 0};
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    for (; i + 3 * stride < n; i += 4 * stride) {
+        const u32x4 v0 = ld<NT>(a + i), v1 = ld<NT>(a + i + stride), v2 = ld<NT>(a + i + 2 * stride),
+                    v3 = ld<NT>(a + i + 3 * stride);
+        acc ^= v0 ^ v1 ^ v2 ^ v3;
+    }
+    for (; i < n; i += stride) acc ^= ld<NT>(a + i);
+    if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9E3779B9u) sink[0] = 1;  // keeps the loads alive
+}
+
+// Each wave streams one tile of 16 rows (row length 4096 bytes) in 128-byte K blocks.
+template <bool NT>
+__global__ __launch_bounds__(256) void tiles_kernel(const uint8_t *__restrict__ a, size_t n_tiles,
+                                                    uint32_t *__restrict__ sink)
+{
+    const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+    u32x4 acc = {0, 0, 0, 0};
+    for (size_t t = (size_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < n_tiles; t += (size_t)gridDim.x * 4) {
+        const uint8_t *row = a + t * 16 * 4096 + (size_t)r * 4096;
+#pragma unroll 4
+        for (int kb = 0; kb < 32; ++kb) {
+            acc ^= ld<NT>(reinterpret_cast<const u32x4 *>(row + kb * 128 + 16 * g));
+            acc ^= ld<NT>(reinterpret_cast<const u32x4 *>(row + kb * 128 + 64 + 16 * g));
+        }
+    }
+    if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9E3779B9u) sink[0] = 1;
+}
+
+__global__ __launch_bounds__(256) void copy_kernel(const u32x4 *__restrict__ a, u32x4 *__restrict__ b, size_t n)
+{
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) b[i] = a[i];
+}
+
+#define CHECK(x)                                                                             \
+    do {                                                                                     \
+        hipError_t e = (x);                                                                  \
+        if (e != hipSuccess) {                                                               \
+            fprintf(stderr, "%s: %s\n", #x, hipGetErrorString(e));                           \
+            exit(1);                                                                         \
+        }                                                                                    \
+    } while (0)
+
+int main(int argc, char **argv)
+{
+    if (argc < 4) {
+        fprintf(stderr, "usage: %s read|read_nt|tiles|tiles_nt|copy MiB iters\n", argv[0]);
+        return 2;
+    }
+    const char *mode = argv[1];
+    const size_t bytes = (size_t)atol(argv[2]) << 20;
+    const int iters = atoi(argv[3]);
+    if (bytes == 0 || bytes % (16 * 4096) != 0 || iters < 1) {
+        fprintf(stderr, "MiB must be positive (multiple of 64 KiB) and iters >= 1\n");
+        return 2;
+    }
+    int cus = 0;
+    CHECK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, 0));
+    uint8_t *a = nullptr, *b = nullptr;
+    uint32_t *sink = nullptr;
+    CHECK(hipMalloc(&a, bytes));
+    CHECK(hipMalloc(&sink, 4));
+    CHECK(hipMemset(a, 1, bytes));
+    const bool copy = strcmp(mode, "copy") == 0;
+    if (copy) CHECK(hipMalloc(&b, bytes));
+    const size_t n16 = bytes / 16, n_tiles = bytes / (16 * 4096);
+    const int grid = cus * 8;
+    hipEvent_t e0, e1;
+    CHECK(hipEventCreate(&e0));
+    CHECK(hipEventCreate(&e1));
+    auto launch = [&]() {
+        if (!strcmp(mode, "read"))
+            read_kernel<false><<<grid, 256>>>((const u32x4 *)a, n16, sink);
+        else if (!strcmp(mode, "read_nt"))
+            read_kernel<true><<<grid, 256>>>((const u32x4 *)a, n16, sink);
+        else if (!strcmp(mode, "tiles"))
+            tiles_kernel<false><<<grid, 256>>>(a, n_tiles, sink);
+        else if (!strcmp(mode, "tiles_nt"))
+            tiles_kernel<true><<<grid, 256>>>(a, n_tiles, sink);
+        else if (copy)
+            copy_kernel<<<grid, 256>>>((const u32x4 *)a, (u32x4 *)b, n16);
+        else {
+            fprintf(stderr, "unknown mode %s\n", mode);
+            exit(2);
+        }
+        CHECK(hipGetLastError());
+    };
+    launch();
+    CHECK(hipDeviceSynchronize());
+    CHECK(hipEventRecord(e0, 0));
+    for (int i = 0; i < iters; ++i) launch();
+    CHECK(hipEventRecord(e1, 0));
+    CHECK(hipEventSynchronize(e1));
+    float ms = 0.f;
+    CHECK(hipEventElapsedTime(&ms, e0, e1));
+    ms /= iters;
+    const double moved = copy ? 2.0 * bytes : (double)bytes;
+    printf("%s bytes=%zu ms=%.4f GBps=%.1f\n", mode, (size_t)moved, ms, moved / (ms * 1e-3) / 1e9);
+    CHECK(hipFree(a));
+    if (b) CHECK(hipFree(b));
+    CHECK(hipFree(sink));
+    return 0;
+}

@@ -270,3 +270,36 @@ def test_full_235b_mxfp4_zipf(dev):
     st, counts = run.m.stats()
     say(f"[zipf] active={st.n_active} max tokens/expert={max(counts)}")
     assert max(counts) > 4 * (256 * cfg.topk / st.n_active)  # skewed popularity
+
+
+# ---------------------------------------------------------------- both expert paths
+
+@pytest.mark.parametrize("mstar", [-1, 1, 2])
+@pytest.mark.parametrize("cfg,T", [(SMALL_FP8, 13), (SMALL_MX, 13), (SMALL_FP8, 32), (C.TINY, 4)])
+def test_expert_paths(dev, cfg, T, mstar):
+    """mfma_min_tokens = -1 forces the GEMV path for every expert, 1 the MFMA path,
+    2 mixes them within one step."""
+    hl = W.host_layer(cfg, seed=520)
+    run = Run(cfg, hl, dev, max_tokens=max(T, 32), mfma_min_tokens=mstar)
+    check_layer(run, W.host_x(cfg, T, seed=520), label=f"{cfg.name} T={T} mstar={mstar}")
+    st, counts = run.m.stats()
+    if mstar == 1:
+        assert st.n_active_mfma == st.n_active
+    elif mstar == -1:
+        assert st.n_active_mfma == 0
+    say(f"[paths] mstar={mstar}: {st.n_active_mfma}/{st.n_active} experts on MFMA tiles")
+
+
+@pytest.mark.parametrize("mstar", [-1, 1])
+def test_full_235b_paths(dev, full_235b, mstar):
+    cfg = C.QWEN3_235B
+    run = Run(cfg, full_235b, dev, max_tokens=64, mfma_min_tokens=mstar)
+    _full(run, cfg, 64, batch=3)
+
+
+@pytest.mark.parametrize("mstar", [-1, 1])
+def test_full_mxfp4_paths(dev, mstar):
+    cfg = C.QWEN3_235B_MXFP4
+    hl = W.host_layer(cfg)
+    run = Run(cfg, hl, dev, max_tokens=256, mfma_min_tokens=mstar)
+    _full(run, cfg, 256, batch=1)
