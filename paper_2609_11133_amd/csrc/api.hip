@@ -33,7 +33,7 @@ size_t carve_workspace(int H, int E, int I, int kmax, int Tmax, void *base, Work
     w.tok_of = (int32_t *)take(sizeof(int32_t) * P);
     w.h = (float *)take(sizeof(float) * P * I);
     w.o = (float *)take(sizeof(float) * P * H);
-    w.sync = (int32_t *)take(sizeof(int32_t) * ((size_t)Tmax + 2));
+    w.sync = (int32_t *)take(sizeof(int32_t) * ((size_t)Tmax + 2) * kCounterStride);
     w.xs_hi = (uint8_t *)take((size_t)Tmax * H);
     w.xs_lo = (uint8_t *)take((size_t)Tmax * H);
     w.xe_hi = (uint8_t *)take((size_t)Tmax * H / 32);
@@ -213,7 +213,7 @@ static void prof_mark(moe_decode_t h, int stage_boundary, hipStream_t st)
 static moe_status ensure_synced(moe_decode_t h, hipStream_t st)
 {
     if (!h->synced) {
-        HIPCHECK(h, launch_zero(h->ws.sync, h->cfg.max_tokens + 2, st));
+        HIPCHECK(h, launch_zero(h->ws.sync, (h->cfg.max_tokens + 2) * kCounterStride, st));
         h->synced = 1;
     }
     return MOE_OK;
@@ -238,8 +238,8 @@ static RouteParams route_params(moe_decode_t h, const void *x, int T, int k, con
     P.slot_of = w.slot_of;
     P.tok_of = w.tok_of;
     P.cnt_tok = w.sync;
-    P.cnt_all = w.sync + h->cfg.max_tokens;
-    P.fb_acc = w.sync + h->cfg.max_tokens + 1;
+    P.cnt_all = w.sync + (size_t)h->cfg.max_tokens * kCounterStride;
+    P.fb_acc = w.sync + ((size_t)h->cfg.max_tokens + 1) * kCounterStride;
     P.xs_hi = split ? w.xs_hi : nullptr;
     P.xs_lo = w.xs_lo;
     P.xe_hi = w.xe_hi;

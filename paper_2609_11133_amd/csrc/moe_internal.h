@@ -17,7 +17,7 @@ struct Workspace {
     int32_t *tok_of;   // [Tmax*kmax] token of slot
     float *h;          // [Tmax*kmax][I] SwiGLU activations per slot (GEMV path)
     float *o;          // [Tmax*kmax][H] expert outputs per slot
-    int32_t *sync;     // [Tmax + 2] routing counters (zero between launches)
+    int32_t *sync;     // [(Tmax + 2) * kCounterStride] routing counters (zero between launches)
     uint8_t *xs_hi, *xs_lo;  // [Tmax][H] 2-term FP8 split of x (MFMA path)
     uint8_t *xe_hi, *xe_lo;  // [Tmax][H/32] E8M0 exponents of the split
     uint8_t *hs_hi, *hs_lo;  // [Tmax*kmax][I] 2-term FP8 split of h (MFMA path)
@@ -46,7 +46,8 @@ struct MetaIdx {
 
 __host__ __device__ inline int max_mfma_chunks(int E, int Tmax, int kmax) { return E + (Tmax * kmax + 31) / 32; }
 
-constexpr int kMfmaChunk = 32;  // tokens per MFMA pass (two 16-column tiles)
+constexpr int kMfmaChunk = 32;      // tokens per MFMA pass (two 16-column tiles)
+constexpr int kCounterStride = 64;  // int32 words between routing counters (256 bytes)
 
 size_t carve_workspace(int H, int E, int I, int kmax, int Tmax, void *base, Workspace *ws);
 

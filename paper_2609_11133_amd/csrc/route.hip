@@ -12,6 +12,17 @@ namespace {
 
 constexpr int kWave = 64;
 
+// Values exchanged between workgroups of this kernel (logits, selected experts) are
+// written and read with device-scope atomic stores and loads, which bypass the
+// per-XCD L2 caches; a producer waits for its stores to complete before it bumps a
+// counter.  This avoids whole-cache write-back / invalidate fences, which serialise
+// per XCD.
+template <typename T>
+__device__ inline void st_dev(T *p, T v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+template <typename T>
+__device__ inline T ld_dev(const T *p) { return __hip_atomic_load(const_cast<T *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+__device__ inline void wait_stores() { __builtin_amdgcn_s_waitcnt(0); }
+
 // ------------------------------------------------------------------ router logits
 //
 // Canonical logit: one round-to-nearest-even to fp32 of the exact value of
@@ -92,71 +103,146 @@ __device__ inline void load8<float>(const float *p, double (&v)[8])
     v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
 }
 
-// Canonical logit of token row xr against router row wrow, computed by one wave.
-// Every lane returns the same value; *fallback is set when the exact path ran.
+// Exact (double-double) logit of one (token, expert) pair, computed by one wave: the
+// slow path taken when the fp64 sum cannot certify its fp32 rounding.
 template <typename XT, typename WT>
-__device__ inline float wave_logit(const XT *__restrict__ xr, const WT *__restrict__ wrow, const float *bias_e, int H,
-                                   int lane, int &fallback)
+__device__ inline float wave_logit_exact(const XT *__restrict__ xr, const WT *__restrict__ wrow, double b, int H,
+                                         int lane)
 {
-    const int per_lane = ((H + 511) / 512) * 8;
-    const double gamma = (double)(per_lane + 6 + 1 + 2) * 0x1p-52;  // >= 2 gamma_D
-    double s = 0.0, a = 0.0;
+    double hi = 0.0, lo = 0.0;
     for (int h = lane * 8; h < H; h += 512) {
         double xv[8], wv[8];
         load8<XT>(xr + h, xv);
         load8<WT>(wrow + h, wv);
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-            s = fma(xv[i], wv[i], s);
-            a = fma(fabs(xv[i]), fabs(wv[i]), a);
+            double p = xv[i] * wv[i], ss, ee;  // exact product
+            two_sum(hi, p, ss, ee);
+            hi = ss;
+            lo += ee;
         }
     }
+    double nh = hi + lo;  // normalise the lane's pair before combining
+    lo = lo - (nh - hi);
+    hi = nh;
 #pragma unroll
     for (int o = kWave / 2; o >= 1; o >>= 1) {
-        s += __shfl_xor(s, o);
-        a += __shfl_xor(a, o);
+        double h2 = __shfl_xor(hi, o), l2 = __shfl_xor(lo, o);
+        dd_add(hi, lo, h2, l2);
     }
-    const double b = bias_e ? (double)*bias_e : 0.0;
-    float r;
-    fallback = 0;
-    if (!certain_f32(s + b, gamma * (a + fabs(b)), r)) {
-        // Exact path: error-free accumulation of the same (exact) products.
-        double hi = 0.0, lo = 0.0;
-        for (int h = lane * 8; h < H; h += 512) {
-            double xv[8], wv[8];
-            load8<XT>(xr + h, xv);
-            load8<WT>(wrow + h, wv);
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                double p = xv[i] * wv[i], ss, ee;
-                two_sum(hi, p, ss, ee);
-                hi = ss;
-                lo += ee;
-            }
-        }
-        double nh = hi + lo;  // normalise the lane's pair before combining
-        lo = lo - (nh - hi);
-        hi = nh;
-#pragma unroll
-        for (int o = kWave / 2; o >= 1; o >>= 1) {
-            double h2 = __shfl_xor(hi, o), l2 = __shfl_xor(lo, o);
-            dd_add(hi, lo, h2, l2);
-        }
-        dd_add(hi, lo, b, 0.0);
-        r = round_dd_to_f32(hi, lo);
-        fallback = 1;
-    }
-    return r + 0.0f;  // -0 -> +0
+    dd_add(hi, lo, b, 0.0);
+    return round_dd_to_f32(hi, lo);
 }
 
-// ------------------------------------------------------------------ top-k softmax
+// Eight consecutive inputs of one lane, as raw bits (bf16: 4 words, fp32: 8 words).
+template <typename T>
+struct Chunk8 {
+    uint32_t d[sizeof(T) == 2 ? 4 : 8];
+};
+
+template <typename T>
+__device__ inline void ld_chunk(const T *p, Chunk8<T> &c)
+{
+#pragma unroll
+    for (int q = 0; q < (int)(sizeof(c.d) / 16); ++q) {
+        const uint4 u = reinterpret_cast<const uint4 *>(p)[q];
+        c.d[4 * q] = u.x;
+        c.d[4 * q + 1] = u.y;
+        c.d[4 * q + 2] = u.z;
+        c.d[4 * q + 3] = u.w;
+    }
+}
+
+template <typename T>
+__device__ inline double elem(const Chunk8<T> &c, int i)
+{
+    if constexpr (sizeof(T) == 2)
+        return (double)__uint_as_float((i & 1) ? (c.d[i >> 1] & 0xFFFF0000u) : (c.d[i >> 1] << 16));
+    else
+        return (double)__uint_as_float(c.d[i]);
+}
+
+constexpr int kEPW = 4;        // experts per wave, at most
+constexpr int kSegChunks = 4;  // 8-input chunks per lane held at once (2048 inputs)
+
+// Canonical logits of one token row xr against router rows e0 .. e0+ne-1 (ne <= kEPW),
+// computed by one wave and written to lrow[e].  The lane's inputs are loaded once per
+// segment and reused for every expert; the next expert's router row is in flight
+// while the current one accumulates.  Returns the number of fallbacks taken.
+template <typename XT, typename WT>
+__device__ inline int wave_logits(const XT *__restrict__ xr, const WT *__restrict__ wr, const float *bias, int H,
+                                  int e0, int ne, int lane, float *lrow)
+{
+    const int nck = (H + 511) / 512;  // chunks of the lane with the most
+    // Two accumulators per expert (even and odd chunks): each sums at most
+    // ceil(nck/2)*8 products, then they are added and reduced over the wave.
+    const int per_acc = ((nck + 1) / 2) * 8;
+    const double gamma = (double)(per_acc + 1 + 6 + 1 + 2) * 0x1p-52;  // >= 2 gamma_D
+    double s[kEPW][2], a[kEPW][2];
+#pragma unroll
+    for (int i = 0; i < kEPW; ++i) s[i][0] = s[i][1] = a[i][0] = a[i][1] = 0.0;
+    for (int seg = 0; seg < nck; seg += kSegChunks) {
+        Chunk8<XT> xc[kSegChunks];
+        bool valid[kSegChunks];
+        int off[kSegChunks];
+#pragma unroll
+        for (int j = 0; j < kSegChunks; ++j) {
+            const int h = lane * 8 + 512 * (seg + j);
+            valid[j] = h < H;
+            off[j] = valid[j] ? h : H - 8;  // clamped: an invalid chunk is loaded but its x is 0
+            ld_chunk<XT>(xr + off[j], xc[j]);
+            if (!valid[j])
+#pragma unroll
+                for (int q = 0; q < (int)(sizeof(xc[j].d) / 4); ++q) xc[j].d[q] = 0u;
+        }
+        Chunk8<WT> wc[2][kSegChunks];
+#pragma unroll
+        for (int j = 0; j < kSegChunks; ++j) ld_chunk<WT>(wr + (size_t)e0 * H + off[j], wc[0][j]);
+#pragma unroll
+        for (int i = 0; i < kEPW; ++i) {
+            if (i < ne) {
+                if (i + 1 < ne)
+#pragma unroll
+                    for (int j = 0; j < kSegChunks; ++j)
+                        ld_chunk<WT>(wr + (size_t)(e0 + i + 1) * H + off[j], wc[(i + 1) & 1][j]);
+#pragma unroll
+                for (int j = 0; j < kSegChunks; ++j)
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) {
+                        const double xv = elem<XT>(xc[j], q), wv = elem<WT>(wc[i & 1][j], q);
+                        s[i][j & 1] = fma(xv, wv, s[i][j & 1]);
+                        a[i][j & 1] = fma(fabs(xv), fabs(wv), a[i][j & 1]);
+                    }
+            }
+        }
+    }
+    int nfb = 0;
+#pragma unroll
+    for (int i = 0; i < kEPW; ++i) {
+        if (i < ne) {
+            double si = s[i][0] + s[i][1], ai = a[i][0] + a[i][1];
+#pragma unroll
+            for (int o = kWave / 2; o >= 1; o >>= 1) {
+                si += __shfl_xor(si, o);
+                ai += __shfl_xor(ai, o);
+            }
+            const int e = e0 + i;
+            const double b = bias ? (double)bias[e] : 0.0;
+            float r;
+            if (!certain_f32(si + b, gamma * (ai + fabs(b)), r)) {
+                r = wave_logit_exact<XT, WT>(xr, wr + (size_t)e * H, b, H, lane);
+                ++nfb;
+            }
+            if (lane == 0) st_dev(&lrow[e], r + 0.0f);  // -0 -> +0
+        }
+    }
+    return nfb;
+}
+
+// ------------------------------------------------------------------ top-k keys
 //
-// One wave per token.  Each lane holds the keys of experts lane, lane+64, ...; a key
-// is (order-preserving integer image of the fp32 logit) << 32 | (~expert), so the
-// largest key is the largest logit, ties going to the lower expert index.  k rounds
-// of a wave-wide arg-max (xor butterfly) pick the experts in rank order.  Weights are
-// the softmax of the selected logits (equal to the full softmax renormalised over
-// the selection), computed in fp32 relative to the largest one.
+// A key is (order-preserving integer image of the fp32 logit) << 32 | (~expert): the
+// largest key is the largest logit, ties going to the lower expert index.
 
 __device__ inline uint32_t ordered_bits(float f)
 {
@@ -165,54 +251,6 @@ __device__ inline uint32_t ordered_bits(float f)
 }
 
 __device__ inline float from_ordered(uint32_t o) { return __uint_as_float((o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o); }
-
-constexpr int kMaxKeysPerLane = 16;  // E <= 1024
-
-__device__ inline void wave_topk(const float *__restrict__ l, int E, int k, int lane, int32_t *ids, float *wts,
-                                 int32_t *ids_user, float *wts_user)
-{
-    uint64_t key[kMaxKeysPerLane];
-    const int nk = (E + kWave - 1) / kWave;
-#pragma unroll
-    for (int c = 0; c < kMaxKeysPerLane; ++c) {
-        const int e = lane + c * kWave;
-        key[c] = (c < nk && e < E) ? (((uint64_t)ordered_bits(l[e]) << 32) | (uint32_t)(~(uint32_t)e)) : 0ull;
-    }
-    float top_l = 0.f, denom = 0.f, my_p = 0.f;
-    int my_e = 0;
-    for (int j = 0; j < k; ++j) {
-        uint64_t best = 0;
-#pragma unroll
-        for (int c = 0; c < kMaxKeysPerLane; ++c)
-            if (c < nk) best = key[c] > best ? key[c] : best;
-#pragma unroll
-        for (int o = kWave / 2; o >= 1; o >>= 1) {
-            const uint64_t other = __shfl_xor(best, o);
-            best = other > best ? other : best;
-        }
-        const int e = (int)(~(uint32_t)best);
-        const float lv = from_ordered((uint32_t)(best >> 32));
-        if ((e & (kWave - 1)) == lane) {
-#pragma unroll
-            for (int c = 0; c < kMaxKeysPerLane; ++c)
-                if (c == e / kWave) key[c] = 0ull;
-        }
-        if (j == 0) top_l = lv;
-        const float p = expf(lv - top_l);
-        denom += p;  // same order (j ascending) in every lane
-        if (lane == j) {
-            my_e = e;
-            my_p = p;
-        }
-    }
-    if (lane < k) {
-        const float w = my_p / denom;
-        ids[lane] = my_e;
-        wts[lane] = w;
-        if (ids_user) ids_user[lane] = my_e;
-        if (wts_user) wts_user[lane] = w;
-    }
-}
 
 template <typename XT>
 __device__ inline void load32_f32(const XT *p, float (&v)[32]);
@@ -276,6 +314,48 @@ __device__ inline void block_exscan4(int (&v)[4], int (&tot)[4], int *sh /* [4 w
     __syncthreads();
 }
 
+// Top-k softmax of one token by a whole workgroup.  Each expert's rank is the number
+// of keys above its own (larger logit first, then lower index),
+// counted over the token's keys staged in LDS; the expert of rank j < k is choice j.
+// Weights are the softmax of the selected logits in fp32 relative to the largest,
+// normalised by their sum taken in rank order.
+__device__ inline void block_topk(const float *__restrict__ l, int E, int k, int32_t *ids, float *wts,
+                                  int32_t *ids_user, float *wts_user, uint32_t *lds)
+{
+    uint64_t *skey = reinterpret_cast<uint64_t *>(lds);  // [E]
+    int32_t *ssel = reinterpret_cast<int32_t *>(lds + 2 * E);  // [k]
+    float *sp = reinterpret_cast<float *>(lds + 2 * E + k);    // [k]
+    for (int e = threadIdx.x; e < E; e += blockDim.x)
+        skey[e] = ((uint64_t)ordered_bits(ld_dev(&l[e])) << 32) | (uint32_t)(~(uint32_t)e);
+    __syncthreads();
+    for (int e = threadIdx.x; e < E; e += blockDim.x) {
+        const uint64_t ke = skey[e];
+        int rank = 0;
+        for (int f = 0; f < E; ++f) rank += skey[f] > ke ? 1 : 0;
+        if (rank < k) ssel[rank] = e;
+    }
+    __syncthreads();
+    const int j = threadIdx.x;
+    float lj = 0.f;
+    if (j < k) {
+        const float top = from_ordered((uint32_t)(skey[ssel[0]] >> 32));
+        lj = from_ordered((uint32_t)(skey[ssel[j]] >> 32));
+        sp[j] = expf(lj - top);
+    }
+    __syncthreads();
+    if (j < k) {
+        float denom = 0.f;
+        for (int i = 0; i < k; ++i) denom += sp[i];  // rank order, as in every thread
+        const float w = sp[j] / denom;
+        const int e = ssel[j];
+        st_dev(&ids[j], e);
+        wts[j] = w;
+        if (ids_user) ids_user[j] = e;
+        if (wts_user) wts_user[j] = w;
+    }
+    __syncthreads();  // LDS is reused by the caller
+}
+
 // ------------------------------------------------------------------ fused routing kernel
 //
 // Grid = T x bpt workgroups of 4 waves.  Workgroup (t, q) computes the logits of token
@@ -285,10 +365,6 @@ __device__ inline void block_exscan4(int (&v)[4], int (&tot)[4], int *sh /* [4 w
 // (token, choice) pairs by expert.  The counters are reset by the workgroup that
 // consumes them, so they read zero at the start of every launch.
 
-// Device-scope release / acquire fences (the agent is the whole GPU: its XCDs have
-// separate L2 caches, so publishing writes them back and consuming invalidates).
-__device__ inline void release_agent() { __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent"); }
-__device__ inline void acquire_agent() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
 
 struct RouteArgs {
     const void *x;
@@ -298,7 +374,7 @@ struct RouteArgs {
     int32_t *ids, *ids_user;
     float *wts, *wts_user;
     int32_t *meta, *slot_of, *tok_of;
-    int32_t *cnt_tok;  // [Tmax]
+    int32_t *cnt_tok;  // [Tmax][kCounterStride], one counter per 256-byte line
     int32_t *cnt_all;  // [1]
     int32_t *fb_acc;   // [1]
     uint8_t *xs_hi, *xs_lo, *xe_hi, *xe_lo;  // activation split (NULL: MFMA path off)
@@ -308,7 +384,7 @@ struct RouteArgs {
 template <typename XT, typename WT>
 __global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
 {
-    extern __shared__ uint32_t lds[];
+    extern __shared__ __attribute__((aligned(16))) uint32_t lds[];  // 64-bit keys: keep 8-byte alignment
     __shared__ int s_flag;
     __shared__ int s_scan[16];
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
@@ -317,60 +393,54 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
     const int E = A.E, H = A.H;
     const XT *xr = (const XT *)A.x + (size_t)t * H;
 
-    // 1. logits of this workgroup's experts
+    // 1. logits of this workgroup's experts, and its share of the token's activation
+    // split (groups of 32 inputs spread over the token's workgroups)
     {
         const int e0 = (q * 4 + wave) * A.epw;
-        const int e1 = min(E, e0 + A.epw);
-        int nfb = 0;
-        for (int e = e0; e < e1; ++e) {
-            int fb;
-            const float r = wave_logit<XT, WT>(xr, (const WT *)A.wr + (size_t)e * H, A.bias ? A.bias + e : nullptr,
-                                               H, lane, fb);
-            nfb += fb;
-            if (lane == 0) A.logits[(size_t)t * E + e] = r;
+        const int ne = min(E, e0 + A.epw) - e0;
+        if (ne > 0) {
+            const int nfb = wave_logits<XT, WT>(xr, (const WT *)A.wr, A.bias, H, e0, ne, lane, A.logits + (size_t)t * E);
+            if (lane == 0 && nfb) atomicAdd(A.fb_acc, nfb);
         }
-        if (lane == 0 && nfb) atomicAdd(A.fb_acc, nfb);
+        if (A.xs_hi) {
+            const int G = H / 32, per = (G + A.bpt - 1) / A.bpt;
+            for (int g = q * per + threadIdx.x; g < min(G, (q + 1) * per); g += blockDim.x) {
+                float v[32], res[32];
+                uint32_t qh[8], ql[8];
+                load32_f32<XT>(xr + g * 32, v);
+                const int ch = exp_for_group(amax_of(v));
+                split_hi(v, ch, qh, res);
+                const int cl = exp_for_group(amax_of(res));
+                split_lo(res, cl, ql);
+                const size_t o = (size_t)t * H + g * 32;
+                reinterpret_cast<uint4 *>(A.xs_hi + o)[0] = make_uint4(qh[0], qh[1], qh[2], qh[3]);
+                reinterpret_cast<uint4 *>(A.xs_hi + o)[1] = make_uint4(qh[4], qh[5], qh[6], qh[7]);
+                reinterpret_cast<uint4 *>(A.xs_lo + o)[0] = make_uint4(ql[0], ql[1], ql[2], ql[3]);
+                reinterpret_cast<uint4 *>(A.xs_lo + o)[1] = make_uint4(ql[4], ql[5], ql[6], ql[7]);
+                A.xe_hi[(size_t)t * (H / 32) + g] = (uint8_t)ch;
+                A.xe_lo[(size_t)t * (H / 32) + g] = (uint8_t)cl;
+            }
+        }
     }
-    // Publish this workgroup's logits (release: write back, no invalidate), count it;
-    // only the last workgroup of the token acquires (invalidates its caches).
-    release_agent();
+    // Publish this workgroup's logits, then count it; the last workgroup of the token
+    // goes on.
+    wait_stores();
     __syncthreads();
-    if (threadIdx.x == 0) s_flag = atomicAdd(&A.cnt_tok[t], 1) == A.bpt - 1;
+    if (threadIdx.x == 0) s_flag = atomicAdd(&A.cnt_tok[t * kCounterStride], 1) == A.bpt - 1;
     __syncthreads();
     if (!s_flag) return;
-    acquire_agent();
 
-    // 2. last workgroup of token t: top-k softmax and the activation split
-    if (wave == 0)
-        wave_topk(A.logits + (size_t)t * E, E, A.k, lane, A.ids + (size_t)t * A.k, A.wts + (size_t)t * A.k,
-                  A.ids_user ? A.ids_user + (size_t)t * A.k : nullptr,
-                  A.wts_user ? A.wts_user + (size_t)t * A.k : nullptr);
-    if (A.xs_hi) {
-        for (int g = threadIdx.x; g < H / 32; g += blockDim.x) {
-            float v[32], res[32];
-            uint32_t qh[8], ql[8];
-            load32_f32<XT>(xr + g * 32, v);
-            const int ch = exp_for_group(amax_of(v));
-            split_hi(v, ch, qh, res);
-            const int cl = exp_for_group(amax_of(res));
-            split_lo(res, cl, ql);
-            const size_t o = (size_t)t * H + g * 32;
-            reinterpret_cast<uint4 *>(A.xs_hi + o)[0] = make_uint4(qh[0], qh[1], qh[2], qh[3]);
-            reinterpret_cast<uint4 *>(A.xs_hi + o)[1] = make_uint4(qh[4], qh[5], qh[6], qh[7]);
-            reinterpret_cast<uint4 *>(A.xs_lo + o)[0] = make_uint4(ql[0], ql[1], ql[2], ql[3]);
-            reinterpret_cast<uint4 *>(A.xs_lo + o)[1] = make_uint4(ql[4], ql[5], ql[6], ql[7]);
-            A.xe_hi[(size_t)t * (H / 32) + g] = (uint8_t)ch;
-            A.xe_lo[(size_t)t * (H / 32) + g] = (uint8_t)cl;
-        }
-    }
-    if (threadIdx.x == 0) A.cnt_tok[t] = 0;
+    // 2. last workgroup of token t: top-k softmax
+    block_topk(A.logits + (size_t)t * E, E, A.k, A.ids + (size_t)t * A.k, A.wts + (size_t)t * A.k,
+               A.ids_user ? A.ids_user + (size_t)t * A.k : nullptr, A.wts_user ? A.wts_user + (size_t)t * A.k : nullptr,
+               lds);
+    if (threadIdx.x == 0) st_dev(&A.cnt_tok[t * kCounterStride], 0);
     if (!A.do_group) return;
-    release_agent();
+    wait_stores();
     __syncthreads();
     if (threadIdx.x == 0) s_flag = atomicAdd(A.cnt_all, 1) == A.T - 1;
     __syncthreads();
     if (!s_flag) return;
-    acquire_agent();
 
     // 3. last token: group the T*k (token, choice) pairs by expert.  LDS holds one bit
     // per (expert, token): expert e's tokens in token order.  counts = popcounts,
@@ -386,7 +456,7 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
     __syncthreads();
     for (int p = threadIdx.x; p < T * k; p += blockDim.x) {
         const int tt = p / k;
-        atomicOr(&mask[A.ids[p] * W + tt / 32], 1u << (tt % 32));
+        atomicOr(&mask[ld_dev(&A.ids[p]) * W + tt / 32], 1u << (tt % 32));
     }
     __syncthreads();
     // each thread owns up to 4 consecutive experts
@@ -440,11 +510,11 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
         A.meta[mi.n_mfma()] = tot[2];
         A.meta[mi.n_fallback()] = atomicExch(A.fb_acc, 0);
         A.meta[mi.n_mfma_chunks()] = tot[3];
-        *A.cnt_all = 0;
+        st_dev(A.cnt_all, 0);
     }
     __syncthreads();
     for (int p = threadIdx.x; p < T * k; p += blockDim.x) {
-        const int tt = p / k, e = A.ids[p];
+        const int tt = p / k, e = ld_dev(&A.ids[p]);
         int rank = __popc(mask[e * W + tt / 32] & ((1u << (tt % 32)) - 1u));
         for (int w = 0; w < tt / 32; ++w) rank += __popc(mask[e * W + w]);
         const int slot = offs[e] + rank;
@@ -469,9 +539,9 @@ hipError_t launch_zero(int32_t *p, int n, hipStream_t st)
 hipError_t launch_route(const Layer &L, const RouteParams &P, hipStream_t st)
 {
     // Experts per wave: enough waves to cover the GPU, few experts per wave at small T.
-    const int target_waves = 4096;
+    const int target_waves = 2048;
     int epw = (P.T * L.E + target_waves - 1) / target_waves;
-    epw = epw < 1 ? 1 : (epw > 16 ? 16 : epw);
+    epw = epw < 1 ? 1 : (epw > kEPW ? kEPW : epw);
     const int bpt = (L.E + 4 * epw - 1) / (4 * epw);
     RouteArgs A;
     A.x = P.x;
@@ -502,7 +572,9 @@ hipError_t launch_route(const Layer &L, const RouteParams &P, hipStream_t st)
     A.do_group = P.do_group;
     A.max_chunks = P.max_chunks;
     const int W = (P.T + 31) / 32;
-    const size_t lds = P.do_group ? sizeof(uint32_t) * ((size_t)L.E * W + L.E) : 0;
+    const size_t topk_words = 2 * (size_t)L.E + 2 * (size_t)P.k;
+    const size_t group_words = P.do_group ? (size_t)L.E * W + L.E : 0;
+    const size_t lds = sizeof(uint32_t) * (topk_words > group_words ? topk_words : group_words);
     dim3 grid(P.T * bpt), block(256);
     if (L.act_bf16 && L.router_bf16)
         route_kernel<uint16_t, uint16_t><<<grid, block, lds, st>>>(A);
