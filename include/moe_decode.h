@@ -86,8 +86,9 @@ typedef struct moe_decode_config {
     int32_t router_dtype;    /* moe_dtype of router_w */
     int32_t wfmt;            /* moe_wfmt of expert_w / scales */
     int32_t mfma_min_tokens; /* an expert with at least this many tokens in a step runs on
-                                MFMA tiles, below it on the GEMV path; 0 = library default,
-                                negative = never */
+                                MFMA tiles, below it on the GEMV path; 0 = library default
+                                (1: MFMA for every expert, the faster path on MI355X at
+                                every measured token count), negative = never */
     int32_t reserved[7];     /* must be zero */
 } moe_decode_config;
 

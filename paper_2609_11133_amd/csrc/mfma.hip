@@ -11,9 +11,7 @@
 // (row/column l%16, K block [32g, 32g+32)); the 16x16 fp32 result gives lane l rows
 // 4g..4g+3 of column l%16.
 //
-// Work item = (32 weight rows, chunk of up to 32 tokens of one expert) for one wave;
-// consecutive items walk the row tiles of a chunk, so the four waves of a workgroup
-// share the chunk's activation fragments through the L1 cache.
+// Every wave streams two 16-row weight tiles per work item (see stream_tiles).
 #include <hip/hip_runtime.h>
 #include <math.h>
 
@@ -71,131 +69,207 @@ struct Frags {
 };
 
 // K loop over KB blocks with an S-stage register ring: the loads of block kb+S-1 are
-// issued before block kb is multiplied, so S-1 blocks of weights stay in flight.
+// issued before block kb is multiplied, so S-1 blocks stay in flight.  The steady
+// state has no conditional loads: the compiler's wait counts are exact only when
+// every path issues the same loads, and a guarded load makes it wait for all.
 template <int S, typename FR, typename LoadF, typename CompF>
 __device__ inline void k_pipeline(int KB, FR (&F)[S], LoadF load, CompF compute)
 {
 #pragma unroll
     for (int s = 0; s < S - 1; ++s)
         if (s < KB) load(F[s], s);
-    for (int kb = 0; kb < KB; kb += S) {
+    int kb = 0;
+    for (; kb + 2 * S - 1 <= KB; kb += S) {
 #pragma unroll
         for (int s = 0; s < S; ++s) {
-            const int cur = kb + s;
-            if (cur >= KB) break;
-            if (cur + S - 1 < KB) load(F[(s + S - 1) % S], cur + S - 1);
-            compute(F[s], cur);
+            load(F[(s + S - 1) % S], kb + s + S - 1);
+            compute(F[s], kb + s);
+        }
+    }
+    // fewer than 2S-1 blocks remain; block kb+s sits in F[s % S]
+#pragma unroll
+    for (int s = 0; s < 2 * S - 2; ++s) {
+        if (kb + s < KB) {
+            if (kb + s + S - 1 < KB) load(F[(s + S - 1) % S], kb + s + S - 1);
+            compute(F[s % S], kb + s);
         }
     }
 }
 
-// ------------------------------------------------------------------ gate/up + SiLU-gate
+// ------------------------------------------------------------------ activation operand
+//
+// Activation fragments are read through raw buffer resources sized to the step's
+// data.  Lanes whose token column lies past the chunk use an offset beyond the
+// resource, which the hardware answers with zeros and no memory request: the
+// activation traffic through the L1 then scales with the chunk's real tokens, and
+// no branch guards the loads (a branch around loads makes every K block wait for
+// all outstanding loads).  An output column depends only on its own activation
+// column, and columns past the chunk are never stored.
 
-template <int FMT, int NT, int S>
-__device__ inline void w13_item(const uint8_t *__restrict__ we, const uint8_t *__restrict__ se, int H, int I, int i0,
-                                int slot0, int mc, const int32_t *__restrict__ tok_of,
-                                const uint8_t *__restrict__ xs_hi, const uint8_t *__restrict__ xs_lo,
-                                const uint8_t *__restrict__ xe_hi, const uint8_t *__restrict__ xe_lo,
-                                uint8_t *__restrict__ hs_hi, uint8_t *__restrict__ hs_lo, uint8_t *__restrict__ he_hi,
-                                uint8_t *__restrict__ he_lo, int lane)
+typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+constexpr uint32_t kOutOfRange = 0x80000000u;
+constexpr int kRawBufferWord3 = 0x00020000;  // untyped 32-bit data format, no swizzle
+
+__device__ inline __amdgpu_buffer_rsrc_t raw_rsrc(const void *base, uint32_t bytes)
 {
-    const int r = lane & 15, g = lane >> 4;
-    const int KB = H / 128;
-    const size_t rowb = FMT == 0 ? (size_t)H : (size_t)H / 2;
-    // weight rows of the four tiles: gate [i0, i0+16), gate [i0+16, i0+32), up likewise
-    const uint8_t *arow[4];
-    const uint8_t *erow[4];
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, kRawBufferWord3);
+}
+
+// FP8 fragment of a K block: bytes [16g, 16g+16) and [64+16g, 64+16g+16) at voff+soff.
+__device__ inline i32x8 frag_buf(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff)
+{
+    const u32x4v a = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    const u32x4v b = __builtin_amdgcn_raw_buffer_load_b128(r, voff + 64, soff, 0);
+    return (i32x8){(int)a.x, (int)a.y, (int)a.z, (int)a.w, (int)b.x, (int)b.y, (int)b.z, (int)b.w};
+}
+
+// The four resources of a split activation buffer [rows][K] (hi, lo codes) and
+// [rows][K/32] (hi, lo exponents) holding `rows` rows.
+struct ActRsrc {
+    __amdgpu_buffer_rsrc_t hi, lo, ehi, elo;
+};
+
+__device__ inline ActRsrc act_rsrc(const uint8_t *hi, const uint8_t *lo, const uint8_t *ehi, const uint8_t *elo,
+                                   uint32_t rows, uint32_t K)
+{
+    return ActRsrc{raw_rsrc(hi, rows * K), raw_rsrc(lo, rows * K), raw_rsrc(ehi, rows * (K / 32)),
+                   raw_rsrc(elo, rows * (K / 32))};
+}
+
+// ------------------------------------------------------------------ two weight tiles
+//
+// A wave streams two 16-row weight tiles (this lane's rows arow[0], arow[1]) over KB
+// K blocks against NT 16-token tiles, accumulating acc[t][j] (lane l: rows 4g..4g+3
+// of token column l%16).  Two tiles per wave balance the two costs measured on this
+// GPU: each extra concurrently streamed tile lowers the HBM rate (one: 6.3 TB/s,
+// four: 5.2 TB/s), each activation fragment load is paid per tile pair.
+//   arow[t]  weight row of this lane in tile t (FP8: KB*128 bytes, E2M1: KB*64 bytes)
+//   erow[t]  E8M0 scales of that row (E2M1 only), one per 32 inputs
+//   sblk[t]  fp32 block scale of tile t per K block (FP8 only)
+//   voff[j], eoff[j]  this lane's byte offset of its token row in the code and
+//                     exponent buffers (kOutOfRange past the chunk)
+template <int FMT, int NT, int S>
+__device__ inline void stream_tiles(f32x4 (&acc)[2][NT], const uint8_t *const (&arow)[2],
+                                    const uint8_t *const (&erow)[2], const float *const (&sblk)[2], int KB,
+                                    const ActRsrc &B, const uint32_t (&voff)[NT], const uint32_t (&eoff)[NT], int g)
+{
+    auto load = [&](Frags<2, NT> &F, int kb) {
 #pragma unroll
-    for (int at = 0; at < 4; ++at) {
-        const int row = (at < 2 ? 0 : I) + i0 + 16 * (at & 1) + r;
-        arow[at] = we + (size_t)row * rowb;
-        erow[at] = se + (size_t)row * (H / 32);  // MXFP4 scale rows (gate then up, same stride)
-    }
-    const float *sg = (const float *)se + (size_t)(i0 / 128) * (H / 128);  // FP8 block scales
-    const float *su = sg + (size_t)(I / 128) * (H / 128);
-    // this lane's token in each 16-column tile
-    int tok[NT];
-    bool valid[NT];
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-        const int m = 16 * j + r;
-        valid[j] = m < mc;
-        tok[j] = valid[j] ? tok_of[slot0 + m] : 0;
-    }
-    auto load = [&](Frags<4, NT> &F, int kb) {
-#pragma unroll
-        for (int at = 0; at < 4; ++at) {
+        for (int t = 0; t < 2; ++t) {
             if constexpr (FMT == 0) {
-                F.a[at] = frag_fp8(arow[at] + (size_t)kb * 128, g);
-                F.ea[at] = 127;
+                F.a[t] = frag_fp8(arow[t] + (size_t)kb * 128, g);
+                F.ea[t] = 127;
             } else {
-                F.a[at] = frag_fp4(arow[at] + (size_t)kb * 64, g);
-                F.ea[at] = erow[at][kb * 4 + g];
+                F.a[t] = frag_fp4(arow[t] + (size_t)kb * 64, g);
+                F.ea[t] = erow[t][kb * 4 + g];
             }
         }
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
-            const size_t xo = (size_t)tok[j] * H + (size_t)kb * 128;
-            const size_t eo = (size_t)tok[j] * (H / 32) + kb * 4 + g;
-            F.bh[j] = frag_fp8(xs_hi + xo, g);
-            F.bl[j] = frag_fp8(xs_lo + xo, g);
-            F.eh[j] = xe_hi[eo];
-            F.el[j] = xe_lo[eo];
-            if (!valid[j]) {
-                F.bh[j] = (i32x8){0, 0, 0, 0, 0, 0, 0, 0};
-                F.bl[j] = F.bh[j];
-            }
+            F.bh[j] = frag_buf(B.hi, voff[j], kb * 128);
+            F.bl[j] = frag_buf(B.lo, voff[j], kb * 128);
+            F.eh[j] = __builtin_amdgcn_raw_buffer_load_b8(B.ehi, eoff[j], kb * 4, 0);
+            F.el[j] = __builtin_amdgcn_raw_buffer_load_b8(B.elo, eoff[j], kb * 4, 0);
         }
     };
-    f32x4 acc[4][NT];
 #pragma unroll
-    for (int at = 0; at < 4; ++at)
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int j = 0; j < NT; ++j) acc[at][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
-    auto compute = [&](const Frags<4, NT> &F, int kb) {
-        const float s_g = FMT == 0 ? sg[kb] : 1.f, s_u = FMT == 0 ? su[kb] : 1.f;
+        for (int j = 0; j < NT; ++j) acc[t][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    auto compute = [&](const Frags<2, NT> &F, int kb) {
 #pragma unroll
-        for (int at = 0; at < 4; ++at)
+        for (int t = 0; t < 2; ++t) {
+            const float s = FMT == 0 ? sblk[t][kb] : 1.f;
 #pragma unroll
             for (int j = 0; j < NT; ++j)
-                mma2<FMT>(acc[at][j], F.a[at], F.ea[at], at < 2 ? s_g : s_u, F.bh[j], F.eh[j], F.bl[j], F.el[j]);
+                mma2<FMT>(acc[t][j], F.a[t], F.ea[t], s, F.bh[j], F.eh[j], F.bl[j], F.el[j]);
+        }
     };
-    Frags<4, NT> F[S];
+    Frags<2, NT> F[S];
     k_pipeline<S>(KB, F, load, compute);
-    // epilogue: h = silu(g) * u for rows i0 + {4g+i, 16+4g+i}, then the 2-term split of
-    // the 32-row group [i0, i0+32) of each token (the group spans the four lanes of a
-    // column: l, l^16, l^32, l^48).
+}
+
+// This lane's token-row offsets for the NT token tiles of a chunk.
+template <int NT>
+__device__ inline void token_offsets(uint32_t (&voff)[NT], uint32_t (&eoff)[NT], const int32_t *__restrict__ row_of,
+                                     int slot0, int mc, int K, int r, int g)
+{
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
-        float h[8], res[8];
+        const int m = 16 * j + r;
+        const uint32_t row = m < mc ? (uint32_t)(row_of ? row_of[slot0 + m] : slot0 + m) : 0u;
+        voff[j] = m < mc ? row * (uint32_t)K + 16u * g : kOutOfRange;
+        eoff[j] = m < mc ? row * (uint32_t)(K / 32) + (uint32_t)g : kOutOfRange;
+    }
+}
+
+// ------------------------------------------------------------------ gate/up + SiLU-gate
+//
+// Work item = (chunk of up to 32 tokens of one expert, rows [i0, i0+64) of the
+// intermediate dimension) for a workgroup of four waves.  Wave w takes rows
+// r0 = i0 + 16w .. r0+16 of both the gate and the up matrix, so h = silu(g)*u forms
+// in its registers.  The 2-term split of h groups 32 rows (one E8M0 exponent per
+// token and group): waves 2q and 2q+1 share group q and exchange their column
+// maxima through LDS.
+
+template <int FMT, int NT, int S>
+__device__ inline void w13_rows(int w, const uint8_t *__restrict__ we, const uint8_t *__restrict__ se, int H, int I,
+                                int i0, int slot0, int mc, const int32_t *__restrict__ tok_of, const ActRsrc &X,
+                                uint8_t *__restrict__ hs_hi, uint8_t *__restrict__ hs_lo,
+                                uint8_t *__restrict__ he_hi, uint8_t *__restrict__ he_lo, float (&s_am)[4][2][16],
+                                float (&s_rm)[4][2][16], int lane)
+{
+    const int r = lane & 15, g = lane >> 4;
+    const int r0 = i0 + 16 * w;  // first row of this wave in the gate and in the up matrix
+    const size_t rowb = FMT == 0 ? (size_t)H : (size_t)H / 2;
+    const uint8_t *arow[2] = {we + (size_t)(r0 + r) * rowb, we + (size_t)(I + r0 + r) * rowb};
+    const uint8_t *erow[2] = {se + (size_t)(r0 + r) * (H / 32), se + (size_t)(I + r0 + r) * (H / 32)};
+    const float *sblk[2] = {(const float *)se + (size_t)(r0 / 128) * (H / 128),
+                            (const float *)se + (size_t)((I + r0) / 128) * (H / 128)};
+    uint32_t voff[NT], eoff[NT];
+    token_offsets<NT>(voff, eoff, tok_of, slot0, mc, H, r, g);
+    f32x4 acc[2][NT];
+    stream_tiles<FMT, NT, S>(acc, arow, erow, sblk, H / 128, X, voff, eoff, g);
+
+    // epilogue: h = silu(g)*u for rows r0 + 4g + i of token column r of each tile
+    float h[NT][4], res[NT][4];
+    float am[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const float g0 = acc[0][j][i], g1 = acc[1][j][i];
-            h[i] = g0 / (1.0f + expf(-g0)) * acc[2][j][i];
-            h[4 + i] = g1 / (1.0f + expf(-g1)) * acc[3][j][i];
+            const float gi = acc[0][j][i];
+            h[j][i] = gi / (1.0f + expf(-gi)) * acc[1][j][i];
         }
-        float am = amax_of(h);
-        am = fmaxf(am, __shfl_xor(am, 16));
-        am = fmaxf(am, __shfl_xor(am, 32));
-        const int ch = exp_for_group(am);
-        uint32_t qh[2], ql[2];
-        split_hi(h, ch, qh, res);
-        float rm = amax_of(res);
-        rm = fmaxf(rm, __shfl_xor(rm, 16));
-        rm = fmaxf(rm, __shfl_xor(rm, 32));
-        const int cl = exp_for_group(rm);
-        split_lo(res, cl, ql);
-        if (valid[j]) {
+        float m = amax_of(h[j]);
+        m = fmaxf(m, __shfl_xor(m, 16));
+        am[j] = fmaxf(m, __shfl_xor(m, 32));
+        if (g == 0) s_am[w][j][r] = am[j];
+    }
+    __syncthreads();
+    int ch[NT];
+    uint32_t qh[NT][1], ql[NT][1];
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+        ch[j] = exp_for_group(fmaxf(am[j], s_am[w ^ 1][j][r]));
+        split_hi(h[j], ch[j], qh[j], res[j]);
+        float m = amax_of(res[j]);
+        m = fmaxf(m, __shfl_xor(m, 16));
+        am[j] = fmaxf(m, __shfl_xor(m, 32));
+        if (g == 0) s_rm[w][j][r] = am[j];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+        const int cl = exp_for_group(fmaxf(am[j], s_rm[w ^ 1][j][r]));
+        split_lo(res[j], cl, ql[j]);
+        if (16 * j + r < mc) {
             const size_t slot = (size_t)slot0 + 16 * j + r;
-            uint8_t *ph = hs_hi + slot * I + i0 + 4 * g;
-            uint8_t *pl = hs_lo + slot * I + i0 + 4 * g;
-            *reinterpret_cast<uint32_t *>(ph) = qh[0];
-            *reinterpret_cast<uint32_t *>(ph + 16) = qh[1];
-            *reinterpret_cast<uint32_t *>(pl) = ql[0];
-            *reinterpret_cast<uint32_t *>(pl + 16) = ql[1];
-            if (g == 0) {
-                he_hi[slot * (I / 32) + i0 / 32] = (uint8_t)ch;
-                he_lo[slot * (I / 32) + i0 / 32] = (uint8_t)cl;
+            *reinterpret_cast<uint32_t *>(hs_hi + slot * I + r0 + 4 * g) = qh[j][0];
+            *reinterpret_cast<uint32_t *>(hs_lo + slot * I + r0 + 4 * g) = ql[j][0];
+            if ((w & 1) == 0 && g == 0) {
+                he_hi[slot * (I / 32) + r0 / 32] = (uint8_t)ch[j];
+                he_lo[slot * (I / 32) + r0 / 32] = (uint8_t)cl;
             }
         }
     }
@@ -210,103 +284,60 @@ __global__ __launch_bounds__(256) void w13_mfma_kernel(const uint8_t *__restrict
                                                        const uint8_t *__restrict__ xe_hi,
                                                        const uint8_t *__restrict__ xe_lo, uint8_t *__restrict__ hs_hi,
                                                        uint8_t *__restrict__ hs_lo, uint8_t *__restrict__ he_hi,
-                                                       uint8_t *__restrict__ he_lo, int H, int I, int E, size_t ewb,
-                                                       size_t esb)
+                                                       uint8_t *__restrict__ he_lo, int T, int H, int I, int E,
+                                                       size_t ewb, size_t esb)
 {
+    __shared__ float s_am[4][2][16], s_rm[4][2][16];
     const MetaIdx mi{E};
-    const int tiles = I / 32;
+    const int tiles = I / 64;
     const int n_items = meta[mi.n_mfma_chunks()] * tiles;
     const int4 *recs = reinterpret_cast<const int4 *>(meta + mi.chunk_rec());
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    for (int item = blockIdx.x * 4 + wave; item < n_items; item += gridDim.x * 4) {
+    const ActRsrc X = act_rsrc(xs_hi, xs_lo, xe_hi, xe_lo, (uint32_t)T, (uint32_t)H);
+    for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
         const int4 rec = recs[item / tiles];  // {expert, first slot, tokens, -}
-        const int i0 = (item % tiles) * 32;
+        const int i0 = (item % tiles) * 64;
         const uint8_t *we = ew + (size_t)rec.x * ewb;
         const uint8_t *se = es + (size_t)rec.x * esb;
         if (rec.z > 16)
-            w13_item<FMT, 2, 2>(we, se, H, I, i0, rec.y, rec.z, tok_of, xs_hi, xs_lo, xe_hi, xe_lo, hs_hi, hs_lo,
-                                he_hi, he_lo, lane);
+            w13_rows<FMT, 2, 2>(wave, we, se, H, I, i0, rec.y, rec.z, tok_of, X, hs_hi, hs_lo, he_hi, he_lo, s_am,
+                                s_rm, lane);
         else
-            w13_item<FMT, 1, 3>(we, se, H, I, i0, rec.y, rec.z, tok_of, xs_hi, xs_lo, xe_hi, xe_lo, hs_hi, hs_lo,
-                                he_hi, he_lo, lane);
+            w13_rows<FMT, 1, 3>(wave, we, se, H, I, i0, rec.y, rec.z, tok_of, X, hs_hi, hs_lo, he_hi, he_lo, s_am,
+                                s_rm, lane);
     }
 }
 
 // ------------------------------------------------------------------ down projection
+//
+// Work item = (chunk of up to 32 tokens of one expert, 32 output rows [n0, n0+32)) for
+// one wave; the four waves of a workgroup take consecutive row pairs of a chunk and
+// so share its activation fragments through the L1 cache.
 
 template <int FMT, int NT, int S>
-__device__ inline void w2_item(const uint8_t *__restrict__ we2, const uint8_t *__restrict__ se, int H, int I, int n0,
-                               int slot0, int mc, const uint8_t *__restrict__ hs_hi,
-                               const uint8_t *__restrict__ hs_lo, const uint8_t *__restrict__ he_hi,
-                               const uint8_t *__restrict__ he_lo, float *__restrict__ obuf, int lane)
+__device__ inline void w2_rows(const uint8_t *__restrict__ we2, const uint8_t *__restrict__ se, int H, int I, int n0,
+                               int slot0, int mc, const ActRsrc &Hs, float *__restrict__ obuf, int lane)
 {
     const int r = lane & 15, g = lane >> 4;
-    const int KB = I / 128;
     const size_t rowb = FMT == 0 ? (size_t)I : (size_t)I / 2;
-    const uint8_t *arow[2];
-    const uint8_t *erow[2];
     const uint8_t *sd8 = se + (size_t)2 * I * (H / 32);  // MXFP4 down scales
-#pragma unroll
-    for (int at = 0; at < 2; ++at) {
-        const int row = n0 + 16 * at + r;
-        arow[at] = we2 + (size_t)row * rowb;
-        erow[at] = sd8 + (size_t)row * (I / 32);
-    }
-    const float *sd = (const float *)se + (size_t)2 * (I / 128) * (H / 128) + (size_t)(n0 / 128) * (I / 128);
-    size_t slot[NT];
-    bool valid[NT];
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-        const int m = 16 * j + r;
-        valid[j] = m < mc;
-        slot[j] = (size_t)slot0 + (valid[j] ? m : 0);
-    }
-    auto load = [&](Frags<2, NT> &F, int kb) {
-#pragma unroll
-        for (int at = 0; at < 2; ++at) {
-            if constexpr (FMT == 0) {
-                F.a[at] = frag_fp8(arow[at] + (size_t)kb * 128, g);
-                F.ea[at] = 127;
-            } else {
-                F.a[at] = frag_fp4(arow[at] + (size_t)kb * 64, g);
-                F.ea[at] = erow[at][kb * 4 + g];
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < NT; ++j) {
-            const size_t ho = slot[j] * I + (size_t)kb * 128;
-            const size_t eo = slot[j] * (I / 32) + kb * 4 + g;
-            F.bh[j] = frag_fp8(hs_hi + ho, g);
-            F.bl[j] = frag_fp8(hs_lo + ho, g);
-            F.eh[j] = he_hi[eo];
-            F.el[j] = he_lo[eo];
-            if (!valid[j]) {
-                F.bh[j] = (i32x8){0, 0, 0, 0, 0, 0, 0, 0};
-                F.bl[j] = F.bh[j];
-            }
-        }
-    };
+    const uint8_t *arow[2] = {we2 + (size_t)(n0 + r) * rowb, we2 + (size_t)(n0 + 16 + r) * rowb};
+    const uint8_t *erow[2] = {sd8 + (size_t)(n0 + r) * (I / 32), sd8 + (size_t)(n0 + 16 + r) * (I / 32)};
+    const float *sd = (const float *)se + (size_t)2 * (I / 128) * (H / 128);
+    const float *sblk[2] = {sd + (size_t)(n0 / 128) * (I / 128), sd + (size_t)((n0 + 16) / 128) * (I / 128)};
+    uint32_t voff[NT], eoff[NT];
+    token_offsets<NT>(voff, eoff, nullptr, slot0, mc, I, r, g);
     f32x4 acc[2][NT];
-#pragma unroll
-    for (int at = 0; at < 2; ++at)
-#pragma unroll
-        for (int j = 0; j < NT; ++j) acc[at][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
-    auto compute = [&](const Frags<2, NT> &F, int kb) {
-        const float s = FMT == 0 ? sd[kb] : 1.f;
-#pragma unroll
-        for (int at = 0; at < 2; ++at)
-#pragma unroll
-            for (int j = 0; j < NT; ++j) mma2<FMT>(acc[at][j], F.a[at], F.ea[at], s, F.bh[j], F.eh[j], F.bl[j], F.el[j]);
-    };
-    Frags<2, NT> F[S];
-    k_pipeline<S>(KB, F, load, compute);
+    stream_tiles<FMT, NT, S>(acc, arow, erow, sblk, I / 128, Hs, voff, eoff, g);
 #pragma unroll
     for (int j = 0; j < NT; ++j)
-        if (valid[j])
+        if (16 * j + r < mc) {
+            const size_t slot = (size_t)slot0 + 16 * j + r;
 #pragma unroll
-            for (int at = 0; at < 2; ++at)
-                *reinterpret_cast<f32x4 *>(obuf + slot[j] * H + n0 + 16 * at + 4 * g) = acc[at][j];
+            for (int t = 0; t < 2; ++t)
+                *reinterpret_cast<f32x4 *>(obuf + slot * H + n0 + 16 * t + 4 * g) = acc[t][j];
+        }
 }
 
 template <int FMT>
@@ -316,7 +347,7 @@ __global__ __launch_bounds__(256) void w2_mfma_kernel(const uint8_t *__restrict_
                                                       const uint8_t *__restrict__ hs_lo,
                                                       const uint8_t *__restrict__ he_hi,
                                                       const uint8_t *__restrict__ he_lo, float *__restrict__ obuf,
-                                                      int H, int I, int E, size_t ewb, size_t esb)
+                                                      int P, int H, int I, int E, size_t ewb, size_t esb)
 {
     const MetaIdx mi{E};
     const int tiles = H / 32;
@@ -325,24 +356,26 @@ __global__ __launch_bounds__(256) void w2_mfma_kernel(const uint8_t *__restrict_
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const size_t w2off = FMT == 0 ? (size_t)2 * I * H : (size_t)I * H;
+    const ActRsrc Hs = act_rsrc(hs_hi, hs_lo, he_hi, he_lo, (uint32_t)P, (uint32_t)I);
     for (int item = blockIdx.x * 4 + wave; item < n_items; item += gridDim.x * 4) {
         const int4 rec = recs[item / tiles];
         const int n0 = (item % tiles) * 32;
         const uint8_t *we2 = ew + (size_t)rec.x * ewb + w2off;
         const uint8_t *se = es + (size_t)rec.x * esb;
         if (rec.z > 16)
-            w2_item<FMT, 2, 2>(we2, se, H, I, n0, rec.y, rec.z, hs_hi, hs_lo, he_hi, he_lo, obuf, lane);
+            w2_rows<FMT, 2, 2>(we2, se, H, I, n0, rec.y, rec.z, Hs, obuf, lane);
         else
-            w2_item<FMT, 1, 3>(we2, se, H, I, n0, rec.y, rec.z, hs_hi, hs_lo, he_hi, he_lo, obuf, lane);
+            w2_rows<FMT, 1, 3>(we2, se, H, I, n0, rec.y, rec.z, Hs, obuf, lane);
     }
 }
 
-int mfma_grid(const Layer &L, int T, int k, int tiles)
+// Workgroups for `items_per_chunk` items per chunk record, `per_block` items per workgroup.
+int mfma_grid(const Layer &L, int T, int k, int items_per_chunk, int per_block)
 {
     const long pairs = (long)T * k;
     const long recs = pairs < L.E ? pairs : L.E;
     const long chunks = recs + (pairs + kMfmaChunk - 1) / kMfmaChunk;  // >= number of chunk records
-    const long blocks = (chunks * tiles + 3) / 4;
+    const long blocks = (chunks * items_per_chunk + per_block - 1) / per_block;
     return blocks < 1 ? 1 : (blocks > 65535 ? 65535 : (int)blocks);
 }
 
@@ -351,15 +384,15 @@ int mfma_grid(const Layer &L, int T, int k, int tiles)
 hipError_t launch_w13_mfma(const Layer &L, const void *expert_w, const void *scales, int T, int k,
                            const int32_t *meta, const int32_t *tok_of, const Workspace &ws, hipStream_t st)
 {
-    dim3 grid(mfma_grid(L, T, k, L.I / 32)), block(256);
+    dim3 grid(mfma_grid(L, T, k, L.I / 64, 1)), block(256);
     const uint8_t *ew = (const uint8_t *)expert_w, *es = (const uint8_t *)scales;
     if (L.wfmt == 0)
         w13_mfma_kernel<0><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.xs_hi, ws.xs_lo, ws.xe_hi, ws.xe_lo,
-                                                   ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, L.H, L.I, L.E,
+                                                   ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, T, L.H, L.I, L.E,
                                                    L.expert_w_bytes, L.expert_s_bytes);
     else
         w13_mfma_kernel<1><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.xs_hi, ws.xs_lo, ws.xe_hi, ws.xe_lo,
-                                                   ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, L.H, L.I, L.E,
+                                                   ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, T, L.H, L.I, L.E,
                                                    L.expert_w_bytes, L.expert_s_bytes);
     return hipGetLastError();
 }
@@ -367,14 +400,14 @@ hipError_t launch_w13_mfma(const Layer &L, const void *expert_w, const void *sca
 hipError_t launch_w2_mfma(const Layer &L, const void *expert_w, const void *scales, int T, int k,
                           const int32_t *meta, const Workspace &ws, hipStream_t st)
 {
-    dim3 grid(mfma_grid(L, T, k, L.H / 32)), block(256);
+    dim3 grid(mfma_grid(L, T, k, L.H / 32, 4)), block(256);
     const uint8_t *ew = (const uint8_t *)expert_w, *es = (const uint8_t *)scales;
     if (L.wfmt == 0)
-        w2_mfma_kernel<0><<<grid, block, 0, st>>>(ew, es, meta, ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, ws.o, L.H,
-                                                  L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
+        w2_mfma_kernel<0><<<grid, block, 0, st>>>(ew, es, meta, ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, ws.o, T * k,
+                                                  L.H, L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
     else
-        w2_mfma_kernel<1><<<grid, block, 0, st>>>(ew, es, meta, ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, ws.o, L.H,
-                                                  L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
+        w2_mfma_kernel<1><<<grid, block, 0, st>>>(ew, es, meta, ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, ws.o, T * k,
+                                                  L.H, L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
     return hipGetLastError();
 }
 
