@@ -20,6 +20,7 @@ CPU oracle timed on this host's cores on a bounded sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -34,6 +35,37 @@ if ROOT not in sys.path:
 
 PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, published
 METRIC = "MoE decode-layer tokens/s and achieved HBM GB/s (% of peak) vs batch size"
+CSRC = os.path.join(ROOT, "paper_2609_11133_amd", "csrc")
+# sources the gate/up MFMA kernel is compiled from: a counter profile is valid only
+# for the kernel it was taken on
+W13_SOURCES = ["mfma.hip", "fp8split.h", "moe_internal.h"]
+
+
+def w13_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in W13_SOURCES:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def w13_traffic(cfg, T):
+    """HBM bytes per launch of the gate/up MFMA kernel from the committed counter
+    profile of this workload (FETCH_SIZE + WRITE_SIZE, each scaled by what the same
+    counter reads for a copy kernel of known size); None if there is no profile or
+    the kernel sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"w13_mfma_{cfg.name}_T{T}_traffic.txt")
+    if not os.path.exists(path):
+        return None, "no counter profile for this workload"
+    kv = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith((" ", "#")):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("kernel_source_sha256") != w13_source_hash():
+        return None, f"{os.path.relpath(path, ROOT)} was taken on an older kernel"
+    return float(kv["traffic_bytes_per_launch"]), os.path.relpath(path, ROOT)
 
 
 def parse():
@@ -108,7 +140,8 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     cfg = C.BY_NAME[args.config]
-    T_main = args.tokens or max(t for t in cfg.tokens if t <= 64)
+    small = [t for t in cfg.tokens if t <= 64]
+    T_main = args.tokens or (max(small) if small else min(cfg.tokens))
     sweep_T = sorted(set(cfg.tokens) | {T_main}) if not args.no_sweep else [T_main]
     Tmax = max(sweep_T)
     layer_bytes = cfg.n_experts * (cfg.expert_weight_bytes() + cfg.expert_scale_bytes())
@@ -233,6 +266,7 @@ def main():
                           f"{dt:.1f} s wall")
 
     R = results[T_main]
+    traffic, traffic_src = w13_traffic(cfg, T_main)
     line = {
         "metric": METRIC,
         "value": R["tokens_per_s"],
@@ -244,7 +278,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "fp8" if cfg.wfmt == "fp8" else "fp4",
         "data": "synthetic",
         "config": {
             "workload": f"{cfg.name} MoE decode layer: hidden {cfg.hidden}, {cfg.n_experts} experts, top-{cfg.topk}, "
@@ -264,13 +298,15 @@ def main():
             "n_active_mean": R["n_active_mean"],
         },
         "roofline": {
-            "kernel": "w13 (grouped gate/up + SiLU-gate)",
+            "kernel": ("w13_mfma_kernel (grouped gate/up + SiLU-gate, MFMA for every expert)"
+                       if args.mstar in (0, 1) else "w13 stage (GEMV and MFMA kernels)"),
             "bound": "hbm",
             "achieved": R["w13_GBs"],
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",
             "frac": R["w13_GBs"] / PEAK_HBM_GBS,
-            "traffic": None,
+            "traffic": traffic,
+            "traffic_source": traffic_src,
             "avg_launch_us": R["stage_ms"]["w13"] * 1e3,
             "bytes_per_launch": R["w13_bytes_per_launch"],
         },
