@@ -226,6 +226,25 @@ def test_max_tokens(dev):
     check_layer(run, W.host_x(cfg, 1024, seed=510), tokens=[0, 511, 1023], label="T=1024")
 
 
+# LDS-staged MFMA kernels (K spanning a multiple of four 128-input blocks; the down
+# projection from 16 blocks): small layers whose I reaches them, with Zipf skew so that
+# some expert holds more than 16 tokens (32-token tiles) and others a single one.
+LDS_FP8 = LayerConfig("lds-fp8", 512, 16, 4, 2048, "bf16", "bf16", "fp8", "zipf:1.1", [])
+LDS_MX = LayerConfig("lds-mxfp4", 1024, 16, 4, 2048, "bf16", "bf16", "mxfp4", "zipf:1.1", [])
+
+
+@pytest.mark.parametrize("cfg", [LDS_FP8, LDS_MX], ids=["fp8", "mxfp4"])
+@pytest.mark.parametrize("T", [1, 7, 32])
+def test_lds_staged_kernels(dev, cfg, T):
+    hl = W.host_layer(cfg, seed=530)
+    run = Run(cfg, hl, dev, max_tokens=32)
+    check_layer(run, W.host_x(cfg, T, seed=530 + T), label=f"{cfg.name} T={T}")
+    st, counts = run.m.stats()
+    say(f"[lds] {cfg.name} T={T}: tokens per expert {sorted(counts, reverse=True)[:4]}")
+    if T == 32:
+        assert max(counts) > 16
+
+
 # ---------------------------------------------------------------- full-size layers
 
 @pytest.fixture(scope="module")
