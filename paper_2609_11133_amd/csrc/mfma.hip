@@ -375,19 +375,19 @@ __global__ __launch_bounds__(256) void w2_mfma_kernel(const uint8_t *__restrict_
 // item is one workgroup of four waves over one chunk, and each wave streams exactly
 // one 16-row weight tile with a four-deep register ring.  The chunk's split
 // activations are staged once per workgroup in LDS, in double-buffered segments of
-// two K blocks, and every wave reads its fragments from there.  Measured on this GPU,
+// four K blocks, and every wave reads its fragments from there.  Measured on this GPU,
 // a wave streaming one tile reaches 6.3 TB/s and one streaming two 5.6 TB/s, but one
 // tile per wave pays a full activation fragment per weight fragment when each wave
 // fetches its own; staging removes that cost.
 
-constexpr int kSegK = 2;                // K blocks per staged segment
+constexpr int kSegK = 4;                // K blocks per staged segment
 constexpr int kSegBytes = kSegK * 128;  // activation bytes per token row and segment
 constexpr int kStageTok = 32;           // token rows of a chunk
 
 struct ActSeg {
     uint8_t code[2][kStageTok][kSegBytes];  // [hi, lo][token][16-byte pieces, swizzled]
     uint8_t ex[2][kStageTok][kSegK * 4];    // [hi, lo][token][E8M0 per 32 inputs]
-    uint8_t sink[8];                        // target of the threads that stage no exponents
+    uint8_t sink[kSegK * 4];                // target of the threads that stage no exponents
 };
 
 // Piece c (16 bytes) of token t's row is stored at piece swz(c, t): the piece index
@@ -397,30 +397,29 @@ __device__ inline int swz(int c, int t) { return (c & ~7) | ((c ^ t) & 7); }
 
 __device__ inline void sync_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
-
-// One thread's share of staging a segment: token row 16p + tid/16, piece tid%16, for
-// each 16-token part p < NT, in both the hi and lo codes; threads tid < 32 also stage
-// token tid's 8 exponent bytes of each.  Every thread issues the same loads (tokens
-// past the chunk read out of range), so the loads need no branch.
+// One thread's share of staging a segment: piece tid%32 of token rows 8q + tid/32
+// (q < 2*NT) in both the hi and lo codes; threads tid < 32 also stage token tid's
+// exponent bytes of each.  Every thread issues the same loads (tokens past the chunk
+// read out of range), so the loads need no branch.
 template <int NT>
 struct Stager {
-    uint32_t voff[NT];  // byte offset of this thread's piece in its token row, segment 0
-    uint32_t eoff;      // exponent offset of token tid, segment 0 (out of range if none)
-    int tok[NT];
+    static constexpr int Q = 2 * NT;
+    uint32_t voff[Q];  // byte offset of this thread's piece in its token rows, segment 0
+    uint32_t eoff;     // exponent offset of token tid, segment 0 (out of range if none)
+    int tok[Q];
     int piece;
-    u32x4v code[2][NT];
-    u32x2v ex[2];
+    u32x4v code[2][Q];
+    u32x4v ex[2];
 
     __device__ void init(const int32_t *__restrict__ row_of, int slot0, int mc, int K, int tid)
     {
-        piece = tid & 15;
+        piece = tid & 31;
 #pragma unroll
-        for (int p = 0; p < NT; ++p) {
-            const int t = 16 * p + (tid >> 4);
-            tok[p] = t;
+        for (int q = 0; q < Q; ++q) {
+            const int t = 8 * q + (tid >> 5);
+            tok[q] = t;
             const uint32_t row = t < mc ? (uint32_t)(row_of ? row_of[slot0 + t] : slot0 + t) : 0u;
-            voff[p] = t < mc ? row * (uint32_t)K + 16u * piece : kOutOfRange;
+            voff[q] = t < mc ? row * (uint32_t)K + 16u * piece : kOutOfRange;
         }
         const uint32_t erow = tid < mc ? (uint32_t)(row_of ? row_of[slot0 + tid] : slot0 + tid) : 0u;
         eoff = (tid < 32 && tid < mc) ? erow * (uint32_t)(K / 32) : kOutOfRange;
@@ -430,31 +429,31 @@ struct Stager {
     {
         const uint32_t d = (uint32_t)sg * kSegBytes, de = (uint32_t)sg * (kSegK * 4);
 #pragma unroll
-        for (int p = 0; p < NT; ++p) {
-            code[0][p] = __builtin_amdgcn_raw_buffer_load_b128(B.hi, voff[p] + d, 0, 0);
-            code[1][p] = __builtin_amdgcn_raw_buffer_load_b128(B.lo, voff[p] + d, 0, 0);
+        for (int q = 0; q < Q; ++q) {
+            code[0][q] = __builtin_amdgcn_raw_buffer_load_b128(B.hi, voff[q] + d, 0, 0);
+            code[1][q] = __builtin_amdgcn_raw_buffer_load_b128(B.lo, voff[q] + d, 0, 0);
         }
-        ex[0] = __builtin_amdgcn_raw_buffer_load_b64(B.ehi, eoff + de, 0, 0);
-        ex[1] = __builtin_amdgcn_raw_buffer_load_b64(B.elo, eoff + de, 0, 0);
+        ex[0] = __builtin_amdgcn_raw_buffer_load_b128(B.ehi, eoff + de, 0, 0);
+        ex[1] = __builtin_amdgcn_raw_buffer_load_b128(B.elo, eoff + de, 0, 0);
     }
     __device__ void store(ActSeg &S, int tid) const
     {
 #pragma unroll
         for (int h = 0; h < 2; ++h)
 #pragma unroll
-            for (int p = 0; p < NT; ++p)
-                *reinterpret_cast<u32x4v *>(&S.code[h][tok[p]][swz(piece, tok[p]) * 16]) = code[h][p];
+            for (int q = 0; q < Q; ++q)
+                *reinterpret_cast<u32x4v *>(&S.code[h][tok[q]][swz(piece, tok[q]) * 16]) = code[h][q];
         uint8_t *e0 = tid < 32 ? &S.ex[0][tid][0] : S.sink;
         uint8_t *e1 = tid < 32 ? &S.ex[1][tid][0] : S.sink;
-        *reinterpret_cast<u32x2v *>(e0) = ex[0];
-        *reinterpret_cast<u32x2v *>(e1) = ex[1];
+        *reinterpret_cast<u32x4v *>(e0) = ex[0];
+        *reinterpret_cast<u32x4v *>(e1) = ex[1];
     }
 };
 
 // Streams this wave's weight tile (this lane's row `arow`) over KB K blocks (KB a
 // multiple of 4) against NT staged token tiles; acc[j] as in stream_tiles.  All
 // four waves of the workgroup call it together: it synchronises them once per
-// staged segment.
+// staged segment (four K blocks).
 template <int FMT, int NT>
 __device__ inline void stream_tile_lds(f32x4 (&acc)[NT], const uint8_t *__restrict__ arow,
                                        const uint8_t *__restrict__ erow, const float *__restrict__ sblk, int KB,
@@ -496,19 +495,17 @@ __device__ inline void stream_tile_lds(f32x4 (&acc)[NT], const uint8_t *__restri
     st.store(seg[0], tid);
     st.load(B, nseg > 1 ? 1 : 0);
     sync_lds();
-    for (int kb = 0; kb < KB; kb += 4) {
+    for (int kb = 0; kb < KB; kb += kSegK) {  // one staged segment per iteration
+        const int sg = kb / kSegK;
+        const ActSeg &cur = seg[sg & 1];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int blk = kb + u;
-            loadA((u + 3) & 3, min(blk + 3, KB - 1));  // past the end: reload the last block
-            compute(u, seg[(u / kSegK) & 1], u % kSegK, blk);
-            if (u % kSegK == kSegK - 1) {  // end of segment blk/kSegK
-                const int sg = blk / kSegK;
-                st.store(seg[(sg + 1) & 1], tid);
-                st.load(B, min(sg + 2, nseg - 1));
-                sync_lds();
-            }
+        for (int u = 0; u < kSegK; ++u) {
+            loadA((u + 3) & 3, min(kb + u + 3, KB - 1));  // past the end: reload the last block
+            compute(u, cur, u, kb + u);
         }
+        st.store(seg[(sg + 1) & 1], tid);
+        st.load(B, min(sg + 2, nseg - 1));
+        sync_lds();
     }
 }
 
@@ -699,8 +696,10 @@ hipError_t launch_w2_mfma(const Layer &L, const void *expert_w, const void *scal
 {
     const uint8_t *ew = (const uint8_t *)expert_w, *es = (const uint8_t *)scales;
     // Staging pays a per-item prologue; with fewer than 16 K blocks per row (I < 2048)
-    // the two-tile kernel measured faster (235B-shaped layer: 155 against 160 us at T=64).
-    if ((L.I / 128) % 4 == 0 && L.I / 128 >= 16) {
+    // the two-tile kernel measured faster for FP8 weights (235B-shaped layer: 155
+    // against 160 us at T=64).  E2M1 weights carry half the bytes per activation
+    // fragment, so they always take the staged kernel.
+    if ((L.I / 128) % 4 == 0 && (L.I / 128 >= 16 || L.wfmt == 1)) {
         dim3 grid(mfma_grid(L, T, k, L.H / 64, 1)), block(256);
         if (L.wfmt == 0)
             w2_mfma_lds_kernel<0><<<grid, block, 0, st>>>(ew, es, meta, ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, ws.o,
