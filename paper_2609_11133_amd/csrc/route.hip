@@ -314,55 +314,115 @@ __device__ inline void block_exscan4(int (&v)[4], int (&tot)[4], int *sh /* [4 w
     __syncthreads();
 }
 
-// Top-k softmax of one token by a whole workgroup.  Each expert's rank is the number
-// of keys above its own (larger logit first, then lower index),
-// counted over the token's keys staged in LDS; the expert of rank j < k is choice j.
-// Weights are the softmax of the selected logits in fp32 relative to the largest,
-// normalised by their sum taken in rank order.
-__device__ inline void block_topk(const float *__restrict__ l, int E, int k, int32_t *ids, float *wts,
-                                  int32_t *ids_user, float *wts_user, uint32_t *lds)
+// Wave-wide maximum of 64-bit keys with DPP lane permutations: two quad permutes
+// and the half-row and row mirrors leave every lane of a 16-lane row with the row's
+// maximum; the four row maxima are combined in scalar registers.
+__device__ inline uint64_t dpp_max64(uint64_t v, int ctrl_sel)
 {
-    uint64_t *skey = reinterpret_cast<uint64_t *>(lds);  // [E]
-    int32_t *ssel = reinterpret_cast<int32_t *>(lds + 2 * E);  // [k]
-    float *sp = reinterpret_cast<float *>(lds + 2 * E + k);    // [k]
-    for (int e = threadIdx.x; e < E; e += blockDim.x)
-        skey[e] = ((uint64_t)ordered_bits(ld_dev(&l[e])) << 32) | (uint32_t)(~(uint32_t)e);
-    __syncthreads();
-    for (int e = threadIdx.x; e < E; e += blockDim.x) {
-        const uint64_t ke = skey[e];
-        int rank = 0;
-        for (int f = 0; f < E; ++f) rank += skey[f] > ke ? 1 : 0;
-        if (rank < k) ssel[rank] = e;
+    uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32), olo, ohi;
+    switch (ctrl_sel) {  // the DPP control is an immediate
+    case 0:
+        olo = __builtin_amdgcn_update_dpp(0u, lo, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
+        ohi = __builtin_amdgcn_update_dpp(0u, hi, 0xB1, 0xF, 0xF, false);
+        break;
+    case 1:
+        olo = __builtin_amdgcn_update_dpp(0u, lo, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
+        ohi = __builtin_amdgcn_update_dpp(0u, hi, 0x4E, 0xF, 0xF, false);
+        break;
+    case 2:
+        olo = __builtin_amdgcn_update_dpp(0u, lo, 0x141, 0xF, 0xF, false);  // row_half_mirror
+        ohi = __builtin_amdgcn_update_dpp(0u, hi, 0x141, 0xF, 0xF, false);
+        break;
+    default:
+        olo = __builtin_amdgcn_update_dpp(0u, lo, 0x140, 0xF, 0xF, false);  // row_mirror
+        ohi = __builtin_amdgcn_update_dpp(0u, hi, 0x140, 0xF, 0xF, false);
+        break;
     }
-    __syncthreads();
-    const int j = threadIdx.x;
-    float lj = 0.f;
-    if (j < k) {
-        const float top = from_ordered((uint32_t)(skey[ssel[0]] >> 32));
-        lj = from_ordered((uint32_t)(skey[ssel[j]] >> 32));
-        sp[j] = expf(lj - top);
+    const uint64_t o = ((uint64_t)ohi << 32) | olo;
+    return o > v ? o : v;
+}
+
+__device__ inline uint64_t wave_max64(uint64_t v)
+{
+    v = dpp_max64(v, 0);
+    v = dpp_max64(v, 1);
+    v = dpp_max64(v, 2);
+    v = dpp_max64(v, 3);
+    uint64_t m = 0;
+#pragma unroll
+    for (int row = 0; row < 4; ++row) {
+        // readlane returns a signed int: widen through uint32_t
+        const uint64_t r = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(v >> 32), 16 * row) << 32) |
+                           (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, 16 * row);
+        m = r > m ? r : m;
     }
-    __syncthreads();
-    if (j < k) {
-        float denom = 0.f;
-        for (int i = 0; i < k; ++i) denom += sp[i];  // rank order, as in every thread
-        const float w = sp[j] / denom;
-        const int e = ssel[j];
-        st_dev(&ids[j], e);
-        wts[j] = w;
-        if (ids_user) ids_user[j] = e;
-        if (wts_user) wts_user[j] = w;
+    return m;
+}
+
+// Top-k softmax of one token by one wave.  Keys are (ordered logit bits, complemented
+// expert index): a larger logit wins, and among equal logits the lower index.  Lane
+// owns keys of experts lane, lane+64, ... (V per lane, E <= 64V).  k rounds of a
+// wave-wide argmax (DPP lane permutations, see wave_max64) each take the largest
+// remaining key; lane j keeps choice j.  Weights are the softmax of the selected logits in
+// fp32 relative to the largest, normalised by their butterfly sum, which every lane
+// forms from the same pairs.
+template <int V>
+__device__ inline void wave_topk(const float *__restrict__ l, int E, int k, int32_t *ids, float *wts,
+                                 int32_t *ids_user, float *wts_user, int lane)
+{
+    uint64_t key[V];
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+        const int e = 64 * v + lane;
+        key[v] = e < E ? ((uint64_t)ordered_bits(ld_dev(&l[e])) << 32) | (uint32_t)(~(uint32_t)e) : 0;
     }
-    __syncthreads();  // LDS is reused by the caller
+    uint64_t mine = 0;  // lane j < k: key of choice j
+    for (int j = 0; j < k; ++j) {
+        uint64_t best = key[0];
+#pragma unroll
+        for (int v = 1; v < V; ++v) best = key[v] > best ? key[v] : best;
+        best = wave_max64(best);
+        if (lane == j) mine = best;
+#pragma unroll
+        for (int v = 0; v < V; ++v) key[v] = key[v] == best ? 0 : key[v];  // keys are unique
+    }
+    const float top = from_ordered((uint32_t)__shfl((uint32_t)(mine >> 32), 0));
+    const float p = lane < k ? expf(from_ordered((uint32_t)(mine >> 32)) - top) : 0.f;
+    float den = p;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) den += __shfl_xor(den, o);
+    if (lane < k) {
+        const int e = (int)(~(uint32_t)mine);
+        const float w = p / den;
+        st_dev(&ids[lane], e);
+        wts[lane] = w;
+        if (ids_user) ids_user[lane] = e;
+        if (wts_user) wts_user[lane] = w;
+    }
+}
+
+__device__ inline void token_topk(const float *__restrict__ l, int E, int k, int32_t *ids, float *wts,
+                                  int32_t *ids_user, float *wts_user, int lane)
+{
+    if (E <= 64)
+        wave_topk<1>(l, E, k, ids, wts, ids_user, wts_user, lane);
+    else if (E <= 128)
+        wave_topk<2>(l, E, k, ids, wts, ids_user, wts_user, lane);
+    else if (E <= 256)
+        wave_topk<4>(l, E, k, ids, wts, ids_user, wts_user, lane);
+    else if (E <= 512)
+        wave_topk<8>(l, E, k, ids, wts, ids_user, wts_user, lane);
+    else
+        wave_topk<16>(l, E, k, ids, wts, ids_user, wts_user, lane);
 }
 
 // ------------------------------------------------------------------ fused routing kernel
 //
 // Grid = T x bpt workgroups of 4 waves.  Workgroup (t, q) computes the logits of token
-// t for experts [4*q*epw, 4*(q+1)*epw).  The last workgroup of token t to finish (a
-// device-scope counter) runs that token's top-k softmax and, when the MFMA path is
-// enabled, its 2-term FP8 activation split.  The last token to finish then groups all
-// (token, choice) pairs by expert.  The counters are reset by the workgroup that
+// t for experts [4*q*epw, 4*(q+1)*epw) and, when the MFMA path is enabled, its share
+// of the token's 2-term FP8 activation split.  The last workgroup of token t to finish
+// (a device-scope counter) runs that token's top-k softmax in one wave.  The last
+// token to finish then groups all (token, choice) pairs by expert.  The counters are reset by the workgroup that
 // consumes them, so they read zero at the start of every launch.
 
 
@@ -384,7 +444,7 @@ struct RouteArgs {
 template <typename XT, typename WT>
 __global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
 {
-    extern __shared__ __attribute__((aligned(16))) uint32_t lds[];  // 64-bit keys: keep 8-byte alignment
+    extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
     __shared__ int s_flag;
     __shared__ int s_scan[16];
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
@@ -430,10 +490,11 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
     __syncthreads();
     if (!s_flag) return;
 
-    // 2. last workgroup of token t: top-k softmax
-    block_topk(A.logits + (size_t)t * E, E, A.k, A.ids + (size_t)t * A.k, A.wts + (size_t)t * A.k,
-               A.ids_user ? A.ids_user + (size_t)t * A.k : nullptr, A.wts_user ? A.wts_user + (size_t)t * A.k : nullptr,
-               lds);
+    // 2. last workgroup of token t: top-k softmax (wave 0)
+    if (wave == 0)
+        token_topk(A.logits + (size_t)t * E, E, A.k, A.ids + (size_t)t * A.k, A.wts + (size_t)t * A.k,
+                   A.ids_user ? A.ids_user + (size_t)t * A.k : nullptr,
+                   A.wts_user ? A.wts_user + (size_t)t * A.k : nullptr, lane);
     if (threadIdx.x == 0) st_dev(&A.cnt_tok[t * kCounterStride], 0);
     if (!A.do_group) return;
     wait_stores();
@@ -572,9 +633,7 @@ hipError_t launch_route(const Layer &L, const RouteParams &P, hipStream_t st)
     A.do_group = P.do_group;
     A.max_chunks = P.max_chunks;
     const int W = (P.T + 31) / 32;
-    const size_t topk_words = 2 * (size_t)L.E + 2 * (size_t)P.k;
-    const size_t group_words = P.do_group ? (size_t)L.E * W + L.E : 0;
-    const size_t lds = sizeof(uint32_t) * (topk_words > group_words ? topk_words : group_words);
+    const size_t lds = P.do_group ? sizeof(uint32_t) * ((size_t)L.E * W + L.E) : 0;  // grouping bitmasks
     dim3 grid(P.T * bpt), block(256);
     if (L.act_bf16 && L.router_bf16)
         route_kernel<uint16_t, uint16_t><<<grid, block, lds, st>>>(A);
