@@ -80,6 +80,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-power", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU work of the oracle sample")
+    ap.add_argument("--stack", action="store_true",
+                    help="also time the stack of 12 distinct 480B-shaped layers decoded back to back, T = 1..256")
+    ap.add_argument("--stack-steps", type=int, default=20)
     ap.add_argument("--mstar", type=int, default=0,
                     help="tokens per expert from which MFMA tiles are used (0: library default, -1: GEMV only)")
     return ap.parse_args()
@@ -117,6 +120,71 @@ class PowerSampler:
             except Exception:  # noqa: BLE001
                 pass
             stop.wait(0.1)
+
+
+def run_stack(args, dev):
+    """Decode steps through a stack of distinct 480B-shaped layers (one handle, one
+    stream, layer after layer with its own input batch), swept over T.  Weights are
+    generated layer by layer on the host and kept on the device (about 90 GB), so no
+    step finds its experts in the MALL."""
+    import statistics
+
+    import torch
+
+    from paper_2609_11133_amd import binding as B
+    from paper_2609_11133_amd import configs as C
+    from paper_2609_11133_amd import workload as W
+
+    cfg = C.QWEN3_480B_X12
+    t0 = time.time()
+    layers = []
+    for li in range(cfg.layers):
+        hl = W.host_layer(cfg, layer=li)
+        layers.append((W.to_device(hl.router_w, dev), W.to_device(hl.bias, dev), W.to_device(hl.expert_w, dev),
+                       W.to_device(hl.scales, dev)))
+        del hl
+        print(f"[stack] layer {li} resident ({time.time() - t0:.0f} s)", file=sys.stderr, flush=True)
+    m = B.MoEDecode(W.binding_config(cfg, max(cfg.tokens), args.mstar), device=dev)
+    stream = torch.cuda.current_stream(dev)
+    Be = cfg.expert_bytes()
+    out = {}
+    for T in cfg.tokens:
+        xs = [W.to_device(W.host_x(cfg, T, batch=li), dev) for li in range(cfg.layers)]
+        ys = [W.empty_y(cfg, T, dev) for _ in range(2)]
+        n_act = []
+        for li, (rw, bias, ew, sc) in enumerate(layers):
+            m.forward(xs[li], T, rw, bias, ew, sc, cfg.topk, ys[0])
+            n_act.append(m.stats()[0].n_active)
+
+        def step():
+            for li, (rw, bias, ew, sc) in enumerate(layers):
+                m.forward(xs[li], T, rw, bias, ew, sc, cfg.topk, ys[li & 1])
+
+        for _ in range(2):
+            step()
+        torch.cuda.synchronize(dev)
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record(stream)
+        for _ in range(args.stack_steps):
+            step()
+        end.record(stream)
+        torch.cuda.synchronize(dev)
+        ms = start.elapsed_time(end) / args.stack_steps
+        bytes_step = sum(n_act) * Be
+        out[str(T)] = dict(tokens_per_s=round(T / (ms * 1e-3), 1), ms_per_stack_step=round(ms, 4),
+                           us_per_layer=round(ms * 1e3 / cfg.layers, 1), n_active_mean=statistics.mean(n_act),
+                           GBs=round(bytes_step / (ms * 1e-3) / 1e9, 1),
+                           frac_of_peak=round(bytes_step / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4))
+        print(f"[stack] T={T}: {out[str(T)]['tokens_per_s']:.0f} tok/s, {ms * 1e3:.0f} us per 12-layer step, "
+              f"{out[str(T)]['GBs']:.0f} GB/s", file=sys.stderr, flush=True)
+        del xs, ys
+    m.close()
+    del layers
+    torch.cuda.empty_cache()
+    return dict(workload=f"{cfg.layers} distinct {cfg.name[:-4]}-shaped layers (H {cfg.hidden}, {cfg.n_experts} "
+                         f"experts, top-{cfg.topk}, I {cfg.inter}, fp8), back to back, "
+                         f"{cfg.layers * cfg.n_experts * Be / 1e9:.1f} GB of expert weights",
+                steps=args.stack_steps, by_tokens=out)
 
 
 def main():
@@ -267,6 +335,12 @@ def main():
 
     R = results[T_main]
     traffic, traffic_src = w13_traffic(cfg, T_main)
+    stack = None
+    if args.stack:
+        m.close()
+        del ews, scs, xs
+        torch.cuda.empty_cache()
+        stack = run_stack(args, dev)
     line = {
         "metric": METRIC,
         "value": R["tokens_per_s"],
@@ -314,6 +388,7 @@ def main():
                   for T, r in results.items()},
         "power": power,
         "cpu_baseline": cpu,
+        "stack": stack,
         "setup_s": round(setup_s, 1),
     }
     print(json.dumps(line))

@@ -280,6 +280,38 @@ def test_full_480b(dev, full_480b, T):
     _full(run, C.QWEN3_480B, T, batch=T)
 
 
+def test_stack_480b_back_to_back(dev, full_480b):
+    """Twelve 480B-shaped layers decoded back to back at T=256 on one handle and one
+    stream with no synchronisation between them: expert weights at twelve distinct
+    addresses (device copies of one layer), a distinct input batch per layer.  Every
+    layer's outputs are checked after a single synchronisation, on sampled tokens."""
+    cfg = C.QWEN3_480B
+    L, T = C.QWEN3_480B_X12.layers, max(C.QWEN3_480B_X12.tokens)
+    run = Run(cfg, full_480b, dev, max_tokens=T)
+    ews = [run.ew] + [run.ew.clone() for _ in range(L - 1)]
+    xs = [W.host_x(cfg, T, batch=200 + li) for li in range(L)]
+    ys = [W.empty_y(cfg, T, dev) for _ in range(L)]
+    ids = [torch.full((T, cfg.topk), -1, dtype=torch.int32, device=dev) for _ in range(L)]
+    wts = [torch.zeros((T, cfg.topk), dtype=torch.float32, device=dev) for _ in range(L)]
+    xd = [W.to_device(x, dev) for x in xs]
+    say(f"[stack] {L} layers x T={T}, {L * run.ew.numel() / 1e9:.1f} GB of expert weights")
+    for li in range(L):
+        run.m.forward(xd[li], T, run.rw, run.bias, ews[li], run.sc, cfg.topk, ys[li], ids[li], wts[li])
+    torch.cuda.synchronize(dev)
+    for li in range(L):
+        tokens = [(37 * li) % T, (101 * li + 255) % T]
+        lo, io, wo, yo = oracle.forward(xs[li], full_480b.router_w, full_480b.bias, full_480b.expert_w,
+                                        full_480b.scales, cfg.topk, cfg.inter, cfg.wfmt_id, tokens=tokens,
+                                        threads=THREADS)
+        got_ids = ids[li].cpu().numpy()[tokens]
+        got_y = W.y_to_f64(ys[li])[tokens]
+        assert np.array_equal(got_ids, io), f"layer {li}: selection differs"
+        assert np.abs(wts[li].cpu().numpy()[tokens] - wo).max() <= 1e-6
+        err, scale = np.abs(got_y - yo).max(), np.abs(yo).max()
+        say(f"[stack] layer {li} tokens {tokens}: max|err|/max|ref| = {err / scale:.3e}")
+        assert err <= TOL * scale
+
+
 def test_full_235b_mxfp4_zipf(dev):
     cfg = C.QWEN3_235B_MXFP4
     say("[gen] qwen3-235b-a22b mxfp4 layer")
