@@ -14,8 +14,10 @@ whose layers follow each other.
 Printed: one JSON line with tokens/s (value), the layer-level HBM rate of the
 unique activated-expert bytes, the sweep over the layer's batch sizes, the roofline
 of the dominant kernel (gate/up projection, from HIP events around it on the
-launch stream inside the timed region), board power where readable, and the fp64
-CPU oracle timed on this host's cores on a bounded sample of the same workload.
+launch stream over a second timed region of K steps: events between kernels add a
+launch gap at every boundary, so the headline steps are timed without them), board
+power where readable, and the fp64 CPU oracle timed on this host's cores on a
+bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -245,9 +247,8 @@ def main():
         for i in range(args.warmup):
             step(i)
         torch.cuda.synchronize(dev)
-        # timed region: K steps between two events on the launch stream, with the
-        # library's stage events recording each step's kernels on the same stream
-        B.moe_decode_profile_enable(m.handle, args.steps)
+        # timed region: K steps between two events on the launch stream (events
+        # between the kernels would add a launch gap at every boundary)
         start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize(dev)
         start.record(stream)
@@ -256,6 +257,12 @@ def main():
         end.record(stream)
         torch.cuda.synchronize(dev)
         ms = start.elapsed_time(end) / args.steps
+        # per-kernel durations: K more steps with the library's stage events recording
+        # each kernel on the same stream
+        B.moe_decode_profile_enable(m.handle, args.steps)
+        for i in range(args.steps):
+            step(i)
+        torch.cuda.synchronize(dev)
         stages = B.moe_decode_profile_read(m.handle, args.steps)
         B.moe_decode_profile_enable(m.handle, 0)
         acts = [n_act[i % pool] for i in range(args.steps)]

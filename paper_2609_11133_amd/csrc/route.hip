@@ -165,22 +165,71 @@ __device__ inline double elem(const Chunk8<T> &c, int i)
 constexpr int kEPW = 4;        // experts per wave, at most
 constexpr int kSegChunks = 4;  // 8-input chunks per lane held at once (2048 inputs)
 
+// One fp64 value moved by a DPP lane permutation (ctrl: an immediate DPP control).
+template <int CTRL>
+__device__ inline double dpp_f64(double v)
+{
+    const uint64_t u = __double_as_longlong(v);
+    const uint32_t lo = __builtin_amdgcn_update_dpp(0u, (uint32_t)u, CTRL, 0xF, 0xF, false);
+    const uint32_t hi = __builtin_amdgcn_update_dpp(0u, (uint32_t)(u >> 32), CTRL, 0xF, 0xF, false);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// Sum of v over the wave, the same in every lane: DPP quad permutes and the half-row
+// and row mirrors give each 16-lane row its sum, and the four row sums are added from
+// scalar registers.  Six additions deep, like a butterfly, so the recursive-summation
+// bound of the caller holds.
+__device__ inline double wave_sum_f64(double v)
+{
+    v += dpp_f64<0xB1>(v);   // quad_perm [1,0,3,2]
+    v += dpp_f64<0x4E>(v);   // quad_perm [2,3,0,1]
+    v += dpp_f64<0x141>(v);  // row_half_mirror
+    v += dpp_f64<0x140>(v);  // row_mirror
+    double r[4];
+#pragma unroll
+    for (int row = 0; row < 4; ++row) {
+        const uint64_t u = __double_as_longlong(v);
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, 16 * row);
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), 16 * row);
+        r[row] = __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+    }
+    return (r[0] + r[1]) + (r[2] + r[3]);
+}
+
+__device__ inline float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ inline float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
 // Canonical logits of one token row xr against router rows e0 .. e0+ne-1 (ne <= kEPW),
 // computed by one wave and written to lrow[e].  The lane's inputs are loaded once per
 // segment and reused for every expert; the next expert's router row is in flight
 // while the current one accumulates.  Returns the number of fallbacks taken.
+//
+// Each lane sums exact products in fp64 (two accumulators per expert) next to a bound
+// on the sum of their magnitudes; the wave-reduced sum is certified against the fp32
+// rounding midpoints with the recursive-summation error bound, else recomputed exactly.
+// With bf16 inputs a product of two bf16 values is exact in fp32 (16-bit significand),
+// so it is formed in fp32 and added in fp64, and the magnitude bound is summed in fp32
+// and inflated by its own worst-case rounding; products below the fp32 subnormal grain
+// add at most H*2^-149 in absolute error, which the margin covers.  fp32 inputs use
+// fp64 fused multiply-adds throughout.
 template <typename XT, typename WT>
 __device__ inline int wave_logits(const XT *__restrict__ xr, const WT *__restrict__ wr, const float *bias, int H,
                                   int e0, int ne, int lane, float *lrow)
 {
+    constexpr bool kBf16 = sizeof(XT) == 2 && sizeof(WT) == 2;
     const int nck = (H + 511) / 512;  // chunks of the lane with the most
     // Two accumulators per expert (even and odd chunks): each sums at most
     // ceil(nck/2)*8 products, then they are added and reduced over the wave.
     const int per_acc = ((nck + 1) / 2) * 8;
     const double gamma = (double)(per_acc + 1 + 6 + 1 + 2) * 0x1p-52;  // >= 2 gamma_D
+    const double infl = 1.0 + (double)(per_acc + 2) * 0x1p-23;         // fp32 magnitude sums
     double s[kEPW][2], a[kEPW][2];
+    float a32[kEPW][2];
 #pragma unroll
-    for (int i = 0; i < kEPW; ++i) s[i][0] = s[i][1] = a[i][0] = a[i][1] = 0.0;
+    for (int i = 0; i < kEPW; ++i) {
+        s[i][0] = s[i][1] = a[i][0] = a[i][1] = 0.0;
+        a32[i][0] = a32[i][1] = 0.f;
+    }
     for (int seg = 0; seg < nck; seg += kSegChunks) {
         Chunk8<XT> xc[kSegChunks];
         bool valid[kSegChunks];
@@ -195,23 +244,40 @@ __device__ inline int wave_logits(const XT *__restrict__ xr, const WT *__restric
 #pragma unroll
                 for (int q = 0; q < (int)(sizeof(xc[j].d) / 4); ++q) xc[j].d[q] = 0u;
         }
-        Chunk8<WT> wc[2][kSegChunks];
+        float xf[kSegChunks][8];
+        if constexpr (kBf16)
 #pragma unroll
-        for (int j = 0; j < kSegChunks; ++j) ld_chunk<WT>(wr + (size_t)e0 * H + off[j], wc[0][j]);
+            for (int j = 0; j < kSegChunks; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    xf[j][2 * q] = bf16_lo(xc[j].d[q]);
+                    xf[j][2 * q + 1] = bf16_hi(xc[j].d[q]);
+                }
+        // every expert's slice of this segment in flight at once (one memory latency)
+        Chunk8<WT> wc[kEPW][kSegChunks];
+#pragma unroll
+        for (int i = 0; i < kEPW; ++i)
+#pragma unroll
+            for (int j = 0; j < kSegChunks; ++j)
+                ld_chunk<WT>(wr + (size_t)(e0 + (i < ne ? i : 0)) * H + off[j], wc[i][j]);
 #pragma unroll
         for (int i = 0; i < kEPW; ++i) {
             if (i < ne) {
-                if (i + 1 < ne)
-#pragma unroll
-                    for (int j = 0; j < kSegChunks; ++j)
-                        ld_chunk<WT>(wr + (size_t)(e0 + i + 1) * H + off[j], wc[(i + 1) & 1][j]);
 #pragma unroll
                 for (int j = 0; j < kSegChunks; ++j)
 #pragma unroll
                     for (int q = 0; q < 8; ++q) {
-                        const double xv = elem<XT>(xc[j], q), wv = elem<WT>(wc[i & 1][j], q);
-                        s[i][j & 1] = fma(xv, wv, s[i][j & 1]);
-                        a[i][j & 1] = fma(fabs(xv), fabs(wv), a[i][j & 1]);
+                        if constexpr (kBf16) {
+                            const uint32_t wd = wc[i][j].d[q >> 1];
+                            const float wv = (q & 1) ? bf16_hi(wd) : bf16_lo(wd);
+                            const float pv = xf[j][q] * wv;  // exact
+                            s[i][j & 1] += (double)pv;
+                            a32[i][j & 1] = fmaf(fabsf(xf[j][q]), fabsf(wv), a32[i][j & 1]);
+                        } else {
+                            const double xv = elem<XT>(xc[j], q), wv = elem<WT>(wc[i][j], q);
+                            s[i][j & 1] = fma(xv, wv, s[i][j & 1]);
+                            a[i][j & 1] = fma(fabs(xv), fabs(wv), a[i][j & 1]);
+                        }
                     }
             }
         }
@@ -220,16 +286,13 @@ __device__ inline int wave_logits(const XT *__restrict__ xr, const WT *__restric
 #pragma unroll
     for (int i = 0; i < kEPW; ++i) {
         if (i < ne) {
-            double si = s[i][0] + s[i][1], ai = a[i][0] + a[i][1];
-#pragma unroll
-            for (int o = kWave / 2; o >= 1; o >>= 1) {
-                si += __shfl_xor(si, o);
-                ai += __shfl_xor(ai, o);
-            }
+            const double si = wave_sum_f64(s[i][0] + s[i][1]);
+            const double ai = wave_sum_f64(kBf16 ? ((double)a32[i][0] + (double)a32[i][1]) * infl : a[i][0] + a[i][1]);
             const int e = e0 + i;
             const double b = bias ? (double)bias[e] : 0.0;
+            const double slack = kBf16 ? (double)H * 0x1p-148 : 0.0;
             float r;
-            if (!certain_f32(si + b, gamma * (ai + fabs(b)), r)) {
+            if (!certain_f32(si + b, gamma * (ai + fabs(b)) + slack, r)) {
                 r = wave_logit_exact<XT, WT>(xr, wr + (size_t)e * H, b, H, lane);
                 ++nfb;
             }
