@@ -348,21 +348,31 @@ __device__ inline void load32_f32<float>(const float *p, float (&v)[32])
 
 // ------------------------------------------------------------------ block scan
 
+// Inclusive prefix sum over a wave with DPP row shifts (each 16-lane row), then the
+// row totals read from lanes 15, 31, 47 and 63.  Returns the wave total.
+__device__ inline int wave_inclusive_scan(int &v, int lane)
+{
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, false);  // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, false);  // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, false);  // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, false);  // row_shr:8
+    const int t0 = __builtin_amdgcn_readlane(v, 15), t1 = __builtin_amdgcn_readlane(v, 31),
+              t2 = __builtin_amdgcn_readlane(v, 47), t3 = __builtin_amdgcn_readlane(v, 63);
+    const int row = lane >> 4;
+    v += (row >= 1 ? t0 : 0) + (row >= 2 ? t1 : 0) + (row >= 3 ? t2 : 0);
+    return t0 + t1 + t2 + t3;
+}
+
 // Exclusive prefix sums of four counters over the 256 threads of a workgroup.
 __device__ inline void block_exscan4(int (&v)[4], int (&tot)[4], int *sh /* [4 waves][4] */)
 {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     int inc[4] = {v[0], v[1], v[2], v[3]};
+    int wt[4];
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const int y = __shfl_up(inc[c], o);
-            if (lane >= o) inc[c] += y;
-        }
-    }
-    if (lane == 63)
-        for (int c = 0; c < 4; ++c) sh[wave * 4 + c] = inc[c];
+    for (int c = 0; c < 4; ++c) wt[c] = wave_inclusive_scan(inc[c], lane);
+    if (lane == 0)
+        for (int c = 0; c < 4; ++c) sh[wave * 4 + c] = wt[c];
     __syncthreads();
     for (int c = 0; c < 4; ++c) {
         int before = 0, all = 0;
@@ -502,6 +512,7 @@ struct RouteArgs {
     int32_t *fb_acc;   // [1]
     uint8_t *xs_hi, *xs_lo, *xe_hi, *xe_lo;  // activation split (NULL: MFMA path off)
     int T, E, H, k, epw, bpt, mstar, do_group, max_chunks;
+    int id_cache;  // the grouping keeps the choices in LDS (sized by the launch)
 };
 
 template <typename XT, typename WT>
@@ -571,16 +582,34 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
     // offsets = exclusive prefix sum, slot of pair (t, j) choosing e = offsets[e] +
     // (number of earlier tokens that chose e).  Experts with at least `mstar` tokens
     // go to the MFMA list, the others to the GEMV list, each in expert order.
-    const int T = A.T, k = A.k;
+    const int T = A.T, k = A.k, P = T * k;
     const int W = (T + 31) / 32;
     uint32_t *mask = lds;                        // [E][W]
     int32_t *offs = (int32_t *)(lds + E * W);    // [E]
+    int32_t *idc = offs + E;                     // [P] when the launch sized LDS for it: the choices, read once
+    const bool cached = A.id_cache != 0;
     const MetaIdx mi{E, A.max_chunks};
+    int nfb_total = 0;
+    if (threadIdx.x == 0) nfb_total = atomicExch(A.fb_acc, 0);  // in flight during the grouping
     for (int i = threadIdx.x; i < E * W; i += blockDim.x) mask[i] = 0u;
     __syncthreads();
-    for (int p = threadIdx.x; p < T * k; p += blockDim.x) {
-        const int tt = p / k;
-        atomicOr(&mask[ld_dev(&A.ids[p]) * W + tt / 32], 1u << (tt % 32));
+    // this thread's choices, eight loads in flight at a time
+    for (int p0 = threadIdx.x; p0 < P; p0 += 8 * blockDim.x) {
+        int e8[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int p = p0 + u * blockDim.x;
+            e8[u] = p < P ? ld_dev(&A.ids[p]) : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int p = p0 + u * blockDim.x;
+            if (p < P) {
+                const int tt = p / k;
+                atomicOr(&mask[e8[u] * W + tt / 32], 1u << (tt % 32));
+                if (cached) idc[p] = e8[u];
+            }
+        }
     }
     __syncthreads();
     // each thread owns up to 4 consecutive experts
@@ -632,13 +661,13 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
         A.meta[mi.n_active()] = tot[1] + tot[2];
         A.meta[mi.n_gemv()] = tot[1];
         A.meta[mi.n_mfma()] = tot[2];
-        A.meta[mi.n_fallback()] = atomicExch(A.fb_acc, 0);
+        A.meta[mi.n_fallback()] = nfb_total;
         A.meta[mi.n_mfma_chunks()] = tot[3];
         st_dev(A.cnt_all, 0);
     }
     __syncthreads();
-    for (int p = threadIdx.x; p < T * k; p += blockDim.x) {
-        const int tt = p / k, e = ld_dev(&A.ids[p]);
+    for (int p = threadIdx.x; p < P; p += blockDim.x) {
+        const int tt = p / k, e = cached ? idc[p] : ld_dev(&A.ids[p]);
         int rank = __popc(mask[e * W + tt / 32] & ((1u << (tt % 32)) - 1u));
         for (int w = 0; w < tt / 32; ++w) rank += __popc(mask[e * W + w]);
         const int slot = offs[e] + rank;
@@ -696,7 +725,11 @@ hipError_t launch_route(const Layer &L, const RouteParams &P, hipStream_t st)
     A.do_group = P.do_group;
     A.max_chunks = P.max_chunks;
     const int W = (P.T + 31) / 32;
-    const size_t lds = P.do_group ? sizeof(uint32_t) * ((size_t)L.E * W + L.E) : 0;  // grouping bitmasks
+    // grouping LDS: bitmasks [E][W] and offsets [E], plus the choices [T*k] while the
+    // whole stays within 64 KiB
+    const size_t base_words = (size_t)L.E * W + L.E, pairs = (size_t)P.T * P.k;
+    A.id_cache = P.do_group && (base_words + pairs) * sizeof(uint32_t) <= 65536 ? 1 : 0;
+    const size_t lds = P.do_group ? sizeof(uint32_t) * (base_words + (A.id_cache ? pairs : 0)) : 0;
     dim3 grid(P.T * bpt), block(256);
     if (L.act_bf16 && L.router_bf16)
         route_kernel<uint16_t, uint16_t><<<grid, block, lds, st>>>(A);

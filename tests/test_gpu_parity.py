@@ -155,6 +155,29 @@ def test_topk_extremes(dev, k):
     check_layer(run, W.host_x(cfg, 5, seed=505), topk=k, label=f"k={k}")
 
 
+def test_single_expert_dense(dev):
+    """E = 1, k = 1: every token routes to expert 0 with weight 1 and the layer is one
+    dense SwiGLU block (the degenerate case of the method)."""
+    cfg = LayerConfig("one-expert", 512, 1, 1, 512, "bf16", "bf16", "fp8", None, [])
+    hl = W.host_layer(cfg, seed=511)
+    run = Run(cfg, hl, dev, max_tokens=40)
+    ids, wts, _ = check_layer(run, W.host_x(cfg, 37, seed=511), label="E=1")
+    assert np.all(ids == 0) and np.all(wts == 1.0)
+
+
+@pytest.mark.parametrize("cfg,k", [
+    (LayerConfig("wide-1024", 256, 1024, 64, 256, "bf16", "bf16", "fp8", "normal:0.5", []), 64),
+    (LayerConfig("wide-600", 512, 600, 24, 512, "bf16", "bf16", "mxfp4", "zipf:1.1", []), 24),
+], ids=["E1024-k64", "E600-k24"])
+def test_many_experts(dev, cfg, k):
+    """The largest expert counts and top-k the library accepts (16 keys per lane in
+    the wave top-k, the widest grouping bitmasks)."""
+    hl = W.host_layer(cfg, seed=512)
+    run = Run(cfg, hl, dev, max_tokens=48)
+    check_layer(run, W.host_x(cfg, 33, seed=512), topk=k, label=f"{cfg.name} k={k}")
+    check_routing(run, W.host_x(cfg, 9, seed=513), topk=k, label=f"{cfg.name} k={k}")
+
+
 def test_zero_input_and_ties(dev):
     """x = 0, no bias: every logit is +0, the selection is experts 0..k-1 with equal
     weights, and y = 0.  Duplicate router rows tie; the lower index wins."""
