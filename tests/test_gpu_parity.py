@@ -268,6 +268,34 @@ def test_lds_staged_kernels(dev, cfg, T):
         assert max(counts) > 16
 
 
+# Seeded random small layers across the accepted shapes: weight formats, activation
+# and router dtypes, bias recipes, K extents that take the staged or the two-tile
+# kernels, top-k up to 16 and ragged token counts.
+def _random_layer(i):
+    rng = np.random.default_rng(9000 + i)
+    wfmt = ["fp8", "mxfp4"][i % 2]
+    q = 128 if wfmt == "fp8" else 256
+    H = q * int(rng.integers(1, 9))
+    I = q * int(rng.integers(1, 9))
+    E = int(rng.choice([2, 5, 16, 40, 96, 160]))
+    k = int(min(E, rng.choice([1, 2, 4, 8, 16])))
+    act = ["bf16", "f32"][int(rng.integers(0, 4)) == 0]
+    router = ["bf16", "f32"][int(rng.integers(0, 4)) == 0]
+    bias = [None, "normal:0.5", "zipf:1.1"][int(rng.integers(0, 3))]
+    T = int(rng.integers(1, 70))
+    return LayerConfig(f"rand{i}", H, E, k, I, act, router, wfmt, bias, []), T
+
+
+@pytest.mark.parametrize("i", range(12))
+def test_random_small_layers(dev, i):
+    cfg, T = _random_layer(i)
+    assert 4 * max(cfg.hidden, cfg.inter) * (2 if cfg.act == "bf16" else 4) <= 65536  # accepted shapes
+    hl = W.host_layer(cfg, seed=700 + i)
+    run = Run(cfg, hl, dev, max_tokens=T, mfma_min_tokens=[0, -1, 2][i % 3])
+    say(f"[random] {cfg}")
+    check_layer(run, W.host_x(cfg, T, seed=700 + i), label=f"random {i}")
+
+
 # ---------------------------------------------------------------- full-size layers
 
 @pytest.fixture(scope="module")
