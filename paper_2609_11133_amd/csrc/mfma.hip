@@ -384,7 +384,7 @@ constexpr int kSegK = 4;                // K blocks per staged segment
 constexpr int kSegBytes = kSegK * 128;  // activation bytes per token row and segment
 constexpr int kStageTok = 32;           // token rows of a chunk
 
-struct ActSeg {
+struct alignas(16) ActSeg {
     uint8_t code[2][kStageTok][kSegBytes];  // [hi, lo][token][16-byte pieces, swizzled]
     uint8_t ex[2][kStageTok][kSegK * 4];    // [hi, lo][token][E8M0 per 32 inputs]
     uint8_t sink[kSegK * 4];                // target of the threads that stage no exponents
@@ -397,13 +397,14 @@ __device__ inline int swz(int c, int t) { return (c & ~7) | ((c ^ t) & 7); }
 
 __device__ inline void sync_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-// One thread's share of staging a segment: piece tid%32 of token rows 8q + tid/32
-// (q < 2*NT) in both the hi and lo codes; threads tid < 32 also stage token tid's
-// exponent bytes of each.  Every thread issues the same loads (tokens past the chunk
-// read out of range), so the loads need no branch.
-template <int NT>
+// One thread's share of staging a segment for a workgroup of W waves: piece tid%32
+// of token rows 2W*q + tid/32 (q < 8*NT/W) in both the hi and lo codes; threads
+// tid < 32 also stage token tid's exponent bytes of each.  Every thread issues the
+// same loads (tokens past the chunk read out of range), so the loads need no branch.
+template <int NT, int W>
 struct Stager {
-    static constexpr int Q = 2 * NT;
+    static_assert(W == 4 || W == 8, "four or eight waves per workgroup");
+    static constexpr int Q = 8 * NT / W;
     uint32_t voff[Q];  // byte offset of this thread's piece in its token rows, segment 0
     uint32_t eoff;     // exponent offset of token tid, segment 0 (out of range if none)
     int tok[Q];
@@ -416,7 +417,7 @@ struct Stager {
         piece = tid & 31;
 #pragma unroll
         for (int q = 0; q < Q; ++q) {
-            const int t = 8 * q + (tid >> 5);
+            const int t = 2 * W * q + (tid >> 5);
             tok[q] = t;
             const uint32_t row = t < mc ? (uint32_t)(row_of ? row_of[slot0 + t] : slot0 + t) : 0u;
             voff[q] = t < mc ? row * (uint32_t)K + 16u * piece : kOutOfRange;
@@ -451,13 +452,13 @@ struct Stager {
 };
 
 // Streams this wave's weight tile (this lane's row `arow`) over KB K blocks (KB a
-// multiple of 4) against NT staged token tiles; acc[j] as in stream_tiles.  All
-// four waves of the workgroup call it together: it synchronises them once per
-// staged segment (four K blocks).
-template <int FMT, int NT>
+// multiple of 4) against NT staged token tiles; acc[j] as in stream_tiles.  All W
+// waves of the workgroup call it together: it synchronises them once per staged
+// segment (four K blocks).  On return no wave reads `seg` any more.
+template <int FMT, int NT, int W>
 __device__ inline void stream_tile_lds(f32x4 (&acc)[NT], const uint8_t *__restrict__ arow,
                                        const uint8_t *__restrict__ erow, const float *__restrict__ sblk, int KB,
-                                       const ActRsrc &B, Stager<NT> &st, ActSeg (&seg)[2], int lane, int tid)
+                                       const ActRsrc &B, Stager<NT, W> &st, ActSeg (&seg)[2], int lane, int tid)
 {
     const int r = lane & 15, g = lane >> 4;
     const int nseg = KB / kSegK;
@@ -509,31 +510,41 @@ __device__ inline void stream_tile_lds(f32x4 (&acc)[NT], const uint8_t *__restri
     }
 }
 
-// gate/up: item = (chunk, rows [i0, i0+32)); wave w streams gate (w < 2) or up
-// (w >= 2) rows i0 + 16*(w&1); the accumulators meet in LDS and wave j forms h and
-// its 2-term split for token tile j (the 32 rows are one E8M0 group per token).
-template <int FMT, int NT>
+// gate/up: item = (chunk, rows [i0, i0+8W)) for W waves; wave w streams gate
+// (w < W/2) or up (w >= W/2) rows i0 + 16*(w % (W/2)).  The accumulators meet in
+// LDS (over the staging buffer the last segment no longer needs) and wave e < NT*W/4
+// forms h and its 2-term split for token tile e % NT of 32-row group e / NT (32 rows
+// are one E8M0 group per token).
+template <int FMT, int NT, int W>
 __device__ inline void w13_item_lds(const uint8_t *__restrict__ we, const uint8_t *__restrict__ se, int H, int I,
                                     int i0, int slot0, int mc, const int32_t *__restrict__ tok_of, const ActRsrc &X,
                                     uint8_t *__restrict__ hs_hi, uint8_t *__restrict__ hs_lo,
                                     uint8_t *__restrict__ he_hi, uint8_t *__restrict__ he_lo, ActSeg (&seg)[2],
-                                    f32x4 (&red)[4][2][64], int wave, int lane, int tid)
+                                    int wave, int lane, int tid)
 {
+    constexpr int HW = W / 2;  // waves per projection
+    constexpr int NG = W / 4;  // 32-row groups per item
     const int r = lane & 15, g = lane >> 4;
-    const int row0 = (wave >= 2 ? I : 0) + i0 + 16 * (wave & 1);
+    const int row0 = (wave >= HW ? I : 0) + i0 + 16 * (wave % HW);
     const uint8_t *arow = we + (size_t)(row0 + r) * (FMT == 0 ? (size_t)H : (size_t)H / 2);
     const uint8_t *erow = se + (size_t)(row0 + r) * (H / 32);
     const float *sblk = (const float *)se + (size_t)(row0 / 128) * (H / 128);
-    Stager<NT> st;
+    Stager<NT, W> st;
     st.init(tok_of, slot0, mc, H, tid);
     f32x4 acc[NT];
-    stream_tile_lds<FMT, NT>(acc, arow, erow, sblk, H / 128, X, st, seg, lane, tid);
+    stream_tile_lds<FMT, NT, W>(acc, arow, erow, sblk, H / 128, X, st, seg, lane, tid);
+    // red[w][j][lane]: W*2*64 f32x4 fit in seg[1].code, which the next item first
+    // writes after its first barrier, so no wave still reads red by then.
+    static_assert(sizeof(f32x4) * W * 2 * 64 <= sizeof(seg[1].code), "reduction buffer");
+    f32x4 *red = reinterpret_cast<f32x4 *>(&seg[1].code[0][0][0]);
 #pragma unroll
-    for (int j = 0; j < NT; ++j) red[wave][j][lane] = acc[j];
+    for (int j = 0; j < NT; ++j) red[(wave * 2 + j) * 64 + lane] = acc[j];
     sync_lds();
-    if (wave < NT) {
-        const int j = wave;
-        const f32x4 g0 = red[0][j][lane], g1 = red[1][j][lane], u0 = red[2][j][lane], u1 = red[3][j][lane];
+    if (wave < NG * NT) {
+        const int j = wave % NT, grp = wave / NT;
+        const f32x4 g0 = red[((2 * grp) * 2 + j) * 64 + lane], g1 = red[((2 * grp + 1) * 2 + j) * 64 + lane];
+        const f32x4 u0 = red[((HW + 2 * grp) * 2 + j) * 64 + lane];
+        const f32x4 u1 = red[((HW + 2 * grp + 1) * 2 + j) * 64 + lane];
         float h[8], res[8];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -553,22 +564,23 @@ __device__ inline void w13_item_lds(const uint8_t *__restrict__ we, const uint8_
         split_lo(res, cl, ql);
         if (16 * j + r < mc) {
             const size_t slot = (size_t)slot0 + 16 * j + r;
-            uint8_t *ph = hs_hi + slot * I + i0 + 4 * g;
-            uint8_t *pl = hs_lo + slot * I + i0 + 4 * g;
+            const int c0 = i0 + 32 * grp;
+            uint8_t *ph = hs_hi + slot * I + c0 + 4 * g;
+            uint8_t *pl = hs_lo + slot * I + c0 + 4 * g;
             *reinterpret_cast<uint32_t *>(ph) = qh[0];
             *reinterpret_cast<uint32_t *>(ph + 16) = qh[1];
             *reinterpret_cast<uint32_t *>(pl) = ql[0];
             *reinterpret_cast<uint32_t *>(pl + 16) = ql[1];
             if (g == 0) {
-                he_hi[slot * (I / 32) + i0 / 32] = (uint8_t)ch;
-                he_lo[slot * (I / 32) + i0 / 32] = (uint8_t)cl;
+                he_hi[slot * (I / 32) + c0 / 32] = (uint8_t)ch;
+                he_lo[slot * (I / 32) + c0 / 32] = (uint8_t)cl;
             }
         }
     }
 }
 
-template <int FMT>
-__global__ __launch_bounds__(256) void w13_mfma_lds_kernel(
+template <int FMT, int W>
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W == 8 ? 4 : 1))) void w13_mfma_lds_kernel(
     const uint8_t *__restrict__ ew, const uint8_t *__restrict__ es, const int32_t *__restrict__ meta,
     const int32_t *__restrict__ tok_of, const uint8_t *__restrict__ xs_hi, const uint8_t *__restrict__ xs_lo,
     const uint8_t *__restrict__ xe_hi, const uint8_t *__restrict__ xe_lo, uint8_t *__restrict__ hs_hi,
@@ -576,9 +588,8 @@ __global__ __launch_bounds__(256) void w13_mfma_lds_kernel(
     int E, size_t ewb, size_t esb)
 {
     __shared__ ActSeg seg[2];
-    __shared__ f32x4 red[4][2][64];
     const MetaIdx mi{E};
-    const int tiles = I / 32;
+    const int tiles = I / (8 * W);
     const int n_items = meta[mi.n_mfma_chunks()] * tiles;
     const int4 *recs = reinterpret_cast<const int4 *>(meta + mi.chunk_rec());
     const int tid = threadIdx.x, lane = tid & 63;
@@ -586,20 +597,20 @@ __global__ __launch_bounds__(256) void w13_mfma_lds_kernel(
     const ActRsrc X = act_rsrc(xs_hi, xs_lo, xe_hi, xe_lo, (uint32_t)T, (uint32_t)H);
     for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
         const int4 rec = recs[item / tiles];  // {expert, first slot, tokens, -}
-        const int i0 = (item % tiles) * 32;
+        const int i0 = (item % tiles) * 8 * W;
         const uint8_t *we = ew + (size_t)rec.x * ewb;
         const uint8_t *se = es + (size_t)rec.x * esb;
         if (rec.z > 16)
-            w13_item_lds<FMT, 2>(we, se, H, I, i0, rec.y, rec.z, tok_of, X, hs_hi, hs_lo, he_hi, he_lo, seg, red,
-                                 wave, lane, tid);
+            w13_item_lds<FMT, 2, W>(we, se, H, I, i0, rec.y, rec.z, tok_of, X, hs_hi, hs_lo, he_hi, he_lo, seg,
+                                    wave, lane, tid);
         else
-            w13_item_lds<FMT, 1>(we, se, H, I, i0, rec.y, rec.z, tok_of, X, hs_hi, hs_lo, he_hi, he_lo, seg, red,
-                                 wave, lane, tid);
+            w13_item_lds<FMT, 1, W>(we, se, H, I, i0, rec.y, rec.z, tok_of, X, hs_hi, hs_lo, he_hi, he_lo, seg,
+                                    wave, lane, tid);
     }
 }
 
-// down: item = (chunk, rows [n0, n0+64)); wave w streams rows n0 + 16w.
-template <int FMT, int NT>
+// down: item = (chunk, rows [n0, n0+16W)) for W waves; wave w streams rows n0 + 16w.
+template <int FMT, int NT, int W>
 __device__ inline void w2_item_lds(const uint8_t *__restrict__ we2, const uint8_t *__restrict__ se, int H, int I,
                                    int n0, int slot0, int mc, const ActRsrc &Hs, float *__restrict__ obuf,
                                    ActSeg (&seg)[2], int wave, int lane, int tid)
@@ -609,30 +620,30 @@ __device__ inline void w2_item_lds(const uint8_t *__restrict__ we2, const uint8_
     const uint8_t *arow = we2 + (size_t)(row0 + r) * (FMT == 0 ? (size_t)I : (size_t)I / 2);
     const uint8_t *erow = se + (size_t)2 * I * (H / 32) + (size_t)(row0 + r) * (I / 32);
     const float *sblk = (const float *)se + (size_t)2 * (I / 128) * (H / 128) + (size_t)(row0 / 128) * (I / 128);
-    Stager<NT> st;
+    Stager<NT, W> st;
     st.init(nullptr, slot0, mc, I, tid);
     f32x4 acc[NT];
-    stream_tile_lds<FMT, NT>(acc, arow, erow, sblk, I / 128, Hs, st, seg, lane, tid);
+    stream_tile_lds<FMT, NT, W>(acc, arow, erow, sblk, I / 128, Hs, st, seg, lane, tid);
 #pragma unroll
     for (int j = 0; j < NT; ++j)
         if (16 * j + r < mc)
             *reinterpret_cast<f32x4 *>(obuf + ((size_t)slot0 + 16 * j + r) * H + row0 + 4 * g) = acc[j];
 }
 
-template <int FMT>
-__global__ __launch_bounds__(256) void w2_mfma_lds_kernel(const uint8_t *__restrict__ ew,
-                                                          const uint8_t *__restrict__ es,
-                                                          const int32_t *__restrict__ meta,
-                                                          const uint8_t *__restrict__ hs_hi,
-                                                          const uint8_t *__restrict__ hs_lo,
-                                                          const uint8_t *__restrict__ he_hi,
-                                                          const uint8_t *__restrict__ he_lo,
-                                                          float *__restrict__ obuf, int P, int H, int I, int E,
-                                                          size_t ewb, size_t esb)
+template <int FMT, int W>
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W == 8 ? 4 : 1))) void w2_mfma_lds_kernel(const uint8_t *__restrict__ ew,
+                                                             const uint8_t *__restrict__ es,
+                                                             const int32_t *__restrict__ meta,
+                                                             const uint8_t *__restrict__ hs_hi,
+                                                             const uint8_t *__restrict__ hs_lo,
+                                                             const uint8_t *__restrict__ he_hi,
+                                                             const uint8_t *__restrict__ he_lo,
+                                                             float *__restrict__ obuf, int P, int H, int I, int E,
+                                                             size_t ewb, size_t esb)
 {
     __shared__ ActSeg seg[2];
     const MetaIdx mi{E};
-    const int tiles = H / 64;
+    const int tiles = H / (16 * W);
     const int n_items = meta[mi.n_mfma_chunks()] * tiles;
     const int4 *recs = reinterpret_cast<const int4 *>(meta + mi.chunk_rec());
     const int tid = threadIdx.x, lane = tid & 63;
@@ -641,15 +652,25 @@ __global__ __launch_bounds__(256) void w2_mfma_lds_kernel(const uint8_t *__restr
     const ActRsrc Hs = act_rsrc(hs_hi, hs_lo, he_hi, he_lo, (uint32_t)P, (uint32_t)I);
     for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
         const int4 rec = recs[item / tiles];
-        const int n0 = (item % tiles) * 64;
+        const int n0 = (item % tiles) * 16 * W;
         const uint8_t *we2 = ew + (size_t)rec.x * ewb + w2off;
         const uint8_t *se = es + (size_t)rec.x * esb;
         if (rec.z > 16)
-            w2_item_lds<FMT, 2>(we2, se, H, I, n0, rec.y, rec.z, Hs, obuf, seg, wave, lane, tid);
+            w2_item_lds<FMT, 2, W>(we2, se, H, I, n0, rec.y, rec.z, Hs, obuf, seg, wave, lane, tid);
         else
-            w2_item_lds<FMT, 1>(we2, se, H, I, n0, rec.y, rec.z, Hs, obuf, seg, wave, lane, tid);
+            w2_item_lds<FMT, 1, W>(we2, se, H, I, n0, rec.y, rec.z, Hs, obuf, seg, wave, lane, tid);
     }
 }
+
+// Waves per workgroup of the staged kernels.  FP8 weights stream at 4 waves and two
+// workgroups per CU: eight waves per CU hold the HBM stream at its best, and more
+// waves per CU slowed it (the 235B- and 480B-shaped layers lost 9-18%).  E2M1
+// weights carry half the bytes per activation fragment, so staging and fragment
+// reads, not HBM, bound them; 8-wave workgroups halve the staged activation bytes per
+// weight byte and, held to 128 VGPRs, run two per CU (the MXFP4 layer at T=256:
+// 570k against 604k tokens/s).
+template <int FMT>
+constexpr int kStagedWaves = FMT == 0 ? 4 : 8;
 
 // Workgroups for `items_per_chunk` items per chunk record, `per_block` items per workgroup.
 int mfma_grid(const Layer &L, int T, int k, int items_per_chunk, int per_block)
@@ -661,24 +682,38 @@ int mfma_grid(const Layer &L, int T, int k, int items_per_chunk, int per_block)
     return blocks < 1 ? 1 : (blocks > 65535 ? 65535 : (int)blocks);
 }
 
+template <int FMT>
+hipError_t launch_w13_lds(const Layer &L, const uint8_t *ew, const uint8_t *es, int T, int k, const int32_t *meta,
+                          const int32_t *tok_of, const Workspace &ws, hipStream_t st)
+{
+    constexpr int W = kStagedWaves<FMT>;
+    dim3 grid(mfma_grid(L, T, k, L.I / (8 * W), 1)), block(64 * W);
+    w13_mfma_lds_kernel<FMT, W><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.xs_hi, ws.xs_lo, ws.xe_hi, ws.xe_lo,
+                                                        ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, T, L.H, L.I, L.E,
+                                                        L.expert_w_bytes, L.expert_s_bytes);
+    return hipGetLastError();
+}
+
+template <int FMT>
+hipError_t launch_w2_lds(const Layer &L, const uint8_t *ew, const uint8_t *es, int T, int k, const int32_t *meta,
+                         const Workspace &ws, hipStream_t st)
+{
+    constexpr int W = kStagedWaves<FMT>;
+    dim3 grid(mfma_grid(L, T, k, L.H / (16 * W), 1)), block(64 * W);
+    w2_mfma_lds_kernel<FMT, W><<<grid, block, 0, st>>>(ew, es, meta, ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, ws.o,
+                                                       T * k, L.H, L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_w13_mfma(const Layer &L, const void *expert_w, const void *scales, int T, int k,
                            const int32_t *meta, const int32_t *tok_of, const Workspace &ws, hipStream_t st)
 {
     const uint8_t *ew = (const uint8_t *)expert_w, *es = (const uint8_t *)scales;
-    if ((L.H / 128) % 4 == 0) {
-        dim3 grid(mfma_grid(L, T, k, L.I / 32, 1)), block(256);
-        if (L.wfmt == 0)
-            w13_mfma_lds_kernel<0><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.xs_hi, ws.xs_lo, ws.xe_hi,
-                                                           ws.xe_lo, ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, T, L.H,
-                                                           L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
-        else
-            w13_mfma_lds_kernel<1><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.xs_hi, ws.xs_lo, ws.xe_hi,
-                                                           ws.xe_lo, ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, T, L.H,
-                                                           L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
-        return hipGetLastError();
-    }
+    if ((L.H / 128) % 4 == 0)
+        return L.wfmt == 0 ? launch_w13_lds<0>(L, ew, es, T, k, meta, tok_of, ws, st)
+                           : launch_w13_lds<1>(L, ew, es, T, k, meta, tok_of, ws, st);
     dim3 grid(mfma_grid(L, T, k, L.I / 64, 1)), block(256);
     if (L.wfmt == 0)
         w13_mfma_kernel<0><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.xs_hi, ws.xs_lo, ws.xe_hi, ws.xe_lo,
@@ -699,16 +734,9 @@ hipError_t launch_w2_mfma(const Layer &L, const void *expert_w, const void *scal
     // the two-tile kernel measured faster for FP8 weights (235B-shaped layer: 155
     // against 160 us at T=64).  E2M1 weights carry half the bytes per activation
     // fragment, so they always take the staged kernel.
-    if ((L.I / 128) % 4 == 0 && (L.I / 128 >= 16 || L.wfmt == 1)) {
-        dim3 grid(mfma_grid(L, T, k, L.H / 64, 1)), block(256);
-        if (L.wfmt == 0)
-            w2_mfma_lds_kernel<0><<<grid, block, 0, st>>>(ew, es, meta, ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, ws.o,
-                                                          T * k, L.H, L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
-        else
-            w2_mfma_lds_kernel<1><<<grid, block, 0, st>>>(ew, es, meta, ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, ws.o,
-                                                          T * k, L.H, L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
-        return hipGetLastError();
-    }
+    if ((L.I / 128) % 4 == 0 && (L.I / 128 >= 16 || L.wfmt == 1))
+        return L.wfmt == 0 ? launch_w2_lds<0>(L, ew, es, T, k, meta, ws, st)
+                           : launch_w2_lds<1>(L, ew, es, T, k, meta, ws, st);
     dim3 grid(mfma_grid(L, T, k, L.H / 32, 4)), block(256);
     if (L.wfmt == 0)
         w2_mfma_kernel<0><<<grid, block, 0, st>>>(ew, es, meta, ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, ws.o, T * k,
