@@ -396,7 +396,7 @@ def main():
             "n_active_mean": R["n_active_mean"],
         },
         "roofline": {
-            "kernel": ("w13_mfma_kernel (grouped gate/up + SiLU-gate, MFMA for every expert)"
+            "kernel": ("w13_mfma_lds_kernel (grouped gate/up + SiLU-gate, activations staged in LDS, MFMA for every expert)"
                        if args.mstar in (0, 1) else "w13 stage (GEMV and MFMA kernels)"),
             "bound": "hbm",
             "achieved": R["w13_GBs"],
