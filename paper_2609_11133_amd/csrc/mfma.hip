@@ -69,15 +69,23 @@ struct Frags {
 };
 
 // K loop over KB blocks with an S-stage register ring: the loads of block kb+S-1 are
-// issued before block kb is multiplied, so S-1 blocks stay in flight.  The steady
-// state has no conditional loads: the compiler's wait counts are exact only when
-// every path issues the same loads, and a guarded load makes it wait for all.
+// issued before block kb is multiplied, so S-1 blocks stay in flight.  Neither the
+// prologue nor the steady state has conditional loads: the compiler's wait counts
+// are exact only when every path issues the same loads, and a guarded load before
+// the loop makes every iteration wait for all outstanding loads.  So the prologue
+// always fills S-1 slots, with block KB-1 standing in for blocks past the end, and
+// issues them slot by slot: the wait at the top of the loop is one count for the
+// path from the prologue and the path from the previous iteration, and a slot's
+// loads scheduled after a later slot's (the scheduler likes to sink the byte loads)
+// would make it wait for nearly all.
 template <int S, typename FR, typename LoadF, typename CompF>
 __device__ inline void k_pipeline(int KB, FR (&F)[S], LoadF load, CompF compute)
 {
 #pragma unroll
-    for (int s = 0; s < S - 1; ++s)
-        if (s < KB) load(F[s], s);
+    for (int s = 0; s < S - 1; ++s) {
+        load(F[s], s < KB ? s : KB - 1);
+        __builtin_amdgcn_sched_barrier(0);
+    }
     int kb = 0;
     for (; kb + 2 * S - 1 <= KB; kb += S) {
 #pragma unroll
@@ -187,6 +195,72 @@ __device__ inline void stream_tiles(f32x4 (&acc)[2][NT], const uint8_t *const (&
     };
     Frags<2, NT> F[S];
     k_pipeline<S>(KB, F, load, compute);
+}
+
+// stream_tiles for a block count KBC fixed at compile time and fully unrolled.  The
+// activations' E8M0 exponents of the lane's token rows are read up front, 16 bytes
+// (four K blocks) per load, instead of one byte load per block and token tile: on
+// the 235B-shaped down projection (12 K blocks) the byte loads were a fifth of the
+// K loop's memory instructions.
+//   erow_off[j]  byte offset of the lane's token row in the exponent buffers
+//                (kOutOfRange past the chunk)
+template <int FMT, int NT, int S, int KBC>
+__device__ inline void stream_tiles_fixed(f32x4 (&acc)[2][NT], const uint8_t *const (&arow)[2],
+                                          const uint8_t *const (&erow)[2], const float *const (&sblk)[2],
+                                          const ActRsrc &B, const uint32_t (&voff)[NT],
+                                          const uint32_t (&erow_off)[NT], int g)
+{
+    static_assert(KBC % 4 == 0 && S >= 2, "whole 16-byte exponent loads");
+    constexpr int Q = KBC / 4;
+    u32x4v exh[NT][Q], exl[NT][Q];
+#pragma unroll
+    for (int j = 0; j < NT; ++j)
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            exh[j][q] = __builtin_amdgcn_raw_buffer_load_b128(B.ehi, erow_off[j], q * 16, 0);
+            exl[j][q] = __builtin_amdgcn_raw_buffer_load_b128(B.elo, erow_off[j], q * 16, 0);
+        }
+    auto load = [&](Frags<2, NT> &F, int kb) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            if constexpr (FMT == 0) {
+                F.a[t] = frag_fp8(arow[t] + (size_t)kb * 128, g);
+                F.ea[t] = 127;
+            } else {
+                F.a[t] = frag_fp4(arow[t] + (size_t)kb * 64, g);
+                F.ea[t] = erow[t][kb * 4 + g];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+            F.bh[j] = frag_buf(B.hi, voff[j], kb * 128);
+            F.bl[j] = frag_buf(B.lo, voff[j], kb * 128);
+        }
+    };
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[t][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    auto compute = [&](const Frags<2, NT> &F, int kb) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            const float sc = FMT == 0 ? sblk[t][kb] : 1.f;
+#pragma unroll
+            for (int j = 0; j < NT; ++j) {
+                const int eh = (int)__builtin_amdgcn_ubfe(exh[j][kb / 4][kb % 4], 8 * g, 8);
+                const int el = (int)__builtin_amdgcn_ubfe(exl[j][kb / 4][kb % 4], 8 * g, 8);
+                mma2<FMT>(acc[t][j], F.a[t], F.ea[t], sc, F.bh[j], eh, F.bl[j], el);
+            }
+        }
+    };
+    Frags<2, NT> F[S];
+#pragma unroll
+    for (int kb = 0; kb < S - 1; ++kb) load(F[kb], kb);
+#pragma unroll
+    for (int kb = 0; kb < KBC; ++kb) {
+        if (kb + S - 1 < KBC) load(F[(kb + S - 1) % S], kb + S - 1);
+        compute(F[kb % S], kb);
+    }
 }
 
 // This lane's token-row offsets for the NT token tiles of a chunk.
@@ -329,7 +403,14 @@ __device__ inline void w2_rows(const uint8_t *__restrict__ we2, const uint8_t *_
     uint32_t voff[NT], eoff[NT];
     token_offsets<NT>(voff, eoff, nullptr, slot0, mc, I, r, g);
     f32x4 acc[2][NT];
-    stream_tiles<FMT, NT, S>(acc, arow, erow, sblk, I / 128, Hs, voff, eoff, g);
+    if (I == 12 * 128) {  // the 235B-shaped layer
+        uint32_t erow_off[NT];
+#pragma unroll
+        for (int j = 0; j < NT; ++j) erow_off[j] = eoff[j] - (uint32_t)g;
+        stream_tiles_fixed<FMT, NT, S, 12>(acc, arow, erow, sblk, Hs, voff, erow_off, g);
+    } else {
+        stream_tiles<FMT, NT, S>(acc, arow, erow, sblk, I / 128, Hs, voff, eoff, g);
+    }
 #pragma unroll
     for (int j = 0; j < NT; ++j)
         if (16 * j + r < mc) {
