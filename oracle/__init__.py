@@ -17,7 +17,7 @@ _SRC = os.path.join(_HERE, "moe_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 DT_F32, DT_BF16 = 0, 1
-WF_FP8, WF_MXFP4 = 0, 1
+WF_FP8, WF_MXFP4, WF_NVFP4 = 0, 1, 2
 
 
 def build(force: bool = True) -> str:
@@ -126,7 +126,7 @@ def forward(x, router_w, bias, expert_w, scales, k, inter, wfmt, tokens=None, th
 
     ``x`` [T,H] bf16 bits (uint16) or float32; ``router_w`` [E,H] likewise; ``bias`` [E]
     float32 or None; ``expert_w`` uint8 [E, expert bytes]; ``scales`` [E, ...] (float32
-    for FP8, uint8 for MXFP4).  Returns ``(logits f32 [n,E], ids int32 [n,k], w f64 [n,k],
+    for FP8, uint8 for MXFP4 and NVFP4).  Returns ``(logits f32 [n,E], ids int32 [n,k], w f64 [n,k],
     y f64 [n,H])``.
     """
     x = np.ascontiguousarray(x)

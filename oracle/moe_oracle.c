@@ -17,6 +17,7 @@
  *   O4 renormalise    w[t,j] = p[t,id_j] / sum_{i<k} p[t,id_i]
  *   O5 dequantise     FP8 : W[n][c] = e4m3(q[n][c]) * s[n/128][c/128]
  *                     MXFP4: W[n][c] = e2m1(q[n][c]) * 2^(e8m0[n][c/32] - 127)
+ *                     NVFP4: W[n][c] = e2m1(q[n][c]) * e4m3(sb[n][c/16]) * ts
  *   O6 expert FFN     g = Wgate x, u = Wup x, a_i = g_i / (1 + exp(-g_i)) * u_i, o = Wdown a
  *   O7 combine        y[t] = sum_{j=0..k-1} w[t,j] * o[t,j]   (j ascending)
  *
@@ -27,12 +28,16 @@
  *
  * Formats: OCP FP8 E4M3FN (bias 7, max 448, S.1111.111 = NaN, no infinities);
  * OCP MX v1.0 E2M1 (bias 1, values 0, 0.5, 1, 1.5, 2, 3, 4, 6) and E8M0
- * (2^(e-127), 0xFF = NaN); bf16 = the upper 16 bits of an fp32.
+ * (2^(e-127), 0xFF = NaN); bf16 = the upper 16 bits of an fp32.  NVFP4, NVIDIA's
+ * two-level 4-bit format: E2M1 elements, an E4M3 scale per 16 consecutive inputs
+ * and an fp32 scale ts per matrix.
  *
  * Expert weight packing (per expert, contiguous): gate [I][H], up [I][H] (input
  * index contiguous), down [H][I]; FP8 one byte per weight, MXFP4 two per byte with
- * the even input index in the low nibble.  Scales: FP8 fp32 gate [I/128][H/128] |
- * up | down [H/128][I/128]; MXFP4 E8M0 bytes gate [I][H/32] | up | down [H][I/32].
+ * the even input index in the low nibble (NVFP4 packed as MXFP4).  Scales: FP8 fp32
+ * gate [I/128][H/128] | up | down [H/128][I/128]; MXFP4 E8M0 bytes gate [I][H/32] | up |
+ * down [H][I/32]; NVFP4 four fp32 {ts gate, ts up, ts down, unused}, then E4M3 bytes
+ * gate [I][H/16] | up | down [H][I/16].
  */
 #include <math.h>
 #include <pthread.h>
@@ -41,7 +46,7 @@
 #include <string.h>
 
 enum { DT_F32 = 0, DT_BF16 = 1 };
-enum { WF_FP8 = 0, WF_MXFP4 = 1 };
+enum { WF_FP8 = 0, WF_MXFP4 = 1, WF_NVFP4 = 2 };
 
 /* ------------------------------------------------------------------ formats */
 
@@ -212,7 +217,17 @@ typedef struct {
 static int64_t expert_w_bytes(const experts_t *X) { return X->wfmt == WF_FP8 ? 3 * X->H * X->I : 3 * X->H * X->I / 2; }
 static int64_t expert_s_bytes(const experts_t *X)
 {
-    return X->wfmt == WF_FP8 ? 4 * 3 * (X->H / 128) * (X->I / 128) : 3 * X->H * X->I / 32;
+    if (X->wfmt == WF_FP8) return 4 * 3 * (X->H / 128) * (X->I / 128);
+    if (X->wfmt == WF_MXFP4) return 3 * X->H * X->I / 32;
+    return 16 + 3 * X->H * X->I / 16;
+}
+
+/* E2M1 code of input c of row n of a packed [N][K] 4-bit matrix q (the even input
+ * index in the low nibble). */
+static uint8_t nibble(const uint8_t *q, int64_t n, int64_t K, int64_t c)
+{
+    uint8_t byte = q[(n * K + c) / 2];
+    return (c % 2 == 0) ? (byte & 15) : (byte >> 4);
 }
 
 /* Dequantised weight of matrix `mat` (0 gate, 1 up, 2 down) of expert e, row n, input c. */
@@ -227,13 +242,17 @@ static double weight(const experts_t *X, int e, int mat, int64_t n, int64_t c)
         const uint8_t *q = w + (int64_t)mat * I * H;
         const float *sc = (const float *)s + (int64_t)mat * (I / 128) * (H / 128);
         return oracle_dec_e4m3(q[n * K + c]) * (double)sc[(n / 128) * (K / 128) + c / 128];
-    } else {
+    } else if (X->wfmt == WF_MXFP4) {
         const uint8_t *q = w + (int64_t)mat * I * H / 2;
         const uint8_t *sc = s + (int64_t)mat * I * H / 32;
-        uint8_t byte = q[(n * K + c) / 2];
-        uint8_t nib = (c % 2 == 0) ? (byte & 15) : (byte >> 4);
         (void)N;
-        return oracle_dec_e2m1(nib) * oracle_dec_e8m0(sc[n * (K / 32) + c / 32]);
+        return oracle_dec_e2m1(nibble(q, n, K, c)) * oracle_dec_e8m0(sc[n * (K / 32) + c / 32]);
+    } else {
+        const uint8_t *q = w + (int64_t)mat * I * H / 2;
+        float ts;
+        memcpy(&ts, s + 4 * mat, 4);
+        const uint8_t *sb = s + 16 + (int64_t)mat * I * H / 16;
+        return oracle_dec_e2m1(nibble(q, n, K, c)) * oracle_dec_e4m3(sb[n * (K / 16) + c / 16]) * (double)ts;
     }
 }
 
@@ -295,6 +314,8 @@ int oracle_forward(int64_t H, int E, int64_t I, int act_dtype, int router_dtype,
     if (k < 1 || k > E || H <= 0 || I <= 0 || T <= 0) return -1;
     if (wfmt == WF_FP8 && (H % 128 || I % 128)) return -1;
     if (wfmt == WF_MXFP4 && (H % 32 || I % 32)) return -1;
+    if (wfmt == WF_NVFP4 && (H % 16 || I % 16)) return -1;
+    if (wfmt < WF_FP8 || wfmt > WF_NVFP4) return -1;
     if (!tokens) n_sel = T;
     experts_t X = {H, I, E, wfmt, (const uint8_t *)expert_w, scales};
     int64_t esz = act_dtype == DT_BF16 ? 2 : 4;

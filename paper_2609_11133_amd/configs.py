@@ -24,14 +24,15 @@ class LayerConfig:
     inter: int
     act: str  # "bf16" or "f32"
     router: str  # "bf16" or "f32"
-    wfmt: str  # "fp8" (E4M3, 128x128 fp32 block scales) or "mxfp4" (E2M1, E8M0 per 32)
+    wfmt: str  # "fp8" (E4M3, 128x128 fp32 block scales), "mxfp4" (E2M1, E8M0 per 32) or
+    #            "nvfp4" (E2M1, E4M3 per 16, fp32 per matrix)
     bias: Optional[str]  # None, "normal:0.5" (sd) or "zipf:1.1"
     tokens: List[int] = field(default_factory=list)
     layers: int = 1
 
     @property
     def wfmt_id(self) -> int:
-        return 0 if self.wfmt == "fp8" else 1
+        return {"fp8": 0, "mxfp4": 1, "nvfp4": 2}[self.wfmt]
 
     def expert_weight_bytes(self) -> int:
         H, I = self.hidden, self.inter
@@ -39,7 +40,21 @@ class LayerConfig:
 
     def expert_scale_bytes(self) -> int:
         H, I = self.hidden, self.inter
-        return 4 * 3 * (H // 128) * (I // 128) if self.wfmt == "fp8" else 3 * H * I // 32
+        if self.wfmt == "fp8":
+            return 4 * 3 * (H // 128) * (I // 128)
+        if self.wfmt == "mxfp4":
+            return 3 * H * I // 32
+        return 16 + 3 * H * I // 16
+
+    def matrix_bytes(self, mat: int) -> int:
+        """Weight + scale bytes of one matrix of one expert (0 gate, 1 up, 2 down);
+        the NVFP4 matrix scales (16 bytes per expert) are counted with the gate."""
+        H, I = self.hidden, self.inter
+        if self.wfmt == "fp8":
+            return H * I + 4 * (H // 128) * (I // 128)
+        if self.wfmt == "mxfp4":
+            return H * I // 2 + H * I // 32
+        return H * I // 2 + H * I // 16 + (16 if mat == 0 else 0)
 
     def expert_bytes(self) -> int:
         """Algorithmic bytes streamed per activated expert (weights + scales)."""
@@ -47,10 +62,10 @@ class LayerConfig:
 
     def w13_bytes(self) -> int:
         """Gate+up bytes (weights + scales) of one expert."""
-        return (self.expert_weight_bytes() * 2) // 3 + (self.expert_scale_bytes() * 2) // 3
+        return self.matrix_bytes(0) + self.matrix_bytes(1)
 
     def w2_bytes(self) -> int:
-        return self.expert_bytes() - self.w13_bytes()
+        return self.matrix_bytes(2)
 
 
 TINY = LayerConfig("tiny", 256, 8, 2, 128, "f32", "f32", "fp8", None, [4])
@@ -75,5 +90,11 @@ QWEN3_235B_MXFP4 = LayerConfig(
     "qwen3-235b-a22b-mxfp4-zipf", 4096, 128, 8, 1536, "bf16", "bf16", "mxfp4", "zipf:1.1", [256]
 )
 
-ALL = [TINY, QWEN3_235B, QWEN3_480B, QWEN3_480B_X12, QWEN3_235B_MXFP4]
+# The paper deploys Qwen3-235B-A22B in NVFP4 (Experimental Setup, models row).
+QWEN3_235B_NVFP4 = LayerConfig("qwen3-235b-a22b-nvfp4", 4096, 128, 8, 1536, "bf16", "bf16", "nvfp4", None, [1, 8, 32, 64])
+QWEN3_235B_NVFP4_ZIPF = LayerConfig(
+    "qwen3-235b-a22b-nvfp4-zipf", 4096, 128, 8, 1536, "bf16", "bf16", "nvfp4", "zipf:1.1", [256]
+)
+
+ALL = [TINY, QWEN3_235B, QWEN3_480B, QWEN3_480B_X12, QWEN3_235B_MXFP4, QWEN3_235B_NVFP4, QWEN3_235B_NVFP4_ZIPF]
 BY_NAME = {c.name: c for c in ALL}

@@ -4,7 +4,8 @@ Every tensor is a pure function of ``(seed, tag, layer/batch, index)``: the same
 bytes come out on any machine and any slice can be regenerated on its own.  The
 module holds no arithmetic of the layer itself; it only draws Gaussian values and
 quantises weights into the formats the layer consumes (FP8-E4M3 with 128x128 fp32
-block scales, or MXFP4 = E2M1 with one E8M0 scale per 32 inputs).
+block scales, MXFP4 = E2M1 with one E8M0 scale per 32 inputs, or NVFP4 = E2M1 with
+one E4M3 scale per 16 inputs and one fp32 scale per matrix).
 """
 from __future__ import annotations
 
@@ -20,6 +21,7 @@ _LIB = os.path.join(_HERE, "libsynth.so")
 
 WFMT_FP8 = 0
 WFMT_MXFP4 = 1
+WFMT_NVFP4 = 2
 
 
 def build(force: bool = True) -> str:
@@ -148,7 +150,8 @@ def experts(seed: int, layer: int, wfmt: int, E: int, H: int, I: int, e0: int = 
     """Quantised expert weights for experts [e0, e1) of one layer.
 
     Returns ``(w, s)``: ``w`` uint8 [n, expert_bytes], ``s`` [n, ...] float32 block
-    scales (FP8) or uint8 E8M0 scales (MXFP4), packed as the library expects.
+    scales (FP8), uint8 E8M0 scales (MXFP4), or uint8 bytes holding four fp32 matrix
+    scales followed by E4M3 block scales (NVFP4), packed as the library expects.
     """
     if e1 is None:
         e1 = E

@@ -25,12 +25,21 @@
  *     consecutive inputs of a row, shared exponent floor(log2(amax)) - 2, codes are
  *     round-to-nearest-even of w/X, saturated to +-6.  Two codes per byte, the even
  *     input index in the low nibble.
+ *   NVFP4 (NVIDIA's two-level 4-bit format): E2M1 elements, one E4M3 scale per 16
+ *     consecutive inputs of a row and one fp32 scale per matrix.  The matrix scale is
+ *     ts = amax(matrix) / (6 * 448) rounded to fp32 (1 if the matrix is zero), so the
+ *     block scales s = RNE_E4M3(amax(block) / (6 * ts)) use the whole E4M3 range;
+ *     codes are round-to-nearest-even of w / (s * ts), saturated to +-6, and 0 where
+ *     s rounds to 0.  Packing as MXFP4.
  *
  * Expert weight packing (per expert e, one contiguous block):
  *   FP8  : gate [I][H] bytes | up [I][H] | down [H][I]            (3*H*I bytes)
  *          scales fp32: gate [I/128][H/128] | up [I/128][H/128] | down [H/128][I/128]
  *   MXFP4: gate [I][H/2] | up [I][H/2] | down [H][I/2]             (3*H*I/2 bytes)
  *          scales E8M0: gate [I][H/32] | up [I][H/32] | down [H][I/32]
+ *   NVFP4: weights as MXFP4
+ *          scales: fp32 matrix scales {gate, up, down, 0} (16 bytes), then E4M3 block
+ *          scales gate [I][H/16] | up [I][H/16] | down [H][I/16]
  */
 #include <math.h>
 #include <stdint.h>
@@ -253,11 +262,47 @@ static void quant_mxfp4_matrix(uint64_t key, double sigma, int64_t N, int64_t K,
         }
 }
 
+/* NVFP4 matrix [N][K]: codes q (packed as MXFP4), E4M3 block scales sc [N][K/16], and
+ * the fp32 matrix scale *ts.  Two passes over the counter stream: the matrix maximum
+ * first, then the blocks. */
+static void quant_nvfp4_matrix(uint64_t key, double sigma, int64_t N, int64_t K, uint8_t *q, uint8_t *sc, float *ts)
+{
+    double amax_m = 0.0;
+    for (int64_t i = 0; i < N * K; i++) {
+        double a = fabs(sigma * normal_at(key, (uint64_t)i));
+        if (a > amax_m) amax_m = a;
+    }
+    float t = amax_m > 0.0 ? (float)(amax_m / (6.0 * 448.0)) : 1.0f;
+    *ts = t;
+    double v[16];
+    for (int64_t n = 0; n < N; n++)
+        for (int64_t b = 0; b < K / 16; b++) {
+            double amax = 0.0;
+            for (int c = 0; c < 16; c++) {
+                v[c] = sigma * normal_at(key, (uint64_t)(n * K + b * 16 + c));
+                if (fabs(v[c]) > amax) amax = fabs(v[c]);
+            }
+            uint8_t s = synth_e4m3_from_f64(amax / (6.0 * (double)t));
+            sc[n * (K / 16) + b] = s;
+            /* decode the (positive) scale code: (1 + m/8) 2^(e-7), subnormal m 2^-9 */
+            int e = (s >> 3) & 15, m = s & 7;
+            double sv = e == 0 ? ldexp((double)m, -9) : ldexp((double)(8 + m), e - 10);
+            double X = sv * (double)t;
+            for (int c = 0; c < 16; c += 2) {
+                uint8_t lo = X > 0.0 ? synth_e2m1_from_f64(v[c] / X) : 0;
+                uint8_t hi = X > 0.0 ? synth_e2m1_from_f64(v[c + 1] / X) : 0;
+                q[(n * K + b * 16 + c) / 2] = (uint8_t)(lo | (hi << 4));
+            }
+        }
+}
+
 int64_t synth_expert_bytes(int wfmt, int64_t H, int64_t I) { return wfmt == 0 ? 3 * H * I : 3 * H * I / 2; }
 
 int64_t synth_expert_scale_bytes(int wfmt, int64_t H, int64_t I)
 {
-    return wfmt == 0 ? 4 * 3 * (H / 128) * (I / 128) : 3 * H * I / 32;
+    if (wfmt == 0) return 4 * 3 * (H / 128) * (I / 128);
+    if (wfmt == 1) return 3 * H * I / 32;
+    return 16 + 3 * H * I / 16;
 }
 
 /* One expert of one layer, FP8-E4M3 with 128x128 fp32 block scales. */
@@ -282,6 +327,20 @@ void synth_expert_mxfp4(uint64_t seed, uint32_t layer, int64_t e, int64_t H, int
     quant_mxfp4_matrix(synth_stream_key(seed, TAG_DOWN, layer, (uint32_t)e), sd, H, I, w + I * H, s + 2 * I * H / 32);
 }
 
+/* One expert of one layer, NVFP4 (E2M1 + E4M3 per 16 + fp32 per matrix). */
+void synth_expert_nvfp4(uint64_t seed, uint32_t layer, int64_t e, int64_t H, int64_t I, uint8_t *w, uint8_t *s)
+{
+    double sg = 1.0 / sqrt((double)H), sd = 1.0 / sqrt((double)I);
+    float ts[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    uint8_t *blk = s + 16;
+    quant_nvfp4_matrix(synth_stream_key(seed, TAG_GATE, layer, (uint32_t)e), sg, I, H, w, blk, &ts[0]);
+    quant_nvfp4_matrix(synth_stream_key(seed, TAG_UP, layer, (uint32_t)e), sg, I, H, w + I * H / 2, blk + I * H / 16,
+                       &ts[1]);
+    quant_nvfp4_matrix(synth_stream_key(seed, TAG_DOWN, layer, (uint32_t)e), sd, H, I, w + I * H,
+                       blk + 2 * I * H / 16, &ts[2]);
+    memcpy(s, ts, sizeof ts);
+}
+
 /* Experts [e0, e1) of a layer; the tensors for expert e are written at offset
  * (e - e0) * per-expert size.  Parallel over experts. */
 void synth_experts(uint64_t seed, uint32_t layer, int wfmt, int64_t e0, int64_t e1, int64_t H, int64_t I,
@@ -294,7 +353,9 @@ void synth_experts(uint64_t seed, uint32_t layer, int wfmt, int64_t e0, int64_t 
         uint8_t *se = (uint8_t *)s + (e - e0) * sb;
         if (wfmt == 0)
             synth_expert_fp8(seed, layer, e, H, I, we, (float *)se);
-        else
+        else if (wfmt == 1)
             synth_expert_mxfp4(seed, layer, e, H, I, we, se);
+        else
+            synth_expert_nvfp4(seed, layer, e, H, I, we, se);
     }
 }

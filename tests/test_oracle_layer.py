@@ -58,12 +58,37 @@ def split_mxfp4_expert(w, s, H, I):
     return g, u, d
 
 
+def dequant_nvfp4_numpy(wq, sb, ts, N, K):
+    """Independent NVFP4 dequantisation: the OCP E2M1 table, torch's float8_e4m3fn
+    decoder for the per-16 block scales, and the fp32 matrix scale."""
+    tab = e2m1_table()
+    b = np.asarray(wq, np.uint8).reshape(N, K // 2)
+    codes = np.empty((N, K), np.int64)
+    codes[:, 0::2] = b & 15
+    codes[:, 1::2] = b >> 4
+    s = torch.from_numpy(np.ascontiguousarray(sb).reshape(N, K // 16)).view(torch.float8_e4m3fn)
+    s = s.to(torch.float64).numpy()
+    return tab[codes] * np.repeat(s, 16, axis=1) * float(ts)
+
+
+def split_nvfp4_expert(w, s, H, I):
+    ts = np.ascontiguousarray(s[:16]).view(np.float32)
+    blk = s[16:]
+    g = dequant_nvfp4_numpy(w[: I * H // 2], blk[: I * H // 16], ts[0], I, H)
+    u = dequant_nvfp4_numpy(w[I * H // 2: I * H], blk[I * H // 16: 2 * I * H // 16], ts[1], I, H)
+    d = dequant_nvfp4_numpy(w[I * H:], blk[2 * I * H // 16:], ts[2], H, I)
+    return g, u, d
+
+
+SPLIT = {0: split_fp8_expert, 1: split_mxfp4_expert, 2: split_nvfp4_expert}
+
+
 def dense_swiglu(x, g, u, d):
     a = x @ g.T
     return ((a / (1.0 + np.exp(-a))) * (x @ u.T)) @ d.T
 
 
-@pytest.mark.parametrize("wfmt", [0, 1])
+@pytest.mark.parametrize("wfmt", [0, 1, 2])
 def test_single_expert_is_dense_swiglu(wfmt):
     H, I, T = 256, 128, 6
     x = synth.x_bf16(31, 0, T, H)
@@ -71,8 +96,7 @@ def test_single_expert_is_dense_swiglu(wfmt):
     w, s = synth.experts(31, 0, wfmt, 1, H, I)
     _, ids, wts, y = oracle.forward(x, rw, None, w, s, 1, I, wfmt)
     assert np.all(ids == 0) and np.all(wts == 1.0)
-    split = split_fp8_expert if wfmt == 0 else split_mxfp4_expert
-    g, u, d = split(w[0], s[0], H, I)
+    g, u, d = SPLIT[wfmt](w[0], s[0], H, I)
     ref = dense_swiglu(bf16_to_f64(x), g, u, d)
     np.testing.assert_allclose(y, ref, rtol=1e-11, atol=1e-13 * np.abs(ref).max())
 
@@ -123,7 +147,7 @@ def _layer(E=8, H=256, I=128, k=2, T=6, wfmt=0, seed=41, bias=True):
     return x, rw, b, w, s
 
 
-@pytest.mark.parametrize("wfmt", [0, 1])
+@pytest.mark.parametrize("wfmt", [0, 1, 2])
 def test_relabel_experts_invariance(wfmt):
     E, H, I, k = 8, 256, 128, 3
     x, rw, b, w, s = _layer(E=E, k=k, wfmt=wfmt)
@@ -150,7 +174,7 @@ def test_token_permutation_and_batch_independence():
     assert np.array_equal(y4[0], y[3])
 
 
-@pytest.mark.parametrize("wfmt", [0, 1])
+@pytest.mark.parametrize("wfmt", [0, 1, 2])
 def test_doubling_down_scales_doubles_output(wfmt):
     E, H, I, k = 8, 256, 128, 2
     x, rw, b, w, s = _layer(E=E, k=k, wfmt=wfmt)
@@ -159,8 +183,10 @@ def test_doubling_down_scales_doubles_output(wfmt):
     if wfmt == 0:
         nsg = 2 * (I // 128) * (H // 128)
         s2[:, nsg:] *= 2
-    else:
+    elif wfmt == 1:
         s2[:, 2 * I * H // 32:] += 1
+    else:
+        s2[:, 8:12] = (s2[:, 8:12].copy().view(np.float32) * 2).view(np.uint8)  # the down matrix scale
     _, _, _, y2 = oracle.forward(x, rw, b, w, s2, k, I, wfmt)
     assert np.array_equal(y2, 2 * y)
 
@@ -186,6 +212,49 @@ def test_all_experts_selected_k_equals_e():
             g, u, d = split_fp8_expert(w[ids[t, j]], s[ids[t, j]], H, I)
             ref[t] += wts[t, j] * dense_swiglu(xf[t:t + 1], g, u, d)[0]
     np.testing.assert_allclose(y, ref, rtol=1e-11, atol=1e-13 * np.abs(ref).max())
+
+
+def test_nvfp4_block_scale_closed_form():
+    """One NVFP4 expert with hand-set codes: gate row i holds code c_i at input i and
+    block scale S_i, up row i holds 1.0 with scale 1, down row i holds 1.0 at input i,
+    and matrix scales tg, tu, td: y[h] = td * silu(tg * e2m1(c_h) * S_h * x_h) * tu * x_h
+    for h < I, 0 above.  Block scales differ in their mantissa bits, so a scale applied
+    per 32 inputs or without its mantissa fails."""
+    H, I, E = 256, 128, 1
+    codes = [0x2, 0x3, 0x5, 0x7, 0x9, 0xB, 0xD, 0xF]  # 1, 1.5, 3, 6 and their negatives
+    scodes = [0x38, 0x39, 0x3A, 0x3B, 0x3C, 0x3D, 0x3E, 0x3F, 0x30, 0x41, 0x2B]  # 1 .. 1.875, 0.5, 2.25, 0.34375
+    tg, tu, td = np.float32(0.75), np.float32(1.25), np.float32(0.5)
+    gate = np.zeros((I, H), np.uint8)
+    up = np.zeros((I, H), np.uint8)
+    down = np.zeros((H, I), np.uint8)
+    sg = np.zeros((I, H // 16), np.uint8)
+    su = np.full((I, H // 16), 0x38, np.uint8)
+    sd = np.full((H, I // 16), 0x38, np.uint8)
+    for i in range(I):
+        gate[i, i] = codes[i % len(codes)]
+        sg[i, i // 16] = scodes[i % len(scodes)]
+        up[i, i] = 0x2
+        down[i, i] = 0x2
+
+    def pack(m):
+        return (m[:, 0::2] | (m[:, 1::2] << 4)).astype(np.uint8).ravel()
+
+    w = np.concatenate([pack(gate), pack(up), pack(down)])[None, :]
+    ts = np.array([tg, tu, td, 0], np.float32).view(np.uint8)
+    s = np.concatenate([ts, sg.ravel(), su.ravel(), sd.ravel()])[None, :]
+    T = 4
+    x = synth.x_bf16(34, 0, T, H)
+    rw = synth.router_bf16(34, 0, E, H)
+    _, _, _, y = oracle.forward(x, rw, None, w, s, 1, I, 2)
+    tab = e2m1_table()
+    s_of = lambda c: torch.tensor([c], dtype=torch.uint8).view(torch.float8_e4m3fn).double().item()
+    xf = bf16_to_f64(x)
+    ref = np.zeros((T, H))
+    for h in range(I):
+        gv = float(tg) * tab[codes[h % len(codes)]] * s_of(scodes[h % len(scodes)]) * xf[:, h]
+        ref[:, h] = float(td) * gv / (1.0 + np.exp(-gv)) * float(tu) * xf[:, h]
+    np.testing.assert_allclose(y, ref, rtol=1e-14, atol=1e-16)
+    assert np.all(y[:, I:] == 0.0)
 
 
 def test_tiny_config_under_one_second():

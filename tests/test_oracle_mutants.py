@@ -33,6 +33,12 @@ MUTANTS = {
     "acc_drops_sign": ("a->d[off / 32 + i] += q < 0 ? -dig : dig;", "a->d[off / 32 + i] += dig;"),
     "subnormal_grid": ("if (lsb < -149) lsb = -149;", "if (lsb < -150) lsb = -150;"),
     "e8m0_bias": ("ldexp(1.0, (int)c - 127)", "ldexp(1.0, (int)c - 128)"),
+    "nvfp4_block_32": ("sb[n * (K / 16) + c / 16]", "sb[n * (K / 16) + c / 32]"),
+    "nvfp4_no_matrix_scale": ("oracle_dec_e4m3(sb[n * (K / 16) + c / 16]) * (double)ts;",
+                              "oracle_dec_e4m3(sb[n * (K / 16) + c / 16]);"),
+    "nvfp4_gate_scale_for_all": ("memcpy(&ts, s + 4 * mat, 4);", "memcpy(&ts, s, 4);"),
+    "nvfp4_scale_bytes_skip_header": ("const uint8_t *sb = s + 16 + (int64_t)mat * I * H / 16;",
+                                      "const uint8_t *sb = s + (int64_t)mat * I * H / 16;"),
     "softmax_without_bias_in_weights": ("pe[e] = exp((double)l[e] - m);", "pe[e] = exp((double)l[e] - m - (bias ? bias[e] : 0));"),
 }
 
@@ -139,10 +145,10 @@ def pin_dense(o):
     H, I = 256, 128
     x = synth.x_bf16(31, 0, 3, H)
     rw = synth.router_bf16(31, 0, 1, H)
-    for wfmt in (0, 1):
+    for wfmt in (0, 1, 2):
         w, s = synth.experts(31, 0, wfmt, 1, H, I)
         _, _, _, y = o.forward(x, rw, None, w, s, 1, I, wfmt)
-        g, u, d = (L.split_fp8_expert if wfmt == 0 else L.split_mxfp4_expert)(w[0], s[0], H, I)
+        g, u, d = L.SPLIT[wfmt](w[0], s[0], H, I)
         ref = L.dense_swiglu(bf16_f64(x), g, u, d)
         if not np.allclose(y, ref, rtol=1e-11, atol=1e-13 * np.abs(ref).max()):
             return False

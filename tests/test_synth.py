@@ -82,3 +82,21 @@ def test_mxfp4_groups_scale():
     mags = (codes & 7).reshape(I, H // 32, 32).max(axis=-1)
     # amax / 2^(floor(log2 amax) - 2) lies in [4, 8): the largest code is 4.0, 6.0 (or saturates to 6)
     assert np.all(mags >= 6)
+
+
+def test_nvfp4_two_level_scales():
+    """NVFP4 recipe: the matrix scale maps the matrix maximum to 6 x 448, every block's
+    E4M3 scale is positive and maps its block maximum onto the top E2M1 code (6), and
+    the block holding the matrix maximum gets the largest scale code (448)."""
+    H, I = 256, 128
+    w, s = synth.experts(12, 0, 2, 1, H, I)
+    ts = s[0, :16].copy().view(np.float32)
+    assert ts[3] == 0.0 and np.all(ts[:3] > 0)
+    g = w[0, : I * H // 2].reshape(I, H // 2)
+    codes = np.stack([g & 15, g >> 4], axis=-1).reshape(I, H)
+    sg = s[0, 16: 16 + I * H // 16].reshape(I, H // 16)
+    assert np.all(sg < 0x80)  # positive scales
+    assert np.all((codes & 7).reshape(I, H // 16, 16).max(axis=-1) == 7)
+    assert sg.max() == 0x7E
+    v = synth.normal(12, "gate", 0, 0, 0, I * H, 1.0 / np.sqrt(H))
+    assert np.float32(np.abs(v).max() / (6 * 448)) == ts[0]
