@@ -383,7 +383,8 @@ def main():
                         f"SwiGLU intermediate {cfg.inter}, {cfg.wfmt} weights, {cfg.act} activations, "
                         f"T={T_main} tokens per step",
             "tokens_per_step": T_main,
-            "weights": "fp8-e4m3, fp32 scale per 128x128 block" if cfg.wfmt == "fp8" else "mxfp4 (e2m1 + e8m0/32)",
+            "weights": {"fp8": "fp8-e4m3, fp32 scale per 128x128 block", "mxfp4": "mxfp4 (e2m1 + e8m0/32)",
+                        "nvfp4": "nvfp4 (e2m1 + e4m3/16 + fp32/matrix)"}[cfg.wfmt],
             "activations": cfg.act,
             "cold_cache": f"{copies} weight copies x 16 token batches cycled",
         },
@@ -396,8 +397,10 @@ def main():
             "n_active_mean": R["n_active_mean"],
         },
         "roofline": {
-            "kernel": ("w13_mfma_lds_kernel (grouped gate/up + SiLU-gate, activations staged in LDS, MFMA for every expert)"
-                       if args.mstar in (0, 1) else "w13 stage (GEMV and MFMA kernels)"),
+            "kernel": (("w13_nvfp4_kernel (grouped gate/up + SiLU-gate, weights dequantised to bf16 in registers, "
+                        "bf16 MFMA)" if cfg.wfmt == "nvfp4" else
+                        "w13_mfma_lds_kernel (grouped gate/up + SiLU-gate, activations staged in LDS, MFMA for every "
+                        "expert)") if args.mstar in (0, 1) else "w13 stage (GEMV and MFMA kernels)"),
             "bound": "hbm",
             "achieved": R["w13_GBs"],
             "peak": PEAK_HBM_GBS,

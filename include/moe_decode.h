@@ -19,7 +19,9 @@
  *                     a = silu(g) * u with silu(z) = z / (1 + e^-z), o = Wdown[e] a
  *   5. combine        y[t] = sum_j w[t,j] * o[t,j], j ascending
  * Weights are dequantised in registers: FP8 E4M3FN (OCP) times one fp32 scale per
- * 128x128 block, or MXFP4 (OCP MX v1.0: E2M1 times 2^(E8M0-127) per 32 inputs).
+ * 128x128 block, MXFP4 (OCP MX v1.0: E2M1 times 2^(E8M0-127) per 32 inputs), or
+ * NVFP4 (E2M1 times an E4M3 scale per 16 inputs times an fp32 scale per matrix; the
+ * paper deploys Qwen3-235B-A22B in this format, Experimental Setup, models row).
  *
  * Memory: every tensor pointer is a DEVICE pointer owned by the caller.  The library
  * never allocates device memory: its scratch lives in a caller-provided workspace
@@ -31,12 +33,15 @@
  *   router_bias   [E]     fp32, or NULL for no bias
  *   expert_w      E consecutive expert blocks; expert e at byte e * expert_stride:
  *                   FP8  : gate [I][H] | up [I][H] | down [H][I]           1 byte/weight
- *                   MXFP4: gate [I][H/2] | up [I][H/2] | down [H][I/2]     even input
- *                          index in the low nibble
+ *                   MXFP4, NVFP4: gate [I][H/2] | up [I][H/2] | down [H][I/2]
+ *                          even input index in the low nibble
  *                 (input index contiguous in every row)
  *   scales        FP8  : fp32, per expert gate [I/128][H/128] | up [I/128][H/128] |
  *                        down [H/128][I/128]
  *                 MXFP4: E8M0 bytes, per expert gate [I][H/32] | up [I][H/32] | down [H][I/32]
+ *                 NVFP4: per expert 16 bytes of fp32 matrix scales {gate, up, down, unused},
+ *                        then E4M3 bytes gate [I][H/16] | up [I][H/16] | down [H][I/16]
+ *                        (block scales are positive codes; expert stride 16 + 3*H*I/16)
  *   topk_ids      [T][k] int32 (optional output), topk_weights [T][k] fp32 (optional)
  *
  * Errors: every argument check runs before anything is enqueued; a failed check
@@ -72,14 +77,16 @@ typedef enum {
 typedef enum { MOE_DTYPE_F32 = 0, MOE_DTYPE_BF16 = 1 } moe_dtype;
 
 typedef enum {
-    MOE_WFMT_FP8_E4M3_B128 = 0, /* E4M3FN weights, fp32 scale per 128x128 block */
-    MOE_WFMT_MXFP4_E2M1_B32 = 1 /* E2M1 weights, E8M0 scale per 32 inputs */
+    MOE_WFMT_FP8_E4M3_B128 = 0,  /* E4M3FN weights, fp32 scale per 128x128 block */
+    MOE_WFMT_MXFP4_E2M1_B32 = 1, /* E2M1 weights, E8M0 scale per 32 inputs */
+    MOE_WFMT_NVFP4_E2M1_B16 = 2  /* E2M1 weights, E4M3 scale per 16 inputs, fp32 scale per matrix;
+                                    needs bf16 activations */
 } moe_wfmt;
 
 typedef struct moe_decode_config {
-    int32_t hidden;          /* H: multiple of 128 (FP8) or 256 (MXFP4) */
+    int32_t hidden;          /* H: multiple of 128 (FP8) or 256 (MXFP4, NVFP4) */
     int32_t n_experts;       /* E: 1..1024 */
-    int32_t inter;           /* I: SwiGLU intermediate size, multiple of 128 (FP8) or 256 (MXFP4) */
+    int32_t inter;           /* I: SwiGLU intermediate size, multiple of 128 (FP8) or 256 (MXFP4, NVFP4) */
     int32_t max_topk;        /* largest k of any call: 1..min(E, 64) */
     int32_t max_tokens;      /* largest T of any call: 1..1024, E * ceil(T/32) <= 8192 */
     int32_t act_dtype;       /* moe_dtype of x and y */

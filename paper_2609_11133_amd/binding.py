@@ -16,7 +16,7 @@ LIB_PATH = os.environ.get("MOE_DECODE_LIB") or os.path.join(_PKG, "libmoe_decode
 
 MOE_OK, MOE_ERR_INVALID, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP = 0, -1, -2, -3, -4
 MOE_DTYPE_F32, MOE_DTYPE_BF16 = 0, 1
-MOE_WFMT_FP8_E4M3_B128, MOE_WFMT_MXFP4_E2M1_B32 = 0, 1
+MOE_WFMT_FP8_E4M3_B128, MOE_WFMT_MXFP4_E2M1_B32, MOE_WFMT_NVFP4_E2M1_B16 = 0, 1, 2
 MOE_STAGE_ROUTE, MOE_STAGE_W13, MOE_STAGE_W2, MOE_STAGE_COMBINE, MOE_N_STAGES = 0, 1, 2, 3, 4
 STAGE_NAMES = ["route", "w13", "w2", "combine"]
 

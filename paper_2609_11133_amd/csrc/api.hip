@@ -14,7 +14,7 @@ namespace moe {
 
 static size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
-size_t carve_workspace(int H, int E, int I, int kmax, int Tmax, void *base, Workspace *ws)
+size_t carve_workspace(int H, int E, int I, int kmax, int Tmax, int wfmt, void *base, Workspace *ws)
 {
     const size_t P = (size_t)Tmax * kmax;  // (token, choice) pairs = slots
     const MetaIdx mi{E, max_mfma_chunks(E, Tmax, kmax)};
@@ -24,7 +24,7 @@ size_t carve_workspace(int H, int E, int I, int kmax, int Tmax, void *base, Work
         off += align256(bytes);
         return (char *)base + o;
     };
-    Workspace w;
+    Workspace w = {};
     w.logits = (float *)take(sizeof(float) * (size_t)Tmax * E);
     w.ids = (int32_t *)take(sizeof(int32_t) * P);
     w.wts = (float *)take(sizeof(float) * P);
@@ -34,14 +34,18 @@ size_t carve_workspace(int H, int E, int I, int kmax, int Tmax, void *base, Work
     w.h = (float *)take(sizeof(float) * P * I);
     w.o = (float *)take(sizeof(float) * P * H);
     w.sync = (int32_t *)take(sizeof(int32_t) * ((size_t)Tmax + 2) * kCounterStride);
-    w.xs_hi = (uint8_t *)take((size_t)Tmax * H);
-    w.xs_lo = (uint8_t *)take((size_t)Tmax * H);
-    w.xe_hi = (uint8_t *)take((size_t)Tmax * H / 32);
-    w.xe_lo = (uint8_t *)take((size_t)Tmax * H / 32);
-    w.hs_hi = (uint8_t *)take(P * I);
-    w.hs_lo = (uint8_t *)take(P * I);
-    w.he_hi = (uint8_t *)take(P * I / 32);
-    w.he_lo = (uint8_t *)take(P * I / 32);
+    if (wfmt == MOE_WFMT_NVFP4_E2M1_B16) {
+        w.hb = (__bf16 *)take(2 * P * I);
+    } else {
+        w.xs_hi = (uint8_t *)take((size_t)Tmax * H);
+        w.xs_lo = (uint8_t *)take((size_t)Tmax * H);
+        w.xe_hi = (uint8_t *)take((size_t)Tmax * H / 32);
+        w.xe_lo = (uint8_t *)take((size_t)Tmax * H / 32);
+        w.hs_hi = (uint8_t *)take(P * I);
+        w.hs_lo = (uint8_t *)take(P * I);
+        w.he_hi = (uint8_t *)take(P * I / 32);
+        w.he_lo = (uint8_t *)take(P * I / 32);
+    }
     w.bytes = off;
     if (ws) *ws = w;
     return off;
@@ -84,7 +88,7 @@ static moe_status check_config(const moe_decode_config *c, char *err)
     if (!c) FAIL(err, MOE_ERR_INVALID, "config is NULL");
     for (int i = 0; i < 7; ++i)
         if (c->reserved[i] != 0) FAIL(err, MOE_ERR_INVALID, "config.reserved[%d] must be zero", i);
-    if (c->wfmt != MOE_WFMT_FP8_E4M3_B128 && c->wfmt != MOE_WFMT_MXFP4_E2M1_B32)
+    if (c->wfmt != MOE_WFMT_FP8_E4M3_B128 && c->wfmt != MOE_WFMT_MXFP4_E2M1_B32 && c->wfmt != MOE_WFMT_NVFP4_E2M1_B16)
         FAIL(err, MOE_ERR_INVALID, "unknown weight format %d", c->wfmt);
     const int q = c->wfmt == MOE_WFMT_FP8_E4M3_B128 ? 128 : 256;
     if (c->hidden <= 0 || c->hidden % q) FAIL(err, MOE_ERR_INVALID, "hidden=%d must be a positive multiple of %d", c->hidden, q);
@@ -100,6 +104,8 @@ static moe_status check_config(const moe_decode_config *c, char *err)
         FAIL(err, MOE_ERR_INVALID, "unknown act_dtype %d", c->act_dtype);
     if (c->router_dtype != MOE_DTYPE_F32 && c->router_dtype != MOE_DTYPE_BF16)
         FAIL(err, MOE_ERR_INVALID, "unknown router_dtype %d", c->router_dtype);
+    if (c->wfmt == MOE_WFMT_NVFP4_E2M1_B16 && c->act_dtype != MOE_DTYPE_BF16)
+        FAIL(err, MOE_ERR_UNSUPPORTED, "NVFP4 weights need bf16 activations (the bf16 matrix cores take x as it is)");
     {
         // The GEMV path stages 4 activation rows of max(H, I) elements in LDS.  The
         // bound also keeps the MFMA path's 32-bit buffer offsets (T*H and T*k*I
@@ -117,7 +123,8 @@ size_t moe_decode_workspace_bytes(const moe_decode_config *cfg)
 {
     char err[256];
     if (check_config(cfg, err) != MOE_OK) return 0;
-    return carve_workspace(cfg->hidden, cfg->n_experts, cfg->inter, cfg->max_topk, cfg->max_tokens, nullptr, nullptr);
+    return carve_workspace(cfg->hidden, cfg->n_experts, cfg->inter, cfg->max_topk, cfg->max_tokens, cfg->wfmt, nullptr,
+                           nullptr);
 }
 
 size_t moe_decode_expert_weight_bytes(const moe_decode_config *cfg)
@@ -133,7 +140,9 @@ size_t moe_decode_expert_scale_bytes(const moe_decode_config *cfg)
     char err[256];
     if (check_config(cfg, err) != MOE_OK) return 0;
     const size_t H = cfg->hidden, I = cfg->inter;
-    return cfg->wfmt == MOE_WFMT_FP8_E4M3_B128 ? 4 * 3 * (H / 128) * (I / 128) : 3 * H * I / 32;
+    if (cfg->wfmt == MOE_WFMT_FP8_E4M3_B128) return 4 * 3 * (H / 128) * (I / 128);
+    if (cfg->wfmt == MOE_WFMT_MXFP4_E2M1_B32) return 3 * H * I / 32;
+    return 16 + 3 * H * I / 16;
 }
 
 moe_status moe_decode_init(const moe_decode_config *cfg, void *workspace, size_t workspace_bytes, moe_decode_t *out)
@@ -159,7 +168,8 @@ moe_status moe_decode_init(const moe_decode_config *cfg, void *workspace, size_t
     h->L.router_bf16 = cfg->router_dtype == MOE_DTYPE_BF16;
     h->L.expert_w_bytes = moe_decode_expert_weight_bytes(cfg);
     h->L.expert_s_bytes = moe_decode_expert_scale_bytes(cfg);
-    carve_workspace(cfg->hidden, cfg->n_experts, cfg->inter, cfg->max_topk, cfg->max_tokens, workspace, &h->ws);
+    carve_workspace(cfg->hidden, cfg->n_experts, cfg->inter, cfg->max_topk, cfg->max_tokens, cfg->wfmt, workspace,
+                    &h->ws);
     h->mstar = cfg->mfma_min_tokens == 0 ? kDefaultMfmaMinTokens : (cfg->mfma_min_tokens < 0 ? 0 : cfg->mfma_min_tokens);
     h->synced = 0;
     h->last_stream = nullptr;
@@ -295,14 +305,19 @@ moe_status moe_decode_forward(moe_decode_t h, void *stream, const void *x, int32
     const bool gemv = h->mstar != 1;
     CHECK(ensure_synced(h, st));
     if (prof) prof_mark(h, 0, st);
-    const RouteParams P = route_params(h, x, T, k, router_w, router_bias, topk_ids, topk_weights, mfma, true);
+    // NVFP4 MFMA kernels read x as it is; FP8 and MXFP4 ones read its 2-term FP8 split,
+    // which the routing kernel writes.
+    const bool nv = L.wfmt == MOE_WFMT_NVFP4_E2M1_B16;
+    const RouteParams P = route_params(h, x, T, k, router_w, router_bias, topk_ids, topk_weights, mfma && !nv, true);
     HIPCHECK(h, launch_route(L, P, st));
     if (prof) prof_mark(h, 1, st);
     if (gemv) HIPCHECK(h, launch_w13(L, expert_w, scales, x, T, k, w.meta, w.tok_of, w.h, st));
-    if (mfma) HIPCHECK(h, launch_w13_mfma(L, expert_w, scales, T, k, w.meta, w.tok_of, w, st));
+    if (mfma && nv) HIPCHECK(h, launch_w13_nvfp4(L, expert_w, scales, x, T, k, w.meta, w.tok_of, w, st));
+    if (mfma && !nv) HIPCHECK(h, launch_w13_mfma(L, expert_w, scales, T, k, w.meta, w.tok_of, w, st));
     if (prof) prof_mark(h, 2, st);
     if (gemv) HIPCHECK(h, launch_w2(L, expert_w, scales, T, k, w.meta, w.h, w.o, st));
-    if (mfma) HIPCHECK(h, launch_w2_mfma(L, expert_w, scales, T, k, w.meta, w, st));
+    if (mfma && nv) HIPCHECK(h, launch_w2_nvfp4(L, expert_w, scales, T, k, w.meta, w, st));
+    if (mfma && !nv) HIPCHECK(h, launch_w2_mfma(L, expert_w, scales, T, k, w.meta, w, st));
     if (prof) prof_mark(h, 3, st);
     HIPCHECK(h, launch_combine(L, T, k, w.slot_of, w.wts, w.o, y, st));
     if (prof) {

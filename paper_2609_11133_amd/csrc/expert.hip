@@ -113,6 +113,17 @@ struct Blk<1> {  // MXFP4: E2M1 pairs, E8M0 scale applied exactly in the convers
     }
 };
 
+template <>
+struct Blk<2> {  // NVFP4: E2M1 pairs converted exactly; the two E4M3 scales of the
+                 // block's 16-input halves multiply the half dots (see apply_chunk)
+    static constexpr int kCols = 32;
+    static constexpr int kPairs = 16;
+    __device__ static inline void cvt_bf16(const uint4 &w, float /*sc*/, uint32_t (&o)[kPairs])
+    {
+        Blk<1>::cvt_bf16(w, 1.0f, o);
+    }
+};
+
 // Converted block . staged activations of one token (bf16 pairs in LDS).
 template <int NP>
 __device__ inline float dot_bf16(const uint32_t (&wc)[NP], const uint4 *xp)
@@ -153,15 +164,15 @@ template <int FMT>
 struct TwoRows {
     const uint8_t *r0, *r1;  // row starts (bytes)
     const float *fs0, *fs1;  // FP8: per-128-input scale rows (uniform over the wave)
-    const uint8_t *es0, *es1;  // MXFP4: per-32-input E8M0 rows
-    int nblk;                // K / (16*8) FP8 or K / (32*8) MXFP4 blocks per lane
+    const uint8_t *es0, *es1;  // MXFP4: per-32-input E8M0 rows; NVFP4: per-16-input E4M3 rows
+    int nblk;                // K / (16*8) FP8 or K / (32*8) MXFP4 / NVFP4 blocks per lane
     int c;                   // lane within the row group
 };
 
 template <int FMT>
 struct Chunk {
     uint4 w[kD][2];
-    uint32_t e[kD][2];  // MXFP4 scale codes
+    uint32_t e[kD][2];  // MXFP4 scale code; NVFP4 the two E4M3 codes of the block's halves
 };
 
 template <int FMT>
@@ -177,8 +188,33 @@ __device__ inline void load_chunk(const TwoRows<FMT> &R, int b0, Chunk<FMT> &C)
         if constexpr (FMT == 1) {
             C.e[d][0] = R.es0[b * 8 + R.c];
             C.e[d][1] = R.es1[b * 8 + R.c];
+        } else if constexpr (FMT == 2) {
+            C.e[d][0] = *reinterpret_cast<const uint16_t *>(R.es0 + 2 * (b * 8 + R.c));
+            C.e[d][1] = *reinterpret_cast<const uint16_t *>(R.es1 + 2 * (b * 8 + R.c));
         }
     }
+}
+
+// E4M3 code (byte `sel` of v) -> fp32, exact.
+__device__ inline float e4m3_to_f32(uint32_t v, int sel)
+{
+    switch (sel) {
+    case 0: return __builtin_amdgcn_cvt_f32_fp8((int)v, 0);
+    default: return __builtin_amdgcn_cvt_f32_fp8((int)v, 1);
+    }
+}
+
+// Half-block dots of an NVFP4 block (pairs [0, 8) and [8, 16)) scaled by their E4M3 codes.
+__device__ inline float dot_nvfp4(const uint32_t (&wc)[16], uint32_t codes, const uint4 *xp)
+{
+    uint32_t lo[8], hi[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        lo[i] = wc[i];
+        hi[i] = wc[8 + i];
+    }
+    const float p0 = dot_bf16<8>(lo, xp), p1 = dot_bf16<8>(hi, xp + 2);
+    return fmaf(e4m3_to_f32(codes, 1), p1, e4m3_to_f32(codes, 0) * p0);
 }
 
 // Apply one chunk (blocks b0 .. b0+kD-1, those below nblk) to M staged tokens.
@@ -207,6 +243,16 @@ __device__ inline void apply_chunk(const TwoRows<FMT> &R, int b0, const Chunk<FM
                     const uint4 *xp = xs + m * xq + xoff;
                     a0[m] = fmaf(s0, dot_f32<NP>(c0, xp), a0[m]);
                     a1[m] = fmaf(s1, dot_f32<NP>(c1, xp), a1[m]);
+                }
+            } else if constexpr (FMT == 2) {
+                uint32_t c0[NP], c1[NP];
+                Blk<FMT>::cvt_bf16(C.w[d][0], 1.f, c0);
+                Blk<FMT>::cvt_bf16(C.w[d][1], 1.f, c1);
+#pragma unroll
+                for (int m = 0; m < M; ++m) {
+                    const uint4 *xp = xs + m * xq + xoff;
+                    a0[m] += dot_nvfp4(c0, C.e[d][0], xp);
+                    a1[m] += dot_nvfp4(c1, C.e[d][1], xp);
                 }
             } else {
                 uint32_t c0[NP], c1[NP];
@@ -304,12 +350,18 @@ __global__ __launch_bounds__(WAVES * 64) void w13_gemv_kernel(const uint8_t *__r
         R.r1 = we + (size_t)(I + i) * rowb;
         R.c = c;
         R.nblk = FMT == 0 ? H / 128 : H / 256;
+        float tg = 1.f, tu = 1.f;  // NVFP4 matrix scales
         if constexpr (FMT == 0) {
             R.fs0 = (const float *)se + (size_t)(ibase / 128) * (H / 128);
             R.fs1 = R.fs0 + (size_t)(I / 128) * (H / 128);
-        } else {
+        } else if constexpr (FMT == 1) {
             R.es0 = se + (size_t)i * (H / 32);
             R.es1 = se + (size_t)(I + i) * (H / 32);
+        } else {
+            tg = reinterpret_cast<const float *>(se)[0];
+            tu = reinterpret_cast<const float *>(se)[1];
+            R.es0 = se + 16 + (size_t)i * (H / 16);
+            R.es1 = se + 16 + (size_t)(I + i) * (H / 16);
         }
         for (int m0 = 0; m0 < M; m0 += mmax) {
             const int mc = min(mmax, M - m0);
@@ -351,7 +403,7 @@ __global__ __launch_bounds__(WAVES * 64) void w13_gemv_kernel(const uint8_t *__r
 #pragma unroll
                 for (int m = 0; m < kMaxM; ++m)
                     if (m < mc) {
-                        const float g = a0[m], u = a1[m];
+                        const float g = tg * a0[m], u = tu * a1[m];
                         hbuf[(size_t)(s0 + m0 + m) * I + i] = g / (1.0f + expf(-g)) * u;
                     }
             }
@@ -397,13 +449,19 @@ __global__ __launch_bounds__(WAVES * 64) void w2_gemv_kernel(const uint8_t *__re
         R.r1 = we + (size_t)n1 * rowb;
         R.c = c;
         R.nblk = FMT == 0 ? I / 128 : I / 256;
+        float td = 1.f;  // NVFP4 matrix scale
         if constexpr (FMT == 0) {
             R.fs0 = (const float *)se + (size_t)2 * (I / 128) * (H / 128) + (size_t)(nbase / 128) * (I / 128);
             R.fs1 = R.fs0;
-        } else {
+        } else if constexpr (FMT == 1) {
             const uint8_t *sd = se + (size_t)2 * I * (H / 32);
             R.es0 = sd + (size_t)n0 * (I / 32);
             R.es1 = sd + (size_t)n1 * (I / 32);
+        } else {
+            td = reinterpret_cast<const float *>(se)[2];
+            const uint8_t *sd = se + 16 + (size_t)2 * I * (H / 16);
+            R.es0 = sd + (size_t)n0 * (I / 16);
+            R.es1 = sd + (size_t)n1 * (I / 16);
         }
         for (int m0 = 0; m0 < M; m0 += mmax) {
             const int mc = min(mmax, M - m0);
@@ -451,8 +509,8 @@ __global__ __launch_bounds__(WAVES * 64) void w2_gemv_kernel(const uint8_t *__re
 #pragma unroll
                 for (int m = 0; m < kMaxM; ++m)
                     if (m < mc) {
-                        obuf[(size_t)(s0 + m0 + m) * H + n0] = a0[m];
-                        obuf[(size_t)(s0 + m0 + m) * H + n1] = a1[m];
+                        obuf[(size_t)(s0 + m0 + m) * H + n0] = td * a0[m];
+                        obuf[(size_t)(s0 + m0 + m) * H + n1] = td * a1[m];
                     }
             }
         }
@@ -520,8 +578,10 @@ hipError_t launch_w13(const Layer &L, const void *expert_w, const void *scales, 
 #define W13W(F, A) (waves == 2 ? (W13(F, A, 2)) : (W13(F, A, 4)))
     if (L.wfmt == 0)
         L.act_bf16 ? W13W(0, false) : W13W(0, true);
-    else
+    else if (L.wfmt == 1)
         L.act_bf16 ? W13W(1, false) : W13W(1, true);
+    else
+        W13W(2, false);  // NVFP4 layers have bf16 activations
 #undef W13W
 #undef W13
     return hipGetLastError();
@@ -542,8 +602,10 @@ hipError_t launch_w2(const Layer &L, const void *expert_w, const void *scales, i
 #define W2W(F, A) (waves == 2 ? (W2(F, A, 2)) : (W2(F, A, 4)))
     if (L.wfmt == 0)
         L.act_bf16 ? W2W(0, false) : W2W(0, true);
-    else
+    else if (L.wfmt == 1)
         L.act_bf16 ? W2W(1, false) : W2W(1, true);
+    else
+        W2W(2, false);
 #undef W2W
 #undef W2
     return hipGetLastError();

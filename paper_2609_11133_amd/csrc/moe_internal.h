@@ -22,6 +22,7 @@ struct Workspace {
     uint8_t *xe_hi, *xe_lo;  // [Tmax][H/32] E8M0 exponents of the split
     uint8_t *hs_hi, *hs_lo;  // [Tmax*kmax][I] 2-term FP8 split of h (MFMA path)
     uint8_t *he_hi, *he_lo;  // [Tmax*kmax][I/32]
+    __bf16 *hb;              // [Tmax*kmax][I] bf16 SwiGLU activations (NVFP4 MFMA path)
     size_t bytes;
 };
 
@@ -49,12 +50,15 @@ __host__ __device__ inline int max_mfma_chunks(int E, int Tmax, int kmax) { retu
 constexpr int kMfmaChunk = 32;      // tokens per MFMA pass (two 16-column tiles)
 constexpr int kCounterStride = 64;  // int32 words between routing counters (256 bytes)
 
-size_t carve_workspace(int H, int E, int I, int kmax, int Tmax, void *base, Workspace *ws);
+// The FP8 split regions are carved for FP8 and MXFP4 weights, hb for NVFP4 weights
+// (the other pointers are NULL).
+size_t carve_workspace(int H, int E, int I, int kmax, int Tmax, int wfmt, void *base, Workspace *ws);
 
 // Geometry of one layer as the kernels see it.
 struct Layer {
     int H, E, I;
-    int wfmt;       // 0 FP8-E4M3 (128x128 fp32 scales), 1 MXFP4 (E8M0 per 32)
+    int wfmt;       // 0 FP8-E4M3 (128x128 fp32 scales), 1 MXFP4 (E8M0 per 32),
+                    // 2 NVFP4 (E4M3 per 16 + fp32 per matrix)
     int act_bf16;   // activations bf16 (1) or fp32 (0)
     int router_bf16;
     size_t expert_w_bytes;  // per expert
@@ -88,6 +92,10 @@ hipError_t launch_w13_mfma(const Layer &L, const void *expert_w, const void *sca
                            const int32_t *meta, const int32_t *tok_of, const Workspace &ws, hipStream_t st);
 hipError_t launch_w2_mfma(const Layer &L, const void *expert_w, const void *scales, int T, int k,
                           const int32_t *meta, const Workspace &ws, hipStream_t st);
+hipError_t launch_w13_nvfp4(const Layer &L, const void *expert_w, const void *scales, const void *x, int T, int k,
+                            const int32_t *meta, const int32_t *tok_of, const Workspace &ws, hipStream_t st);
+hipError_t launch_w2_nvfp4(const Layer &L, const void *expert_w, const void *scales, int T, int k,
+                           const int32_t *meta, const Workspace &ws, hipStream_t st);
 hipError_t launch_combine(const Layer &L, int T, int k, const int32_t *slot_of, const float *wts, const float *o,
                           void *y, hipStream_t st);
 

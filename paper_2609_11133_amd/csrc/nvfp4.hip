@@ -1,0 +1,343 @@
+// NVFP4 path of the grouped expert FFN on the bf16 matrix cores.
+//
+// NVFP4 weights are E2M1 codes with one E4M3 scale per 16 inputs and one fp32 scale
+// per matrix.  The scaled f8f6f4 MFMA takes E8M0 (power-of-two) scales per 32 inputs
+// only, and the gfx950 conversions with an fp32 scale apply only its exponent (checked
+// on the device), so a 16-input E4M3 scale cannot ride along with the stored codes.
+// Each weight is therefore converted in registers: E2M1 -> fp32 (exact), times its
+// block scale (exact in fp32), packed to bf16 (exact: an E2M1 value times an E4M3
+// scale has at most 6 significant bits).  The activations are the layer's bf16 x
+// itself and, for the down projection, h rounded once to bf16; the 16x16x32 bf16 MFMA
+// accumulates in fp32 and the matrix scales multiply the accumulators.
+//
+// Operand layout of v_mfma_f32_16x16x32_bf16 (checked on the device): lane l holds
+// row/column l%16 and K [8g, 8g+8) with g = l/16; the result gives lane l rows
+// 4g..4g+3 of column l%16.  The K order inside one instruction is free as long as
+// both operands agree: instruction q (0..3) of a 128-input block takes, in lane group
+// g, the inputs [32g + 8q, 32g + 8q + 8), so a lane's 16-byte weight load (inputs
+// [32g, 32g+32)) feeds all four and inputs [32g, 32g+16) share block scale 2g.
+//
+// Work items follow the FP8 staged kernels (mfma.hip): one workgroup of W waves per
+// (chunk of <= 32 tokens of one expert, rows), one 16-row weight tile per wave through
+// a four-deep register ring, the chunk's activations staged once per workgroup in LDS
+// (double-buffered segments of 256 inputs, 16-byte pieces XOR-swizzled by token).
+#include <hip/hip_runtime.h>
+#include <math.h>
+
+#include "moe_internal.h"
+
+namespace moe {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+
+constexpr uint32_t kOutOfRange = 0x80000000u;
+constexpr int kRawBufferWord3 = 0x00020000;  // untyped 32-bit data format, no swizzle
+
+constexpr int kSegBlk = 2;                // 128-input blocks per staged segment
+constexpr int kRowBytes = kSegBlk * 256;  // bf16 bytes of one token row per segment
+constexpr int kTok = 32;                  // token rows of a chunk
+
+struct alignas(16) Seg {
+    uint8_t row[kTok][kRowBytes];
+};
+
+// Piece p (16 bytes) of token t's segment row is stored at piece swz(p, t): the piece
+// index within its 128-input block (16 pieces) is XORed with the token, so the 16
+// token columns of a fragment read fall on distinct banks.
+__device__ inline int swz(int p, int t) { return (p & ~15) | ((p ^ t) & 15); }
+
+__device__ inline void sync_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+__device__ inline __amdgpu_buffer_rsrc_t raw_rsrc(const void *base, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, kRawBufferWord3);
+}
+
+// One thread's share of staging a segment of a chunk's bf16 activation rows (K
+// inputs each) for a workgroup of W waves: piece tid%32 of token rows
+// 2W*q + tid/32 (q < Q).  Tokens past the chunk read out of range (zeros, no
+// memory request), so every thread issues the same loads and no branch guards them.
+template <int NT, int W>
+struct Stager {
+    static_assert(W == 4 || W == 8, "four or eight waves per workgroup");
+    static constexpr int Q = 16 * NT / (2 * W);
+    uint32_t voff[Q];
+    int tok[Q];
+    int piece;
+    u32x4v code[Q];
+
+    __device__ void init(const int32_t *__restrict__ row_of, int slot0, int mc, int K, int tid)
+    {
+        piece = tid & 31;
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            const int t = 2 * W * q + (tid >> 5);
+            tok[q] = t;
+            const uint32_t row = t < mc ? (uint32_t)(row_of ? row_of[slot0 + t] : slot0 + t) : 0u;
+            voff[q] = t < mc ? row * (uint32_t)K * 2u + 16u * piece : kOutOfRange;
+        }
+    }
+    // segment sg (callers clamp it to the last segment)
+    __device__ void load(__amdgpu_buffer_rsrc_t rs, int sg)
+    {
+#pragma unroll
+        for (int q = 0; q < Q; ++q)
+            code[q] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff[q] + (uint32_t)sg * kRowBytes, 0, 0);
+    }
+    __device__ void store(Seg &S) const
+    {
+#pragma unroll
+        for (int q = 0; q < Q; ++q)
+            *reinterpret_cast<u32x4v *>(&S.row[tok[q]][swz(piece, tok[q]) * 16]) = code[q];
+    }
+};
+
+// Four bf16x8 operands (instructions q = 0..3) from a lane's 16 weight bytes and the
+// two E4M3 block scales of its 32 inputs (byte 0: inputs [32g, 32g+16), byte 1: the
+// next 16).
+__device__ inline void dequant(const u32x4v &w, uint32_t scodes, bf16x8 (&a)[4])
+{
+    const f32x2 sc = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(scodes, 1.0f, false);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const float s = q < 2 ? sc.x : sc.y;
+        f32x2 v[4];
+        v[0] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[q], 1.0f, 0);
+        v[1] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[q], 1.0f, 1);
+        v[2] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[q], 1.0f, 2);
+        v[3] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[q], 1.0f, 3);
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const bf16x2 p = __builtin_convertvector(v[b] * s, bf16x2);
+            a[q][2 * b] = p.x;
+            a[q][2 * b + 1] = p.y;
+        }
+    }
+}
+
+// Streams this wave's 16-row weight tile (this lane's row `arow`, its E4M3 scale row
+// `srow`) over KB 128-input blocks against NT staged token tiles.  All W waves of the
+// workgroup call it together; it synchronises them once per staged segment.  On
+// return every wave is done reading seg[1], and seg[0] only in the odd tail.
+template <int NT, int W>
+__device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__ arow,
+                                   const uint8_t *__restrict__ srow, int KB, __amdgpu_buffer_rsrc_t rs,
+                                   Stager<NT, W> &st, Seg (&seg)[2], int lane)
+{
+    const int r = lane & 15, g = lane >> 4;
+    const int nseg = KB / kSegBlk;
+    u32x4v A[4];
+    uint32_t S[4];
+    auto loadA = [&](int slot, int kb) {
+        A[slot] = *reinterpret_cast<const u32x4v *>(arow + (size_t)kb * 64 + 16 * g);
+        S[slot] = *reinterpret_cast<const uint16_t *>(srow + (size_t)kb * 8 + 2 * g);
+    };
+    auto compute = [&](int slot, const Seg &sg, int kk) {
+        bf16x8 a[4];
+        dequant(A[slot], S[slot], a);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int j = 0; j < NT; ++j) {
+                const int t = 16 * j + r;
+                const bf16x8 b = *reinterpret_cast<const bf16x8 *>(&sg.row[t][swz(kk * 16 + 4 * g + q, t) * 16]);
+                acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[q], b, acc[j], 0, 0, 0);
+            }
+    };
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[j] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    loadA(0, 0);
+    loadA(1, min(1, KB - 1));
+    loadA(2, min(2, KB - 1));
+    st.load(rs, 0);
+    st.store(seg[0]);
+    st.load(rs, min(1, nseg - 1));
+    sync_lds();
+    int sg = 0, kb = 0;
+    for (; sg + 2 <= nseg; sg += 2, kb += 4) {  // two segments (four blocks) per iteration
+        loadA(3, min(kb + 3, KB - 1));  // past the end: reload the last block
+        compute(0, seg[0], 0);
+        loadA(0, min(kb + 4, KB - 1));
+        compute(1, seg[0], 1);
+        st.store(seg[1]);
+        st.load(rs, min(sg + 2, nseg - 1));
+        sync_lds();
+        loadA(1, min(kb + 5, KB - 1));
+        compute(2, seg[1], 0);
+        loadA(2, min(kb + 6, KB - 1));
+        compute(3, seg[1], 1);
+        st.store(seg[0]);
+        st.load(rs, min(sg + 3, nseg - 1));
+        sync_lds();
+    }
+    if (sg < nseg) {  // odd segment count: the last segment sits in seg[0], slots 0 and 1
+        compute(0, seg[0], 0);
+        compute(1, seg[0], 1);
+    }
+}
+
+// gate/up: item = (chunk, rows [i0, i0 + 8W)); wave w < W/2 streams gate rows
+// i0 + 16w, wave w >= W/2 the up rows of the same 16.  The up accumulators reach the
+// gate waves through LDS (seg[1], free once stream_tile returns; the next item first
+// writes it after its first barrier), and the gate waves form h = silu(g) * u, round
+// it to bf16 and store it.
+template <int NT, int W>
+__device__ inline void w13_item(const uint8_t *__restrict__ we, const uint8_t *__restrict__ se, int H, int I, int i0,
+                                int slot0, int mc, const int32_t *__restrict__ tok_of, __amdgpu_buffer_rsrc_t xr,
+                                __bf16 *__restrict__ hb, Seg (&seg)[2], int wave, int lane, int tid)
+{
+    constexpr int HW = W / 2;
+    const int r = lane & 15, g = lane >> 4;
+    const bool up = wave >= HW;
+    const int rr = i0 + 16 * (wave % HW) + r;  // this lane's intermediate row
+    const uint8_t *arow = we + (size_t)((up ? I : 0) + rr) * (H / 2);
+    const uint8_t *srow = se + 16 + (size_t)((up ? I : 0) + rr) * (H / 16);
+    Stager<NT, W> st;
+    st.init(tok_of, slot0, mc, H, tid);
+    f32x4 acc[NT];
+    stream_tile<NT, W>(acc, arow, srow, H / 128, xr, st, seg, lane);
+    f32x4 *red = reinterpret_cast<f32x4 *>(&seg[1].row[0][0]);
+    static_assert(sizeof(f32x4) * (W / 2) * 2 * 64 <= sizeof(Seg), "reduction buffer");
+    if (up) {
+#pragma unroll
+        for (int j = 0; j < NT; ++j) red[((wave - HW) * 2 + j) * 64 + lane] = acc[j];
+    }
+    sync_lds();
+    if (!up) {
+        const float tg = reinterpret_cast<const float *>(se)[0], tu = reinterpret_cast<const float *>(se)[1];
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+            const f32x4 u = red[(wave * 2 + j) * 64 + lane];
+            bf16x2 hv[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const float g0 = tg * acc[j][2 * i], g1 = tg * acc[j][2 * i + 1];
+                const f32x2 h = {g0 / (1.0f + expf(-g0)) * (tu * u[2 * i]), g1 / (1.0f + expf(-g1)) * (tu * u[2 * i + 1])};
+                hv[i] = __builtin_convertvector(h, bf16x2);
+            }
+            if (16 * j + r < mc) {
+                const size_t slot = (size_t)slot0 + 16 * j + r;
+                *reinterpret_cast<uint2 *>(hb + slot * I + i0 + 16 * wave + 4 * g) =
+                    make_uint2(__builtin_bit_cast(uint32_t, hv[0]), __builtin_bit_cast(uint32_t, hv[1]));
+            }
+        }
+    }
+}
+
+template <int W>
+__global__ __launch_bounds__(64 * W) void w13_nvfp4_kernel(const uint8_t *__restrict__ ew,
+                                                           const uint8_t *__restrict__ es,
+                                                           const int32_t *__restrict__ meta,
+                                                           const int32_t *__restrict__ tok_of,
+                                                           const __bf16 *__restrict__ x, __bf16 *__restrict__ hb,
+                                                           int T, int H, int I, int E, size_t ewb, size_t esb)
+{
+    __shared__ Seg seg[2];
+    const MetaIdx mi{E};
+    const int tiles = I / (8 * W);
+    const int n_items = meta[mi.n_mfma_chunks()] * tiles;
+    const int4 *recs = reinterpret_cast<const int4 *>(meta + mi.chunk_rec());
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const __amdgpu_buffer_rsrc_t xr = raw_rsrc(x, (uint32_t)T * (uint32_t)H * 2u);
+    for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
+        const int4 rec = recs[item / tiles];  // {expert, first slot, tokens, -}
+        const int i0 = (item % tiles) * 8 * W;
+        const uint8_t *we = ew + (size_t)rec.x * ewb;
+        const uint8_t *se = es + (size_t)rec.x * esb;
+        if (rec.z > 16)
+            w13_item<2, W>(we, se, H, I, i0, rec.y, rec.z, tok_of, xr, hb, seg, wave, lane, tid);
+        else
+            w13_item<1, W>(we, se, H, I, i0, rec.y, rec.z, tok_of, xr, hb, seg, wave, lane, tid);
+    }
+}
+
+// down: item = (chunk, rows [n0, n0 + 16W)); wave w streams rows n0 + 16w.
+template <int NT, int W>
+__device__ inline void w2_item(const uint8_t *__restrict__ we, const uint8_t *__restrict__ se, int H, int I, int n0,
+                               int slot0, int mc, __amdgpu_buffer_rsrc_t hr, float *__restrict__ obuf, Seg (&seg)[2],
+                               int wave, int lane, int tid)
+{
+    const int r = lane & 15, g = lane >> 4;
+    const int row0 = n0 + 16 * wave;
+    const uint8_t *arow = we + (size_t)I * H + (size_t)(row0 + r) * (I / 2);
+    const uint8_t *srow = se + 16 + (size_t)2 * I * (H / 16) + (size_t)(row0 + r) * (I / 16);
+    Stager<NT, W> st;
+    st.init(nullptr, slot0, mc, I, tid);
+    f32x4 acc[NT];
+    stream_tile<NT, W>(acc, arow, srow, I / 128, hr, st, seg, lane);
+    const float td = reinterpret_cast<const float *>(se)[2];
+#pragma unroll
+    for (int j = 0; j < NT; ++j)
+        if (16 * j + r < mc)
+            *reinterpret_cast<f32x4 *>(obuf + ((size_t)slot0 + 16 * j + r) * H + row0 + 4 * g) = td * acc[j];
+    sync_lds();  // the next item's staging overwrites seg[0], which the odd tail reads
+}
+
+template <int W>
+__global__ __launch_bounds__(64 * W) void w2_nvfp4_kernel(const uint8_t *__restrict__ ew,
+                                                          const uint8_t *__restrict__ es,
+                                                          const int32_t *__restrict__ meta,
+                                                          const __bf16 *__restrict__ hb, float *__restrict__ obuf,
+                                                          int P, int H, int I, int E, size_t ewb, size_t esb)
+{
+    __shared__ Seg seg[2];
+    const MetaIdx mi{E};
+    const int tiles = H / (16 * W);
+    const int n_items = meta[mi.n_mfma_chunks()] * tiles;
+    const int4 *recs = reinterpret_cast<const int4 *>(meta + mi.chunk_rec());
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const __amdgpu_buffer_rsrc_t hr = raw_rsrc(hb, (uint32_t)P * (uint32_t)I * 2u);
+    for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
+        const int4 rec = recs[item / tiles];
+        const int n0 = (item % tiles) * 16 * W;
+        const uint8_t *we = ew + (size_t)rec.x * ewb;
+        const uint8_t *se = es + (size_t)rec.x * esb;
+        if (rec.z > 16)
+            w2_item<2, W>(we, se, H, I, n0, rec.y, rec.z, hr, obuf, seg, wave, lane, tid);
+        else
+            w2_item<1, W>(we, se, H, I, n0, rec.y, rec.z, hr, obuf, seg, wave, lane, tid);
+    }
+}
+
+constexpr int kWaves = 4;
+
+// Workgroups for `items_per_chunk` items per chunk record (see mfma_grid in mfma.hip).
+int nvfp4_grid(const Layer &L, int T, int k, int items_per_chunk)
+{
+    const long pairs = (long)T * k;
+    const long recs = pairs < L.E ? pairs : L.E;
+    const long chunks = recs + (pairs + kMfmaChunk - 1) / kMfmaChunk;
+    const long blocks = chunks * items_per_chunk;
+    return blocks < 1 ? 1 : (blocks > 65535 ? 65535 : (int)blocks);
+}
+
+}  // namespace
+
+hipError_t launch_w13_nvfp4(const Layer &L, const void *expert_w, const void *scales, const void *x, int T, int k,
+                            const int32_t *meta, const int32_t *tok_of, const Workspace &ws, hipStream_t st)
+{
+    dim3 grid(nvfp4_grid(L, T, k, L.I / (8 * kWaves))), block(64 * kWaves);
+    w13_nvfp4_kernel<kWaves><<<grid, block, 0, st>>>((const uint8_t *)expert_w, (const uint8_t *)scales, meta, tok_of,
+                                                     (const __bf16 *)x, (__bf16 *)ws.hb, T, L.H, L.I, L.E,
+                                                     L.expert_w_bytes, L.expert_s_bytes);
+    return hipGetLastError();
+}
+
+hipError_t launch_w2_nvfp4(const Layer &L, const void *expert_w, const void *scales, int T, int k,
+                           const int32_t *meta, const Workspace &ws, hipStream_t st)
+{
+    dim3 grid(nvfp4_grid(L, T, k, L.H / (16 * kWaves))), block(64 * kWaves);
+    w2_nvfp4_kernel<kWaves><<<grid, block, 0, st>>>((const uint8_t *)expert_w, (const uint8_t *)scales, meta,
+                                                    (const __bf16 *)ws.hb, ws.o, T * k, L.H, L.I, L.E,
+                                                    L.expert_w_bytes, L.expert_s_bytes);
+    return hipGetLastError();
+}
+
+}  // namespace moe

@@ -56,6 +56,10 @@ def test_workspace_bytes_and_sizes(B):
     c4 = cfg(B, wfmt=B.MOE_WFMT_MXFP4_E2M1_B32)
     assert B.moe_decode_expert_weight_bytes(c4) == 3 * 512 * 256 // 2
     assert B.moe_decode_expert_scale_bytes(c4) == 3 * 512 * 256 // 32
+    c5 = cfg(B, wfmt=B.MOE_WFMT_NVFP4_E2M1_B16)
+    assert B.moe_decode_expert_weight_bytes(c5) == 3 * 512 * 256 // 2
+    assert B.moe_decode_expert_scale_bytes(c5) == 16 + 3 * 512 * 256 // 16
+    assert B.moe_decode_workspace_bytes(c5) > 0
 
 
 @pytest.mark.parametrize(
@@ -73,6 +77,8 @@ def test_workspace_bytes_and_sizes(B):
         (dict(max_tokens=4096), -1),
         (dict(act_dtype=7), -1),
         (dict(wfmt=3), -1),
+        (dict(hidden=128, wfmt=2), -1),  # NVFP4 needs multiples of 256
+        (dict(wfmt=2, act_dtype=0), -2),  # NVFP4 needs bf16 activations
     ],
 )
 def test_invalid_configs_rejected(B, kw, code):

@@ -111,6 +111,7 @@ def check_routing(run, x, topk=None, label=""):
 SMALL_FP8 = LayerConfig("small-fp8", 512, 16, 4, 256, "bf16", "bf16", "fp8", "normal:0.5", [])
 SMALL_MX = LayerConfig("small-mxfp4", 512, 16, 4, 512, "bf16", "bf16", "mxfp4", "zipf:1.1", [])
 SMALL_F32_MX = LayerConfig("small-f32-mxfp4", 256, 8, 2, 256, "f32", "f32", "mxfp4", None, [])
+SMALL_NV = LayerConfig("small-nvfp4", 512, 16, 4, 256, "bf16", "bf16", "nvfp4", "normal:0.5", [])
 
 
 @pytest.mark.parametrize("T", [1, 5, 13, 32])
@@ -125,6 +126,28 @@ def test_small_mxfp4_layer(dev, T):
     hl = W.host_layer(SMALL_MX, seed=502)
     run = Run(SMALL_MX, hl, dev, max_tokens=16)
     check_layer(run, W.host_x(SMALL_MX, T, seed=502), label=f"small-mxfp4 T={T}")
+
+
+@pytest.mark.parametrize("T", [1, 5, 13, 32])
+def test_small_nvfp4_layer(dev, T):
+    hl = W.host_layer(SMALL_NV, seed=541)
+    run = Run(SMALL_NV, hl, dev, max_tokens=32)
+    check_layer(run, W.host_x(SMALL_NV, T, seed=541), label=f"small-nvfp4 T={T}")
+
+
+# NVFP4 staged segments hold two 128-input blocks: K = 768 (I) gives an odd segment
+# count (pair loop plus tail), K = 1024 (H) an even one; Zipf skew puts more than 16
+# tokens on some expert (32-token tiles).
+NV_SEG = LayerConfig("nvfp4-seg", 1024, 16, 4, 768, "bf16", "bf16", "nvfp4", "zipf:1.1", [])
+
+
+@pytest.mark.parametrize("T", [1, 7, 32])
+def test_nvfp4_segments(dev, T):
+    hl = W.host_layer(NV_SEG, seed=542)
+    run = Run(NV_SEG, hl, dev, max_tokens=32)
+    check_layer(run, W.host_x(NV_SEG, T, seed=542 + T), label=f"nvfp4-seg T={T}")
+    if T == 32:
+        assert max(run.m.stats()[1]) > 16
 
 
 def test_tiny_config(dev):
@@ -296,6 +319,27 @@ def test_random_small_layers(dev, i):
     check_layer(run, W.host_x(cfg, T, seed=700 + i), label=f"random {i}")
 
 
+def _random_nvfp4_layer(i):
+    rng = np.random.default_rng(9500 + i)
+    H = 256 * int(rng.integers(1, 9))
+    I = 256 * int(rng.integers(1, 9))
+    E = int(rng.choice([2, 5, 16, 40, 96, 160]))
+    k = int(min(E, rng.choice([1, 2, 4, 8, 16])))
+    router = ["bf16", "f32"][int(rng.integers(0, 4)) == 0]
+    bias = [None, "normal:0.5", "zipf:1.1"][int(rng.integers(0, 3))]
+    T = int(rng.integers(1, 70))
+    return LayerConfig(f"rand-nv{i}", H, E, k, I, "bf16", router, "nvfp4", bias, []), T
+
+
+@pytest.mark.parametrize("i", range(6))
+def test_random_nvfp4_layers(dev, i):
+    cfg, T = _random_nvfp4_layer(i)
+    hl = W.host_layer(cfg, seed=750 + i)
+    run = Run(cfg, hl, dev, max_tokens=T, mfma_min_tokens=[0, -1, 2][i % 3])
+    say(f"[random] {cfg}")
+    check_layer(run, W.host_x(cfg, T, seed=750 + i), label=f"random nvfp4 {i}")
+
+
 # ---------------------------------------------------------------- full-size layers
 
 @pytest.fixture(scope="module")
@@ -377,7 +421,7 @@ def test_full_235b_mxfp4_zipf(dev):
 # ---------------------------------------------------------------- both expert paths
 
 @pytest.mark.parametrize("mstar", [-1, 1, 2])
-@pytest.mark.parametrize("cfg,T", [(SMALL_FP8, 13), (SMALL_MX, 13), (SMALL_FP8, 32), (C.TINY, 4)])
+@pytest.mark.parametrize("cfg,T", [(SMALL_FP8, 13), (SMALL_MX, 13), (SMALL_FP8, 32), (C.TINY, 4), (SMALL_NV, 13)])
 def test_expert_paths(dev, cfg, T, mstar):
     """mfma_min_tokens = -1 forces the GEMV path for every expert, 1 the MFMA path,
     2 mixes them within one step."""
@@ -405,3 +449,26 @@ def test_full_mxfp4_paths(dev, mstar):
     hl = W.host_layer(cfg)
     run = Run(cfg, hl, dev, max_tokens=256, mfma_min_tokens=mstar)
     _full(run, cfg, 256, batch=1)
+
+
+@pytest.fixture(scope="module")
+def full_235b_nv(dev):
+    say("[gen] qwen3-235b-a22b nvfp4 layer")
+    return W.host_layer(C.QWEN3_235B_NVFP4)
+
+
+@pytest.mark.parametrize("T", C.QWEN3_235B_NVFP4.tokens)
+def test_full_235b_nvfp4(dev, full_235b_nv, T):
+    run = Run(C.QWEN3_235B_NVFP4, full_235b_nv, dev, max_tokens=max(C.QWEN3_235B_NVFP4.tokens))
+    _full(run, C.QWEN3_235B_NVFP4, T, batch=T)
+
+
+@pytest.mark.parametrize("mstar", [-1, 1])
+def test_full_nvfp4_zipf_paths(dev, mstar):
+    cfg = C.QWEN3_235B_NVFP4_ZIPF
+    say("[gen] qwen3-235b-a22b nvfp4 zipf layer")
+    hl = W.host_layer(cfg)
+    run = Run(cfg, hl, dev, max_tokens=256, mfma_min_tokens=mstar)
+    _full(run, cfg, 256, batch=2)
+    st, counts = run.m.stats()
+    say(f"[zipf] nvfp4 active={st.n_active} max tokens/expert={max(counts)}")
