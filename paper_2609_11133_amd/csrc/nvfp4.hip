@@ -13,14 +13,15 @@
 // Operand layout of v_mfma_f32_16x16x32_bf16 (checked on the device): lane l holds
 // row/column l%16 and K [8g, 8g+8) with g = l/16; the result gives lane l rows
 // 4g..4g+3 of column l%16.  The K order inside one instruction is free as long as
-// both operands agree: instruction q (0..3) of a 128-input block takes, in lane group
-// g, the inputs [32g + 8q, 32g + 8q + 8), so a lane's 16-byte weight load (inputs
-// [32g, 32g+32)) feeds all four and inputs [32g, 32g+16) share block scale 2g.
+// both operands agree.  A K block is 256 inputs (128 weight bytes per row, the access
+// shape of the FP8 kernels); instruction q (0..7) of a block takes, in lane group g,
+// the inputs [64g + 8q, 64g + 8q + 8), so a lane's 32 contiguous weight bytes (inputs
+// [64g, 64g+64)) feed all eight and one 32-bit load brings their four block scales.
 //
 // Work items follow the FP8 staged kernels (mfma.hip): one workgroup of W waves per
 // (chunk of <= 32 tokens of one expert, rows), one 16-row weight tile per wave through
 // a four-deep register ring, the chunk's activations staged once per workgroup in LDS
-// (double-buffered segments of 256 inputs, 16-byte pieces XOR-swizzled by token).
+// (double-buffered segments of 512 inputs, 16-byte pieces XOR-swizzled by token).
 #include <hip/hip_runtime.h>
 #include <math.h>
 
@@ -38,17 +39,18 @@ typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
 constexpr uint32_t kOutOfRange = 0x80000000u;
 constexpr int kRawBufferWord3 = 0x00020000;  // untyped 32-bit data format, no swizzle
 
-constexpr int kSegBlk = 2;                // 128-input blocks per staged segment
-constexpr int kRowBytes = kSegBlk * 256;  // bf16 bytes of one token row per segment
+constexpr int kBlk = 256;                 // inputs per K block
+constexpr int kSegBlk = 2;                // K blocks per staged segment
+constexpr int kRowBytes = kSegBlk * kBlk * 2;  // bf16 bytes of one token row per segment
 constexpr int kTok = 32;                  // token rows of a chunk
 
 struct alignas(16) Seg {
     uint8_t row[kTok][kRowBytes];
 };
 
-// Piece p (16 bytes) of token t's segment row is stored at piece swz(p, t): the piece
-// index within its 128-input block (16 pieces) is XORed with the token, so the 16
-// token columns of a fragment read fall on distinct banks.
+// Piece p (16 bytes) of token t's segment row is stored at piece swz(p, t): the low
+// four bits of the piece index (128 inputs) are XORed with the token, so the 16 token
+// columns of a fragment read fall on distinct banks.
 __device__ inline int swz(int p, int t) { return (p & ~15) | ((p ^ t) & 15); }
 
 __device__ inline void sync_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
@@ -59,13 +61,15 @@ __device__ inline __amdgpu_buffer_rsrc_t raw_rsrc(const void *base, uint32_t byt
 }
 
 // One thread's share of staging a segment of a chunk's bf16 activation rows (K
-// inputs each) for a workgroup of W waves: piece tid%32 of token rows
-// 2W*q + tid/32 (q < Q).  Tokens past the chunk read out of range (zeros, no
-// memory request), so every thread issues the same loads and no branch guards them.
+// inputs each) for a workgroup of W waves: piece tid%64 of token rows W*q + tid/64
+// (q < Q).  Tokens past the chunk read out of range (zeros, no memory request), so
+// every thread issues the same loads and no branch guards them.  A segment that runs
+// past K (an odd block count) stages bytes no block reads.
 template <int NT, int W>
 struct Stager {
     static_assert(W == 4 || W == 8, "four or eight waves per workgroup");
-    static constexpr int Q = 16 * NT / (2 * W);
+    static constexpr int kPieces = kRowBytes / 16;  // per token row and segment
+    static constexpr int Q = 16 * NT * kPieces / (64 * W);
     uint32_t voff[Q];
     int tok[Q];
     int piece;
@@ -73,10 +77,10 @@ struct Stager {
 
     __device__ void init(const int32_t *__restrict__ row_of, int slot0, int mc, int K, int tid)
     {
-        piece = tid & 31;
+        piece = tid & (kPieces - 1);
 #pragma unroll
         for (int q = 0; q < Q; ++q) {
-            const int t = 2 * W * q + (tid >> 5);
+            const int t = (64 * W / kPieces) * q + tid / kPieces;
             tok[q] = t;
             const uint32_t row = t < mc ? (uint32_t)(row_of ? row_of[slot0 + t] : slot0 + t) : 0u;
             voff[q] = t < mc ? row * (uint32_t)K * 2u + 16u * piece : kOutOfRange;
@@ -97,15 +101,14 @@ struct Stager {
     }
 };
 
-// Four bf16x8 operands (instructions q = 0..3) from a lane's 16 weight bytes and the
-// two E4M3 block scales of its 32 inputs (byte 0: inputs [32g, 32g+16), byte 1: the
-// next 16).
-__device__ inline void dequant(const u32x4v &w, uint32_t scodes, bf16x8 (&a)[4])
+// Four bf16x8 operands (instructions q = 4h..4h+3 of a block) from 16 of a lane's
+// weight bytes (w: inputs [64g + 32h, 64g + 32h + 32)) and their two E4M3 block
+// scales (s0: the first 16 inputs, s1: the next 16).
+__device__ inline void dequant(const u32x4v &w, float s0, float s1, bf16x8 (&a)[4])
 {
-    const f32x2 sc = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(scodes, 1.0f, false);
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-        const float s = q < 2 ? sc.x : sc.y;
+        const float s = q < 2 ? s0 : s1;
         f32x2 v[4];
         v[0] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[q], 1.0f, 0);
         v[1] = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w[q], 1.0f, 1);
@@ -121,36 +124,53 @@ __device__ inline void dequant(const u32x4v &w, uint32_t scodes, bf16x8 (&a)[4])
 }
 
 // Streams this wave's 16-row weight tile (this lane's row `arow`, its E4M3 scale row
-// `srow`) over KB 128-input blocks against NT staged token tiles.  All W waves of the
+// `srow`) over KB 256-input blocks against NT staged token tiles.  All W waves of the
 // workgroup call it together; it synchronises them once per staged segment.  On
-// return every wave is done reading seg[1], and seg[0] only in the odd tail.
+// return every wave has passed a barrier after its last read of either buffer.
 template <int NT, int W>
 __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__ arow,
                                    const uint8_t *__restrict__ srow, int KB, __amdgpu_buffer_rsrc_t rs,
                                    Stager<NT, W> &st, Seg (&seg)[2], int lane)
 {
     const int r = lane & 15, g = lane >> 4;
-    const int nseg = KB / kSegBlk;
-    u32x4v A[4];
+    const int nseg = (KB + kSegBlk - 1) / kSegBlk;
+    u32x4v A[4][2];
     uint32_t S[4];
     auto loadA = [&](int slot, int kb) {
-        A[slot] = *reinterpret_cast<const u32x4v *>(arow + (size_t)kb * 64 + 16 * g);
-        S[slot] = *reinterpret_cast<const uint16_t *>(srow + (size_t)kb * 8 + 2 * g);
+        const uint8_t *p = arow + (size_t)kb * (kBlk / 2) + 32 * g;
+        A[slot][0] = *reinterpret_cast<const u32x4v *>(p);
+        A[slot][1] = *reinterpret_cast<const u32x4v *>(p + 16);
+        S[slot] = *reinterpret_cast<const uint32_t *>(srow + (size_t)kb * (kBlk / 16) + 4 * g);
     };
+    // Each half block's activation fragments are read from LDS before its weights are
+    // dequantised, so the LDS latency hides behind that VALU work; instructions q
+    // accumulate into acc2[q % 2], so consecutive MFMAs do not wait on each other.
+    f32x4 acc2[2][NT];
     auto compute = [&](int slot, const Seg &sg, int kk) {
-        bf16x8 a[4];
-        dequant(A[slot], S[slot], a);
+        const f32x2 s01 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(S[slot], 1.0f, false);
+        const f32x2 s23 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(S[slot], 1.0f, true);
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
+        for (int h = 0; h < 2; ++h) {
+            bf16x8 b[4][NT];
 #pragma unroll
-            for (int j = 0; j < NT; ++j) {
-                const int t = 16 * j + r;
-                const bf16x8 b = *reinterpret_cast<const bf16x8 *>(&sg.row[t][swz(kk * 16 + 4 * g + q, t) * 16]);
-                acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[q], b, acc[j], 0, 0, 0);
-            }
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int j = 0; j < NT; ++j) {
+                    const int t = 16 * j + r;
+                    b[q][j] = *reinterpret_cast<const bf16x8 *>(&sg.row[t][swz(kk * 32 + 8 * g + 4 * h + q, t) * 16]);
+                }
+            __builtin_amdgcn_sched_barrier(0);
+            bf16x8 a[4];
+            dequant(A[slot][h], h ? s23.x : s01.x, h ? s23.y : s01.y, a);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int j = 0; j < NT; ++j)
+                    acc2[q & 1][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[q], b[q][j], acc2[q & 1][j], 0, 0, 0);
+        }
     };
 #pragma unroll
-    for (int j = 0; j < NT; ++j) acc[j] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < NT; ++j) acc2[0][j] = acc2[1][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
     loadA(0, 0);
     loadA(1, min(1, KB - 1));
     loadA(2, min(2, KB - 1));
@@ -159,7 +179,7 @@ __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__
     st.load(rs, min(1, nseg - 1));
     sync_lds();
     int sg = 0, kb = 0;
-    for (; sg + 2 <= nseg; sg += 2, kb += 4) {  // two segments (four blocks) per iteration
+    for (; kb + 4 <= KB; sg += 2, kb += 4) {  // two segments (four blocks) per iteration
         loadA(3, min(kb + 3, KB - 1));  // past the end: reload the last block
         compute(0, seg[0], 0);
         loadA(0, min(kb + 4, KB - 1));
@@ -175,10 +195,18 @@ __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__
         st.load(rs, min(sg + 3, nseg - 1));
         sync_lds();
     }
-    if (sg < nseg) {  // odd segment count: the last segment sits in seg[0], slots 0 and 1
-        compute(0, seg[0], 0);
-        compute(1, seg[0], 1);
+    // Fewer than four blocks remain, in ring slots 0..2: segment sg sits in seg[0] and
+    // segment sg + 1 in the stager's registers.
+    if (kb < KB) compute(0, seg[0], 0);
+    if (kb + 1 < KB) compute(1, seg[0], 1);
+    if (kb + 2 < KB) {
+        st.store(seg[1]);
+        sync_lds();
+        compute(2, seg[1], 0);
     }
+    if (kb < KB) sync_lds();
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[j] = acc2[0][j] + acc2[1][j];
 }
 
 // gate/up: item = (chunk, rows [i0, i0 + 8W)); wave w < W/2 streams gate rows
@@ -200,7 +228,7 @@ __device__ inline void w13_item(const uint8_t *__restrict__ we, const uint8_t *_
     Stager<NT, W> st;
     st.init(tok_of, slot0, mc, H, tid);
     f32x4 acc[NT];
-    stream_tile<NT, W>(acc, arow, srow, H / 128, xr, st, seg, lane);
+    stream_tile<NT, W>(acc, arow, srow, H / kBlk, xr, st, seg, lane);
     f32x4 *red = reinterpret_cast<f32x4 *>(&seg[1].row[0][0]);
     static_assert(sizeof(f32x4) * (W / 2) * 2 * 64 <= sizeof(Seg), "reduction buffer");
     if (up) {
@@ -230,7 +258,7 @@ __device__ inline void w13_item(const uint8_t *__restrict__ we, const uint8_t *_
 }
 
 template <int W>
-__global__ __launch_bounds__(64 * W) void w13_nvfp4_kernel(const uint8_t *__restrict__ ew,
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) void w13_nvfp4_kernel(const uint8_t *__restrict__ ew,
                                                            const uint8_t *__restrict__ es,
                                                            const int32_t *__restrict__ meta,
                                                            const int32_t *__restrict__ tok_of,
@@ -270,17 +298,16 @@ __device__ inline void w2_item(const uint8_t *__restrict__ we, const uint8_t *__
     Stager<NT, W> st;
     st.init(nullptr, slot0, mc, I, tid);
     f32x4 acc[NT];
-    stream_tile<NT, W>(acc, arow, srow, I / 128, hr, st, seg, lane);
+    stream_tile<NT, W>(acc, arow, srow, I / kBlk, hr, st, seg, lane);
     const float td = reinterpret_cast<const float *>(se)[2];
 #pragma unroll
     for (int j = 0; j < NT; ++j)
         if (16 * j + r < mc)
             *reinterpret_cast<f32x4 *>(obuf + ((size_t)slot0 + 16 * j + r) * H + row0 + 4 * g) = td * acc[j];
-    sync_lds();  // the next item's staging overwrites seg[0], which the odd tail reads
 }
 
 template <int W>
-__global__ __launch_bounds__(64 * W) void w2_nvfp4_kernel(const uint8_t *__restrict__ ew,
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) void w2_nvfp4_kernel(const uint8_t *__restrict__ ew,
                                                           const uint8_t *__restrict__ es,
                                                           const int32_t *__restrict__ meta,
                                                           const __bf16 *__restrict__ hb, float *__restrict__ obuf,

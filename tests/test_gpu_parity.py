@@ -135,17 +135,21 @@ def test_small_nvfp4_layer(dev, T):
     check_layer(run, W.host_x(SMALL_NV, T, seed=541), label=f"small-nvfp4 T={T}")
 
 
-# NVFP4 staged segments hold two 128-input blocks: K = 768 (I) gives an odd segment
-# count (pair loop plus tail), K = 1024 (H) an even one; Zipf skew puts more than 16
-# tokens on some expert (32-token tiles).
-NV_SEG = LayerConfig("nvfp4-seg", 1024, 16, 4, 768, "bf16", "bf16", "nvfp4", "zipf:1.1", [])
+# NVFP4 staged segments hold two 256-input blocks and the K loop takes four blocks
+# per pass, then a tail of 0-3 blocks.  These (H, I) pairs give the gate/up and down
+# projections every block count from 1 to 7; Zipf skew puts more than 16 tokens on
+# some expert at T=32 (32-token tiles).
+NV_SEG_SHAPES = [(1024, 768), (1280, 512), (1536, 1792), (256, 256)]
 
 
+@pytest.mark.parametrize("shape", NV_SEG_SHAPES)
 @pytest.mark.parametrize("T", [1, 7, 32])
-def test_nvfp4_segments(dev, T):
-    hl = W.host_layer(NV_SEG, seed=542)
-    run = Run(NV_SEG, hl, dev, max_tokens=32)
-    check_layer(run, W.host_x(NV_SEG, T, seed=542 + T), label=f"nvfp4-seg T={T}")
+def test_nvfp4_segments(dev, shape, T):
+    H, I = shape
+    cfg = LayerConfig(f"nvfp4-seg-{H}x{I}", H, 16, 4, I, "bf16", "bf16", "nvfp4", "zipf:1.1", [])
+    hl = W.host_layer(cfg, seed=542)
+    run = Run(cfg, hl, dev, max_tokens=32)
+    check_layer(run, W.host_x(cfg, T, seed=542 + T), label=f"nvfp4-seg {H}x{I} T={T}")
     if T == 32:
         assert max(run.m.stats()[1]) > 16
 
