@@ -308,29 +308,53 @@ def main():
               f"{results[T]['layer_GBs']:.0f} GB/s, experts {exp_gbs:.0f} GB/s, stages(us) "
               + " ".join(f"{n}={v * 1e3:.1f}" for n, v in zip(B.STAGE_NAMES, st_ms)), file=sys.stderr, flush=True)
 
-    # board power over a steady ~4 s loop at the headline batch size
+    # board power over a steady loop at each batch size (4 s at the headline one), and
+    # over 2 s of an idle device (after 3 s of rest) for context
     power = None
     if not args.no_power:
         ps = PowerSampler()
         if ps.ok:
-            ys = [W.empty_y(cfg, T_main, dev) for _ in range(2)]
-            stop = threading.Event()
-            th = threading.Thread(target=ps.run, args=(stop,), daemon=True)
-            th.start()
-            n, tp0 = 0, time.perf_counter()
-            while time.perf_counter() - tp0 < 4.0:
-                for _ in range(50):
-                    c = n % copies
-                    m.forward(xs[T_main][n % pool], T_main, rw, bias, ews[c], scs[c], cfg.topk, ys[n & 1])
-                    n += 1
-                torch.cuda.synchronize(dev)
-            dt = time.perf_counter() - tp0
-            stop.set()
-            th.join()
-            watts = [w for _, w in ps.samples]
-            if watts:
-                pw = statistics.mean(watts)
-                power = dict(board_W=pw, samples=len(watts), tokens_per_J=(n * T_main / dt) / pw)
+
+            def sample(seconds, work):
+                ps.samples = []
+                stop = threading.Event()
+                th = threading.Thread(target=ps.run, args=(stop,), daemon=True)
+                th.start()
+                n, tp0 = 0, time.perf_counter()
+                while time.perf_counter() - tp0 < seconds:
+                    n += work()
+                dt = time.perf_counter() - tp0
+                stop.set()
+                th.join()
+                watts = [w for _, w in ps.samples]
+                return (statistics.mean(watts) if watts else None), len(watts), n, dt
+
+            def loop_at(T):
+                ys = [W.empty_y(cfg, T, dev) for _ in range(2)]
+                ctr = [0]
+
+                def work():
+                    for _ in range(50):
+                        n = ctr[0]
+                        c = n % copies
+                        m.forward(xs[T][n % pool], T, rw, bias, ews[c], scs[c], cfg.topk, ys[n & 1])
+                        ctr[0] += 1
+                    torch.cuda.synchronize(dev)
+                    return 50
+
+                return work
+
+            torch.cuda.synchronize(dev)
+            time.sleep(3.0)  # the board sensor averages over about a second
+            idle_W, idle_n, _, _ = sample(2.0, lambda: (time.sleep(0.05), 0)[1])
+            for T in sweep_T:
+                pw, ns, n, dt = sample(4.0 if T == T_main else 3.0, loop_at(T))
+                if pw:
+                    results[T]["power"] = dict(board_W=pw, samples=ns, tokens_per_J=(n * T / dt) / pw)
+                    print(f"[power] T={T}: {pw:.0f} W board (idle {idle_W or 0:.0f} W), "
+                          f"{results[T]['power']['tokens_per_J']:.1f} tokens/J", file=sys.stderr, flush=True)
+            if results[T_main].get("power"):
+                power = dict(results[T_main]["power"], idle_board_W=idle_W)
         if power is None:
             power = dict(board_W=None, note="amdsmi power unreadable: " + getattr(ps, "err", "no samples"))
 

@@ -162,8 +162,7 @@ __device__ inline double elem(const Chunk8<T> &c, int i)
         return (double)__uint_as_float(c.d[i]);
 }
 
-constexpr int kEPW = 4;        // experts per wave, at most
-constexpr int kSegChunks = 4;  // 8-input chunks per lane held at once (2048 inputs)
+constexpr int kEPW = 4;  // experts per wave, at most
 
 // One fp64 value moved by a DPP lane permutation (ctrl: an immediate DPP control).
 template <int CTRL>
@@ -212,7 +211,10 @@ __device__ inline float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0
 // and inflated by its own worst-case rounding; products below the fp32 subnormal grain
 // add at most H*2^-149 in absolute error, which the margin covers.  fp32 inputs use
 // fp64 fused multiply-adds throughout.
-template <typename XT, typename WT>
+//
+// EPW is the wave's expert capacity (ne <= EPW) and SEG the 8-input chunks per lane
+// held at once: one expert per wave loads a 4096-input row in one round trip.
+template <typename XT, typename WT, int EPW, int SEG>
 __device__ inline int wave_logits(const XT *__restrict__ xr, const WT *__restrict__ wr, const float *bias, int H,
                                   int e0, int ne, int lane, float *lrow)
 {
@@ -223,19 +225,19 @@ __device__ inline int wave_logits(const XT *__restrict__ xr, const WT *__restric
     const int per_acc = ((nck + 1) / 2) * 8;
     const double gamma = (double)(per_acc + 1 + 6 + 1 + 2) * 0x1p-52;  // >= 2 gamma_D
     const double infl = 1.0 + (double)(per_acc + 2) * 0x1p-23;         // fp32 magnitude sums
-    double s[kEPW][2], a[kEPW][2];
-    float a32[kEPW][2];
+    double s[EPW][2], a[EPW][2];
+    float a32[EPW][2];
 #pragma unroll
-    for (int i = 0; i < kEPW; ++i) {
+    for (int i = 0; i < EPW; ++i) {
         s[i][0] = s[i][1] = a[i][0] = a[i][1] = 0.0;
         a32[i][0] = a32[i][1] = 0.f;
     }
-    for (int seg = 0; seg < nck; seg += kSegChunks) {
-        Chunk8<XT> xc[kSegChunks];
-        bool valid[kSegChunks];
-        int off[kSegChunks];
+    for (int seg = 0; seg < nck; seg += SEG) {
+        Chunk8<XT> xc[SEG];
+        bool valid[SEG];
+        int off[SEG];
 #pragma unroll
-        for (int j = 0; j < kSegChunks; ++j) {
+        for (int j = 0; j < SEG; ++j) {
             const int h = lane * 8 + 512 * (seg + j);
             valid[j] = h < H;
             off[j] = valid[j] ? h : H - 8;  // clamped: an invalid chunk is loaded but its x is 0
@@ -244,27 +246,27 @@ __device__ inline int wave_logits(const XT *__restrict__ xr, const WT *__restric
 #pragma unroll
                 for (int q = 0; q < (int)(sizeof(xc[j].d) / 4); ++q) xc[j].d[q] = 0u;
         }
-        float xf[kSegChunks][8];
+        float xf[SEG][8];
         if constexpr (kBf16)
 #pragma unroll
-            for (int j = 0; j < kSegChunks; ++j)
+            for (int j = 0; j < SEG; ++j)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     xf[j][2 * q] = bf16_lo(xc[j].d[q]);
                     xf[j][2 * q + 1] = bf16_hi(xc[j].d[q]);
                 }
         // every expert's slice of this segment in flight at once (one memory latency)
-        Chunk8<WT> wc[kEPW][kSegChunks];
+        Chunk8<WT> wc[EPW][SEG];
 #pragma unroll
-        for (int i = 0; i < kEPW; ++i)
+        for (int i = 0; i < EPW; ++i)
 #pragma unroll
-            for (int j = 0; j < kSegChunks; ++j)
+            for (int j = 0; j < SEG; ++j)
                 ld_chunk<WT>(wr + (size_t)(e0 + (i < ne ? i : 0)) * H + off[j], wc[i][j]);
 #pragma unroll
-        for (int i = 0; i < kEPW; ++i) {
+        for (int i = 0; i < EPW; ++i) {
             if (i < ne) {
 #pragma unroll
-                for (int j = 0; j < kSegChunks; ++j)
+                for (int j = 0; j < SEG; ++j)
 #pragma unroll
                     for (int q = 0; q < 8; ++q) {
                         if constexpr (kBf16) {
@@ -284,7 +286,7 @@ __device__ inline int wave_logits(const XT *__restrict__ xr, const WT *__restric
     }
     int nfb = 0;
 #pragma unroll
-    for (int i = 0; i < kEPW; ++i) {
+    for (int i = 0; i < EPW; ++i) {
         if (i < ne) {
             const double si = wave_sum_f64(s[i][0] + s[i][1]);
             const double ai = wave_sum_f64(kBf16 ? ((double)a32[i][0] + (double)a32[i][1]) * infl : a[i][0] + a[i][1]);
@@ -492,11 +494,12 @@ __device__ inline void token_topk(const float *__restrict__ l, int E, int k, int
 // ------------------------------------------------------------------ fused routing kernel
 //
 // Grid = T x bpt workgroups of 4 waves.  Workgroup (t, q) computes the logits of token
-// t for experts [4*q*epw, 4*(q+1)*epw) and, when the MFMA path is enabled, its share
-// of the token's 2-term FP8 activation split.  The last workgroup of token t to finish
-// (a device-scope counter) runs that token's top-k softmax in one wave.  The last
-// token to finish then groups all (token, choice) pairs by expert.  The counters are reset by the workgroup that
-// consumes them, so they read zero at the start of every launch.
+// t for experts [4*q*epw, 4*(q+1)*epw).  The last workgroup of token t to finish (a
+// device-scope counter) runs that token's top-k softmax in one wave while its other
+// three waves write the token's 2-term FP8 activation split (when the MFMA path is
+// on).  The last token to finish then groups all (token, choice) pairs by expert.  The
+// counters are reset by the workgroup that consumes them, so they read zero at the
+// start of every launch.
 
 
 struct RouteArgs {
@@ -527,18 +530,43 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
     const int E = A.E, H = A.H;
     const XT *xr = (const XT *)A.x + (size_t)t * H;
 
-    // 1. logits of this workgroup's experts, and its share of the token's activation
-    // split (groups of 32 inputs spread over the token's workgroups)
+    // 1. logits of this workgroup's experts
     {
         const int e0 = (q * 4 + wave) * A.epw;
         const int ne = min(E, e0 + A.epw) - e0;
         if (ne > 0) {
-            const int nfb = wave_logits<XT, WT>(xr, (const WT *)A.wr, A.bias, H, e0, ne, lane, A.logits + (size_t)t * E);
+            const WT *wr = (const WT *)A.wr;
+            float *lrow = A.logits + (size_t)t * E;
+            // one expert per wave: no loads for empty expert slots, and a row of up to
+            // 4096 bf16 inputs in one round trip
+            int nfb;
+            if (A.epw > 1)
+                nfb = wave_logits<XT, WT, kEPW, 4>(xr, wr, A.bias, H, e0, ne, lane, lrow);
+            else if (sizeof(XT) == 2 && H <= 8 * 512)
+                nfb = wave_logits<XT, WT, 1, 8>(xr, wr, A.bias, H, e0, ne, lane, lrow);
+            else
+                nfb = wave_logits<XT, WT, 1, 4>(xr, wr, A.bias, H, e0, ne, lane, lrow);
             if (lane == 0 && nfb) atomicAdd(A.fb_acc, nfb);
         }
-        if (A.xs_hi) {
-            const int G = H / 32, per = (G + A.bpt - 1) / A.bpt;
-            for (int g = q * per + threadIdx.x; g < min(G, (q + 1) * per); g += blockDim.x) {
+    }
+    // Publish this workgroup's logits, then count it; the last workgroup of the token
+    // goes on.
+    wait_stores();
+    __syncthreads();
+    if (threadIdx.x == 0) s_flag = atomicAdd(&A.cnt_tok[t * kCounterStride], 1) == A.bpt - 1;
+    __syncthreads();
+    if (!s_flag) return;
+
+    // 2. last workgroup of token t: top-k softmax in wave 0 while waves 1-3 write the
+    // token's 2-term activation split when the MFMA path is on (groups of 32 inputs)
+    if (wave == 0) {
+        token_topk(A.logits + (size_t)t * E, E, A.k, A.ids + (size_t)t * A.k, A.wts + (size_t)t * A.k,
+                   A.ids_user ? A.ids_user + (size_t)t * A.k : nullptr,
+                   A.wts_user ? A.wts_user + (size_t)t * A.k : nullptr, lane);
+    } else if (A.xs_hi) {
+        {
+            const int G = H / 32;
+            for (int g = threadIdx.x - kWave; g < G; g += blockDim.x - kWave) {
                 float v[32], res[32];
                 uint32_t qh[8], ql[8];
                 load32_f32<XT>(xr + g * 32, v);
@@ -556,19 +584,6 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
             }
         }
     }
-    // Publish this workgroup's logits, then count it; the last workgroup of the token
-    // goes on.
-    wait_stores();
-    __syncthreads();
-    if (threadIdx.x == 0) s_flag = atomicAdd(&A.cnt_tok[t * kCounterStride], 1) == A.bpt - 1;
-    __syncthreads();
-    if (!s_flag) return;
-
-    // 2. last workgroup of token t: top-k softmax (wave 0)
-    if (wave == 0)
-        token_topk(A.logits + (size_t)t * E, E, A.k, A.ids + (size_t)t * A.k, A.wts + (size_t)t * A.k,
-                   A.ids_user ? A.ids_user + (size_t)t * A.k : nullptr,
-                   A.wts_user ? A.wts_user + (size_t)t * A.k : nullptr, lane);
     if (threadIdx.x == 0) st_dev(&A.cnt_tok[t * kCounterStride], 0);
     if (!A.do_group) return;
     wait_stores();
