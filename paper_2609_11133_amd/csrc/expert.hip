@@ -520,24 +520,40 @@ __global__ __launch_bounds__(WAVES * 64) void w2_gemv_kernel(const uint8_t *__re
 // ------------------------------------------------------------------ combine
 //
 // y[t] = sum_j w[t,j] * o[slot(t,j)], j ascending; each output element is written by
-// exactly one thread, so no atomics and a fixed summation order.
+// exactly one thread, so no atomics and a fixed summation order.  Choices are taken
+// eight at a time: their slots and weights first, then their rows of o, so a token
+// costs two memory round trips per eight choices rather than two per choice.
 template <bool OUTF32>
 __global__ __launch_bounds__(256) void combine_kernel(int k, int H, const int32_t *__restrict__ slot_of,
                                                       const float *__restrict__ wts, const float *__restrict__ obuf,
                                                       void *__restrict__ y)
 {
+    constexpr int U = 8;
     const int t = blockIdx.y;
     const int n = (blockIdx.x * blockDim.x + threadIdx.x) * 4;
     if (n >= H) return;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int j = 0; j < k; ++j) {
-        const int s = slot_of[(size_t)t * k + j];
-        const float w = wts[(size_t)t * k + j];
-        const float4 v = *reinterpret_cast<const float4 *>(obuf + (size_t)s * H + n);
-        acc.x = fmaf(w, v.x, acc.x);
-        acc.y = fmaf(w, v.y, acc.y);
-        acc.z = fmaf(w, v.z, acc.z);
-        acc.w = fmaf(w, v.w, acc.w);
+    for (int j0 = 0; j0 < k; j0 += U) {
+        const int nu = min(U, k - j0);
+        int s[U];
+        float w[U];
+        float4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            s[u] = slot_of[(size_t)t * k + j0 + min(u, nu - 1)];
+            w[u] = wts[(size_t)t * k + j0 + min(u, nu - 1)];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = *reinterpret_cast<const float4 *>(obuf + (size_t)s[u] * H + n);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (u < nu) {
+                acc.x = fmaf(w[u], v[u].x, acc.x);
+                acc.y = fmaf(w[u], v[u].y, acc.y);
+                acc.z = fmaf(w[u], v[u].z, acc.z);
+                acc.w = fmaf(w[u], v[u].w, acc.w);
+            }
+        }
     }
     if constexpr (OUTF32) {
         *reinterpret_cast<float4 *>((float *)y + (size_t)t * H + n) = acc;
