@@ -1,8 +1,9 @@
-"""TEST INFRASTRUCTURE -- numpy front end of the fp64 CPU oracle (``moe_oracle.c``).
+"""TEST INFRASTRUCTURE -- numpy front end of the fp64 CPU oracles (``moe_oracle.c``, the MoE
+decode layer; ``attn_oracle.c``, decode attention over a paged KV cache).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
 ``bench.py`` may import this package.  It shares no code with the HIP library and
-never imports it.  See ``moe_oracle.c`` for the definition it implements.
+never imports it.  See the C files for the definitions they implement.
 """
 from __future__ import annotations
 
@@ -13,7 +14,7 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRC = os.path.join(_HERE, "moe_oracle.c")
+_SRCS = [os.path.join(_HERE, "moe_oracle.c"), os.path.join(_HERE, "attn_oracle.c")]
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 DT_F32, DT_BF16 = 0, 1
@@ -25,7 +26,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp"
         subprocess.check_call(
-            ["gcc", "-O2", "-fPIC", "-shared", "-std=c11", "-pthread", "-ffp-contract=off", "-o", tmp, _SRC, "-lm"]
+            ["gcc", "-O2", "-fPIC", "-shared", "-std=c11", "-pthread", "-ffp-contract=off", "-o", tmp, *_SRCS, "-lm"]
         )
         os.replace(tmp, _LIB)
     return _LIB
@@ -57,6 +58,8 @@ def _load():
         lib.oracle_forward.argtypes = [
             i64, i32, i64, i32, i32, i32, p, i64, p, p, p, p, i32, p, i64, i32, p, p, p, p
         ]
+        lib.oracle_attn_decode.restype = ctypes.c_int
+        lib.oracle_attn_decode.argtypes = [i32, i32, i32, i32, i32, p, p, p, i64, p, i32, p, ctypes.c_double, p]
         lib.oracle_expert_ffn.restype = ctypes.c_int
         lib.oracle_expert_ffn.argtypes = [i64, i32, i64, i32, p, p, i32, p, p]
         _lib = lib
@@ -161,4 +164,27 @@ def expert_ffn(expert_w, scales, e, xv, hidden, inter, wfmt):
                                    _ptr(xv), _ptr(o))
     if rc != 0:
         raise ValueError("oracle_expert_ffn rejected its arguments")
+    return o
+
+
+def attn_decode(q, k_cache, v_cache, block_table, ctx, scale):
+    """Decode attention over a paged KV cache (``attn_oracle.c``), fp64.
+
+    q [B, Hq, D] bf16 bits (uint16); k_cache [n_pages, Hkv, P, D] and v_cache
+    [n_pages, Hkv, D, P] bf16 bits; block_table [B, max_pages] int32; ctx [B] int32;
+    returns o [B, Hq, D] float64."""
+    q = np.ascontiguousarray(q, np.uint16)
+    k_cache = np.ascontiguousarray(k_cache, np.uint16)
+    v_cache = np.ascontiguousarray(v_cache, np.uint16)
+    block_table = np.ascontiguousarray(block_table, np.int32)
+    ctx = np.ascontiguousarray(ctx, np.int32)
+    B, Hq, D = q.shape
+    n_pages, Hkv, P, D2 = k_cache.shape
+    assert D2 == D and v_cache.shape == (n_pages, Hkv, D, P)
+    assert block_table.shape[0] == B and ctx.shape == (B,)
+    o = np.empty((B, Hq, D), np.float64)
+    rc = _load().oracle_attn_decode(B, Hq, Hkv, D, P, _ptr(q), _ptr(k_cache), _ptr(v_cache), n_pages,
+                                    _ptr(block_table), block_table.shape[1], _ptr(ctx), float(scale), _ptr(o))
+    if rc != 0:
+        raise ValueError("oracle_attn_decode: inconsistent sizes or page index out of range")
     return o

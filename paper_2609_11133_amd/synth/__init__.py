@@ -55,6 +55,7 @@ def _load():
         lib.synth_e2m1_from_f64.restype = ctypes.c_uint8
         lib.synth_e2m1_from_f64.argtypes = [ctypes.c_double]
         lib.synth_x_bf16.argtypes = [u64, u32, i64, i64, p]
+        lib.synth_normal_bf16.argtypes = [u64, u64, i64, ctypes.c_double, p]
         lib.synth_x_f32.argtypes = [u64, u32, i64, i64, p]
         lib.synth_router_bf16.argtypes = [u64, u32, i64, i64, p]
         lib.synth_router_f32.argtypes = [u64, u32, i64, i64, p]
@@ -74,7 +75,7 @@ def _ptr(a: np.ndarray) -> int:
     return a.ctypes.data
 
 
-TAGS = dict(x=1, router=2, bias=3, gate=4, up=5, down=6, perm=7)
+TAGS = dict(x=1, router=2, bias=3, gate=4, up=5, down=6, perm=7, q=8, k=9, v=10)
 
 
 def stream_key(seed: int, tag: str, layer: int, sub: int = 0) -> int:
@@ -85,6 +86,13 @@ def normal(seed: int, tag: str, layer: int, sub: int, start: int, n: int, sigma:
     """Raw Gaussian draws (Irwin-Hall(12)) of one stream, as fp64."""
     out = np.empty(n, np.float64)
     _load().synth_normal_f64(stream_key(seed, tag, layer, sub), start, n, sigma, _ptr(out))
+    return out
+
+
+def normal_bf16(seed: int, tag: str, layer: int, sub: int, n: int, sigma: float = 1.0) -> np.ndarray:
+    """n Gaussian draws of one stream times sigma, rounded to bf16 (uint16 bit patterns)."""
+    out = np.empty(n, np.uint16)
+    _load().synth_normal_bf16(stream_key(seed, tag, layer, sub), 0, n, sigma, _ptr(out))
     return out
 
 

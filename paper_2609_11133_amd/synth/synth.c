@@ -154,6 +154,13 @@ uint8_t synth_e2m1_from_f64(double v)
 
 /* ---------------------------------------------------------------- activations */
 
+/* n values sigma * N(0,1) of one stream (draws start..start+n-1), rounded to bf16. */
+void synth_normal_bf16(uint64_t key, uint64_t start, int64_t n, double sigma, uint16_t *out)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; i++) out[i] = synth_bf16_from_f64(sigma * normal_at(key, start + (uint64_t)i));
+}
+
 void synth_x_bf16(uint64_t seed, uint32_t batch, int64_t T, int64_t H, uint16_t *out)
 {
     uint64_t key = synth_stream_key(seed, TAG_X, batch, 0);
