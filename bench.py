@@ -82,6 +82,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-power", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU work of the oracle sample")
+    ap.add_argument("--attn", action="store_true",
+                    help="decode attention over a paged KV cache instead of the MoE layer: one JSON line per "
+                         "workload of attn_workload.ATTN_CONFIGS")
     ap.add_argument("--stack", action="store_true",
                     help="also time the stack of 12 distinct 480B-shaped layers decoded back to back, T = 1..256")
     ap.add_argument("--stack-steps", type=int, default=20)
@@ -205,6 +208,69 @@ def run_stack(args, dev):
                 steps=args.stack_steps, by_tokens=out)
 
 
+def run_attn(args, dev):
+    """Decode attention: per workload, B sequences' step time between HIP events over K
+    steps that cycle KV-cache copies (>= 1 GB, so no step finds its cache in the MALL)
+    and 4 length draws; GB/s = the context's K and V bytes per step / step time."""
+    import numpy as np
+    import torch
+
+    from paper_2609_11133_amd import attn_workload as A
+    from paper_2609_11133_amd import binding as B
+
+    for cfg in A.ATTN_CONFIGS:
+        draws = [A.host_attn(cfg, draw=d, garbage=False) for d in range(4)]
+        mp = max(h.block_table.shape[1] for h in draws)
+        nbytes = max(h.k_cache.nbytes + h.v_cache.nbytes for h in draws)
+        copies = max(1, math.ceil(1e9 / nbytes))
+        dd = []
+        for h in draws:
+            bt = np.zeros((cfg.batch, mp), np.int32)
+            bt[:, : h.block_table.shape[1]] = h.block_table
+            h.block_table = bt
+            d0 = A.to_device(h, dev)
+            dd.append([d0] + [dict(d0, k_cache=d0["k_cache"].clone(), v_cache=d0["v_cache"].clone())
+                              for _ in range(copies - 1)])
+        m = B.AttnDecode(B.make_attn_config(cfg.n_q_heads, cfg.n_kv_heads, cfg.batch, mp), device=dev)
+        out = torch.empty((cfg.batch, cfg.n_q_heads, 128), dtype=torch.int16, device=dev)
+        scale = 1 / math.sqrt(128)
+
+        def step(i):
+            h, d = draws[i % 4], dd[i % 4][(i // 4) % copies]
+            m.forward(d["q"], d["k_cache"], d["v_cache"], h.n_pages, d["block_table"], d["ctx"], cfg.batch, scale, out)
+
+        for i in range(args.warmup):
+            step(i)
+        stream = torch.cuda.current_stream(dev)
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize(dev)
+        start.record(stream)
+        for i in range(args.steps):
+            step(i)
+        end.record(stream)
+        torch.cuda.synchronize(dev)
+        ms = start.elapsed_time(end) / args.steps
+        kv = statistics.mean(draws[i % 4].kv_bytes(cfg.n_kv_heads) for i in range(args.steps))
+        ctx_mean = statistics.mean(float(h.ctx.mean()) for h in draws)
+        gbs = kv / (ms * 1e-3) / 1e9
+        line = {
+            "metric": "decode attention steps: sequences/s and achieved HBM GB/s (% of peak)",
+            "value": cfg.batch / (ms * 1e-3), "unit": "sequences/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": f"{cfg.name}: {cfg.batch} sequences, {cfg.n_q_heads} query / {cfg.n_kv_heads} "
+                                   f"key-value heads, head dim 128, 16-token pages, {cfg.mix} context lengths "
+                                   f"(mean {ctx_mean:.0f} tokens)", "cold_cache": f"{copies} KV-cache copies x 4 draws"},
+            "roofline": {"kernel": "attn_split_kernel + attn_combine_kernel (one step)", "bound": "hbm",
+                         "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS,
+                         "bytes_per_step": kv},
+        }
+        print(f"[attn] {cfg.name}: {ms * 1e3:.1f} us/step, {gbs:.0f} GB/s ({gbs / PEAK_HBM_GBS:.3f} of peak), "
+              f"mean context {ctx_mean:.0f}", file=sys.stderr, flush=True)
+        print(json.dumps(line), flush=True)
+        del dd, m
+        torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -226,6 +292,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     settle_hbm(dev)
+    if args.attn:
+        run_attn(args, dev)
+        return
     cfg = C.BY_NAME[args.config]
     small = [t for t in cfg.tokens if t <= 64]
     T_main = args.tokens or (max(small) if small else min(cfg.tokens))

@@ -1,4 +1,5 @@
-"""ctypes binding of ``libmoe_decode.so`` (C ABI in ``include/moe_decode.h``).
+"""ctypes binding of ``libmoe_decode.so`` (C ABI in ``include/moe_decode.h`` and
+``include/attn_decode.h``).
 
 Argument marshalling only: every step of the decode layer runs in the library's HIP
 kernels.  Functions carry the C names; pointer arguments accept a torch tensor
@@ -43,6 +44,18 @@ class moe_decode_stats(ctypes.Structure):
         ("n_active_mfma", ctypes.c_int32),
         ("n_fallback", ctypes.c_int32),
         ("active_weight_bytes", ctypes.c_int64),
+    ]
+
+
+class attn_decode_config(ctypes.Structure):
+    _fields_ = [
+        ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("page_size", ctypes.c_int32),
+        ("max_batch", ctypes.c_int32),
+        ("max_pages_per_seq", ctypes.c_int32),
+        ("reserved", ctypes.c_int32 * 4),
     ]
 
 
@@ -91,6 +104,13 @@ def lib():
         L.moe_decode_status_string.argtypes = [ctypes.c_int]
         L.moe_decode_last_error.restype = ctypes.c_char_p
         L.moe_decode_last_error.argtypes = [P]
+        acfgp = ctypes.POINTER(attn_decode_config)
+        L.attn_decode_workspace_bytes.restype = SZ
+        L.attn_decode_workspace_bytes.argtypes = [acfgp]
+        L.attn_decode_forward.restype = ctypes.c_int
+        L.attn_decode_forward.argtypes = [acfgp, P, SZ, P, P, P, P, ctypes.c_int64, P, P, I32, ctypes.c_float, P]
+        L.attn_decode_last_error.restype = ctypes.c_char_p
+        L.attn_decode_last_error.argtypes = []
         _lib = L
     return _lib
 
@@ -226,3 +246,46 @@ class MoEDecode:
             self.close()
         except Exception:
             pass
+
+
+# ---------------------------------------------------------------- decode attention
+
+
+def make_attn_config(n_q_heads, n_kv_heads, max_batch, max_pages_per_seq, head_dim=128, page_size=16):
+    return attn_decode_config(n_q_heads, n_kv_heads, head_dim, page_size, max_batch, max_pages_per_seq)
+
+
+def attn_decode_workspace_bytes(cfg: attn_decode_config) -> int:
+    return int(lib().attn_decode_workspace_bytes(ctypes.byref(cfg)))
+
+
+def attn_decode_forward(cfg, workspace, workspace_bytes, stream, q, k_cache, v_cache, n_pages, block_table, ctx_lens,
+                        batch, scale, out):
+    st = lib().attn_decode_forward(ctypes.byref(cfg), _addr(workspace), workspace_bytes, stream, _addr(q),
+                                   _addr(k_cache), _addr(v_cache), n_pages, _addr(block_table), _addr(ctx_lens),
+                                   batch, scale, _addr(out))
+    if st != MOE_OK:
+        raise MoEDecodeError(st, lib().attn_decode_last_error().decode() or "attn_decode_forward failed")
+
+
+class AttnDecode:
+    """A configuration plus its device workspace (a torch uint8 tensor on ``device``);
+    ``forward`` enqueues one decode step of attention on torch's current stream."""
+
+    def __init__(self, cfg: attn_decode_config, device="cuda"):
+        import torch
+
+        self.cfg = cfg
+        self.nbytes = attn_decode_workspace_bytes(cfg)
+        if self.nbytes == 0:
+            raise MoEDecodeError(MOE_ERR_INVALID, "invalid attention configuration")
+        self.workspace = torch.empty(self.nbytes + 256, dtype=torch.uint8, device=device)
+        self._ws_addr = (self.workspace.data_ptr() + 255) // 256 * 256
+        self.device = self.workspace.device
+
+    def forward(self, q, k_cache, v_cache, n_pages, block_table, ctx_lens, batch, scale, out):
+        import torch
+
+        stream = torch.cuda.current_stream(self.device).cuda_stream
+        attn_decode_forward(self.cfg, self._ws_addr, self.nbytes, stream, q, k_cache, v_cache, n_pages, block_table,
+                            ctx_lens, batch, scale, out)

@@ -10,7 +10,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmoe_decode.so")
 PROBE = os.path.join(PKG, "stream_probe")
-SOURCES = ["route.hip", "expert.hip", "mfma.hip", "nvfp4.hip", "api.hip"]
+SOURCES = ["route.hip", "expert.hip", "mfma.hip", "nvfp4.hip", "attn.hip", "api.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

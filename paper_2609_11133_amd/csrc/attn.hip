@@ -1,0 +1,338 @@
+// Decode attention over a paged KV cache: one decode step of grouped-query attention
+// (scaled dot-product attention with Hq / Hkv query heads per key/value head), the
+// KV-cache half of the decode step's byte streams, on the gfx950 bf16 matrix cores.
+//
+// Split over the context.  Workgroup (c, g, b) of four waves takes tokens
+// [256c, 256c + 256) of sequence b for key/value head g and its (up to 16) query heads;
+// each wave takes 64 of those tokens as four 16-token tiles (one cache page each).
+//   S^T = K_tile . Q^T   v_mfma_f32_16x16x32_bf16, A = keys (rows = tokens, K = dims),
+//                        B = queries (columns = heads): lane l ends with the scores of
+//                        head l%16 for tokens 4(l/16)..4(l/16)+3 of the tile.
+//   O  += P . V          A = probabilities (rows = heads), B = values (columns = dims):
+//                        the lane's eight K slots are its four tokens of two tiles,
+//                        which is exactly what the S^T accumulators hold, so P needs no
+//                        transpose; the values are read dimension-major (a page stores
+//                        V as [D][16]), four contiguous tokens per tile.
+// The workgroup shares one score maximum per head (through LDS), so its four waves' P.V
+// partials add directly; it writes (max, sum, O) of its split, and a second kernel
+// merges the splits of each (sequence, query head) in split order.
+//
+// Operand layout of v_mfma_f32_16x16x32_bf16 (checked on the device): lane l holds
+// row/column l%16 and K [8g, 8g+8) with g = l/16; the result gives lane l rows
+// 4g..4g+3 of column l%16.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "../../include/attn_decode.h"
+
+namespace attn {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+
+constexpr int kD = 128;                    // head dimension
+constexpr int kP = 16;                     // tokens per page
+constexpr int kWaves = 4;                  // waves per workgroup
+constexpr int kWaveTok = 64;               // tokens per wave
+constexpr int kTiles = kWaveTok / kP;      // 16-token tiles (pages) per wave
+constexpr int kChunk = kWaves * kWaveTok;  // tokens per split
+constexpr int kDT = kD / 16;               // 16-column tiles of the output
+constexpr float kLog2e = 1.44269504088896340736f;
+constexpr int kRawBufferWord3 = 0x00020000;  // untyped 32-bit data format, no swizzle
+
+// A raw buffer over `bytes` bytes at `base`: loads past the end return zeros and make
+// no memory request, so a page the kernel must not read gets bytes = 0.
+__device__ inline __amdgpu_buffer_rsrc_t rsrc(const void *base, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, kRawBufferWord3);
+}
+
+__device__ inline bf16x8 as_bf16x8(const u32x4v &u) { return __builtin_bit_cast(bf16x8, u); }
+
+// Split kernel: partial (max, sum, O) of one 256-token split for one (sequence, key/value
+// head) and its query heads.  Grid (splits, Hkv, B), 256 threads.  Scores are kept in
+// log2 units (scale * log2 e folded in), so p = exp2(s - m).
+__global__ __launch_bounds__(256) void attn_split_kernel(const uint16_t *__restrict__ q,
+                                                         const uint16_t *__restrict__ kc,
+                                                         const uint16_t *__restrict__ vc, int64_t n_pages,
+                                                         const int32_t *__restrict__ block_table, int max_pages,
+                                                         const int32_t *__restrict__ ctx, int Hkv, int G,
+                                                         float scale_log2, float *__restrict__ po,
+                                                         float *__restrict__ pml, int S)
+{
+    __shared__ float s_max[kWaves][16], s_sum[kWaves][16];
+    __shared__ f32x4 red[kWaves][kDT][64];
+    const int c = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+    const int L = min(max(ctx[b], 0), max_pages * kP);
+    const int t0 = c * kChunk;
+    if (t0 >= L) return;  // uniform over the workgroup
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int r = lane & 15, lg = lane >> 4;
+
+    // Q^T operand: head r of the group (zeros past it), dims [32i + 8lg, 32i + 8lg + 8)
+    bf16x8 qop[4];
+    {
+        const bool live = r < G;
+        const uint16_t *qrow = q + ((size_t)b * Hkv * G + (size_t)g * G + (live ? r : 0)) * kD;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const u32x4v w = live ? *reinterpret_cast<const u32x4v *>(qrow + 32 * i + 8 * lg) : (u32x4v){0, 0, 0, 0};
+            qop[i] = as_bf16x8(w);
+        }
+    }
+
+    // This wave's four pages: keys (token r, dims [32i + 8lg, +8)) and values (dims
+    // 16j + r, tokens [4lg, 4lg + 4)).  Pages past the context or outside the cache
+    // read as zeros.
+    const int tw = t0 + kWaveTok * wave;
+    u32x4v ka[kTiles][4];
+    u32x2v vb[kTiles][kDT];
+#pragma unroll
+    for (int tt = 0; tt < kTiles; ++tt) {
+        const int ts = tw + kP * tt;  // first token of the tile (page aligned)
+        int pg = ts < L ? block_table[(size_t)b * max_pages + ts / kP] : -1;
+        pg = __builtin_amdgcn_readfirstlane(pg);
+        const bool ok = pg >= 0 && (int64_t)pg < n_pages;
+        const int64_t p = ok ? pg : 0;
+        const __amdgpu_buffer_rsrc_t kr = rsrc(kc + (p * Hkv + g) * (int64_t)(kP * kD), ok ? kP * kD * 2 : 0);
+        const __amdgpu_buffer_rsrc_t vr = rsrc(vc + (p * Hkv + g) * (int64_t)(kP * kD), ok ? kP * kD * 2 : 0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            ka[tt][i] = __builtin_amdgcn_raw_buffer_load_b128(kr, (uint32_t)((r * kD + 32 * i + 8 * lg) * 2), 0, 0);
+#pragma unroll
+        for (int j = 0; j < kDT; ++j)
+            vb[tt][j] = __builtin_amdgcn_raw_buffer_load_b64(vr, (uint32_t)(((16 * j + r) * kP + 4 * lg) * 2), 0, 0);
+    }
+
+    // scores of this lane's 16 (token, head r) pairs, masked past the context
+    float s[kTiles][4];
+    float m = -INFINITY;
+#pragma unroll
+    for (int tt = 0; tt < kTiles; ++tt) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ka[tt][i]), qop[i], acc, 0, 0, 0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const bool live = tw + kP * tt + 4 * lg + e < L;
+            s[tt][e] = live ? acc[e] * scale_log2 : -INFINITY;
+            m = fmaxf(m, s[tt][e]);
+        }
+    }
+    m = fmaxf(m, __shfl_xor(m, 16));
+    m = fmaxf(m, __shfl_xor(m, 32));
+    if (lg == 0) s_max[wave][r] = m;
+    __syncthreads();
+    m = fmaxf(fmaxf(s_max[0][r], s_max[1][r]), fmaxf(s_max[2][r], s_max[3][r]));  // finite: token t0 < L
+
+    // probabilities (bf16 for the P.V product; the sum uses the same rounded values)
+    float l = 0.f;
+    bf16x8 pa[kTiles / 2];
+#pragma unroll
+    for (int st = 0; st < kTiles / 2; ++st)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int e = 0; e < 4; e += 2) {
+                const f32x2 pv = {exp2f(s[2 * st + h][e] - m), exp2f(s[2 * st + h][e + 1] - m)};
+                const bf16x2 pb = __builtin_convertvector(pv, bf16x2);
+                pa[st][4 * h + e] = pb.x;
+                pa[st][4 * h + e + 1] = pb.y;
+                l += (float)pb.x + (float)pb.y;
+            }
+    l += __shfl_xor(l, 16);
+    l += __shfl_xor(l, 32);
+    if (lg == 0) s_sum[wave][r] = l;
+
+    // values past the context are zeroed: a cache slot past it may hold any bits, and
+    // 0 * NaN would not vanish
+#pragma unroll
+    for (int tt = 0; tt < kTiles; ++tt) {
+        const int nv = min(max(L - (tw + kP * tt + 4 * lg), 0), 4);
+        const uint32_t m0 = nv >= 2 ? 0xFFFFFFFFu : (nv == 1 ? 0x0000FFFFu : 0u);
+        const uint32_t m1 = nv >= 4 ? 0xFFFFFFFFu : (nv == 3 ? 0x0000FFFFu : 0u);
+#pragma unroll
+        for (int j = 0; j < kDT; ++j) {
+            vb[tt][j].x &= m0;
+            vb[tt][j].y &= m1;
+        }
+    }
+    f32x4 o[kDT];
+#pragma unroll
+    for (int j = 0; j < kDT; ++j) o[j] = (f32x4){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < kTiles / 2; ++st)
+#pragma unroll
+        for (int j = 0; j < kDT; ++j) {
+            const u32x4v vv = {vb[2 * st][j].x, vb[2 * st][j].y, vb[2 * st + 1][j].x, vb[2 * st + 1][j].y};
+            o[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa[st], as_bf16x8(vv), o[j], 0, 0, 0);
+        }
+
+    // the workgroup's O: the four waves' partials in wave order
+#pragma unroll
+    for (int j = 0; j < kDT; ++j) red[wave][j][lane] = o[j];
+    __syncthreads();
+    const size_t part = ((size_t)b * Hkv + g) * S + c;
+#pragma unroll
+    for (int k = 0; k < 16 * kD / 256; ++k) {
+        const int e = tid + 256 * k;  // (head n, dim d)
+        const int n = e / kD, d = e % kD;
+        const int j = d / 16, ln = 16 * (n / 4) + d % 16, comp = n % 4;
+        const float v = ((red[0][j][ln][comp] + red[1][j][ln][comp]) + red[2][j][ln][comp]) + red[3][j][ln][comp];
+        po[part * 16 * kD + e] = v;
+    }
+    if (tid < 16)
+        reinterpret_cast<f32x2 *>(pml)[part * 16 + tid] =
+            (f32x2){m, ((s_sum[0][tid] + s_sum[1][tid]) + s_sum[2][tid]) + s_sum[3][tid]};
+}
+
+// Combine kernel: out[b][g*G + n][d] = sum_c 2^(m_c - M) O_c[n][d] / sum_c 2^(m_c - M) l_c
+// over the splits c of (b, g) in ascending order, M = max_c m_c; zeros for an empty
+// context.  Grid (G, Hkv, B), 128 threads: thread d of workgroup (n, g, b) owns one
+// output and keeps sixteen splits' loads in flight; every thread forms the same
+// denominator in the same order.
+__global__ __launch_bounds__(128) void attn_combine_kernel(const float *__restrict__ po, const float *__restrict__ pml,
+                                                           const int32_t *__restrict__ ctx, int max_pages, int Hkv,
+                                                           int G, int S, uint16_t *__restrict__ out)
+{
+    constexpr int U = 16;
+    __shared__ float s_m[2];
+    const int n = blockIdx.x, g = blockIdx.y, b = blockIdx.z, d = threadIdx.x;
+    const int L = min(max(ctx[b], 0), max_pages * kP);
+    const int ns = (L + kChunk - 1) / kChunk;
+    const size_t part0 = ((size_t)b * Hkv + g) * S;
+    const f32x2 *ml = reinterpret_cast<const f32x2 *>(pml);
+    float M = -INFINITY;
+    for (int c = d; c < ns; c += 128) M = fmaxf(M, ml[(part0 + c) * 16 + n].x);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o));
+    if ((d & 63) == 0) s_m[d >> 6] = M;
+    __syncthreads();
+    M = fmaxf(s_m[0], s_m[1]);
+    float num = 0.f, den = 0.f;
+    for (int c0 = 0; c0 < ns; c0 += U) {
+        f32x2 mlv[U];
+        float ov[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const size_t c = part0 + min(c0 + u, ns - 1);
+            mlv[u] = ml[c * 16 + n];
+            ov[u] = po[(c * 16 + n) * kD + d];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (c0 + u < ns) {
+                const float w = exp2f(mlv[u].x - M);
+                den = fmaf(w, mlv[u].y, den);
+                num = fmaf(w, ov[u], num);
+            }
+    }
+    const float y = ns ? num / den : 0.f;
+    const bf16x2 yb = __builtin_convertvector((f32x2){y, 0.f}, bf16x2);
+    out[(((size_t)b * Hkv + g) * G + n) * kD + d] = __builtin_bit_cast(uint16_t, yb.x);
+}
+
+thread_local char g_err[256];
+
+int fail(int code, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int check_config(const attn_decode_config *c)
+{
+    if (!c) return fail(ATTN_ERR_INVALID, "config is NULL");
+    for (int i = 0; i < 4; ++i)
+        if (c->reserved[i] != 0) return fail(ATTN_ERR_INVALID, "config.reserved[%d] must be zero", i);
+    if (c->n_kv_heads < 1) return fail(ATTN_ERR_INVALID, "n_kv_heads=%d must be positive", c->n_kv_heads);
+    if (c->n_q_heads < 1 || c->n_q_heads % c->n_kv_heads)
+        return fail(ATTN_ERR_INVALID, "n_q_heads=%d must be a positive multiple of n_kv_heads=%d", c->n_q_heads,
+                    c->n_kv_heads);
+    if (c->n_q_heads / c->n_kv_heads > 16)
+        return fail(ATTN_ERR_UNSUPPORTED, "at most 16 query heads per key/value head (got %d)",
+                    c->n_q_heads / c->n_kv_heads);
+    if (c->n_kv_heads > 65535) return fail(ATTN_ERR_INVALID, "n_kv_heads=%d exceeds 65535", c->n_kv_heads);
+    if (c->head_dim != kD) return fail(ATTN_ERR_UNSUPPORTED, "head_dim=%d (only %d)", c->head_dim, kD);
+    if (c->page_size != kP) return fail(ATTN_ERR_UNSUPPORTED, "page_size=%d (only %d)", c->page_size, kP);
+    if (c->max_batch < 1 || c->max_batch > 4096) return fail(ATTN_ERR_INVALID, "max_batch=%d outside 1..4096", c->max_batch);
+    if (c->max_pages_per_seq < 1 || c->max_pages_per_seq > 65536)
+        return fail(ATTN_ERR_INVALID, "max_pages_per_seq=%d outside 1..65536", c->max_pages_per_seq);
+    return ATTN_OK;
+}
+
+int max_splits(const attn_decode_config *c) { return (c->max_pages_per_seq * kP + kChunk - 1) / kChunk; }
+
+size_t partial_o_bytes(const attn_decode_config *c)
+{
+    return ((size_t)c->max_batch * c->n_kv_heads * max_splits(c) * 16 * kD * 4 + 255) & ~(size_t)255;
+}
+
+bool aligned(const void *p, size_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+}  // namespace
+}  // namespace attn
+
+extern "C" size_t attn_decode_workspace_bytes(const attn_decode_config *cfg)
+{
+    using namespace attn;
+    if (check_config(cfg) != ATTN_OK) return 0;
+    return partial_o_bytes(cfg) + (size_t)cfg->max_batch * cfg->n_kv_heads * max_splits(cfg) * 16 * 8;
+}
+
+extern "C" int attn_decode_forward(const attn_decode_config *cfg, void *workspace, size_t workspace_bytes, void *stream,
+                                   const void *q, const void *k_cache, const void *v_cache, int64_t n_pages,
+                                   const int32_t *block_table, const int32_t *ctx_lens, int32_t batch, float scale,
+                                   void *out)
+{
+    using namespace attn;
+    g_err[0] = 0;
+    const int rc = check_config(cfg);
+    if (rc != ATTN_OK) return rc;
+    if (batch < 0 || batch > cfg->max_batch) return fail(ATTN_ERR_INVALID, "batch=%d outside 0..%d", batch, cfg->max_batch);
+    if (!(scale > 0.f) || !isfinite(scale)) return fail(ATTN_ERR_INVALID, "scale must be finite and positive");
+    if (n_pages < 1) return fail(ATTN_ERR_INVALID, "n_pages=%lld must be positive", (long long)n_pages);
+    const void *ptrs[] = {q, k_cache, v_cache, out};
+    const char *names[] = {"q", "k_cache", "v_cache", "out"};
+    for (int i = 0; i < 4; ++i) {
+        if (!ptrs[i]) return fail(ATTN_ERR_INVALID, "%s is NULL", names[i]);
+        if (!aligned(ptrs[i], 16)) return fail(ATTN_ERR_INVALID, "%s must be 16-byte aligned", names[i]);
+    }
+    if (!block_table || !aligned(block_table, 4)) return fail(ATTN_ERR_INVALID, "block_table is NULL or misaligned");
+    if (!ctx_lens || !aligned(ctx_lens, 4)) return fail(ATTN_ERR_INVALID, "ctx_lens is NULL or misaligned");
+    if (out == q || out == k_cache || out == v_cache) return fail(ATTN_ERR_INVALID, "out must not alias an input");
+    if (!workspace || !aligned(workspace, 256)) return fail(ATTN_ERR_WORKSPACE, "workspace is NULL or not 256-byte aligned");
+    if (workspace_bytes < attn_decode_workspace_bytes(cfg))
+        return fail(ATTN_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes,
+                    attn_decode_workspace_bytes(cfg));
+    if (batch == 0) return ATTN_OK;
+    const int Hkv = cfg->n_kv_heads, G = cfg->n_q_heads / Hkv, S = max_splits(cfg);
+    float *po = (float *)workspace;
+    float *pml = (float *)((char *)workspace + partial_o_bytes(cfg));
+    hipStream_t st = (hipStream_t)stream;
+    attn_split_kernel<<<dim3(S, Hkv, batch), 256, 0, st>>>((const uint16_t *)q, (const uint16_t *)k_cache,
+                                                          (const uint16_t *)v_cache, n_pages, block_table,
+                                                          cfg->max_pages_per_seq, ctx_lens, Hkv, G,
+                                                          scale * kLog2e, po, pml, S);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(ATTN_ERR_HIP, "split kernel launch: %s", hipGetErrorString(e));
+    attn_combine_kernel<<<dim3(G, Hkv, batch), 128, 0, st>>>(po, pml, ctx_lens, cfg->max_pages_per_seq, Hkv, G, S,
+                                                             (uint16_t *)out);
+    e = hipGetLastError();
+    if (e != hipSuccess) return fail(ATTN_ERR_HIP, "combine kernel launch: %s", hipGetErrorString(e));
+    return ATTN_OK;
+}
+
+extern "C" const char *attn_decode_last_error(void) { return attn::g_err; }

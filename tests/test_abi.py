@@ -162,3 +162,80 @@ def test_status_strings(B):
     for s in (0, -1, -2, -3, -4):
         assert B.moe_decode_status_string(s)
     B.lib().moe_decode_free(None)  # NULL is ignored
+
+
+# ---------------------------------------------------------------- decode attention (include/attn_decode.h)
+
+ATTN_HEADER = os.path.join(ROOT, "include", "attn_decode.h")
+
+
+def test_every_attention_symbol_is_exported(B):
+    src = re.sub(r"/\*.*?\*/", "", open(ATTN_HEADER).read(), flags=re.S)
+    names = sorted(set(re.findall(r"\b(attn_decode_\w+)\s*\(", src)))
+    assert names == ["attn_decode_forward", "attn_decode_last_error", "attn_decode_workspace_bytes"]
+    lib = ctypes.CDLL(B.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_attention_workspace_bytes(B):
+    c = B.make_attn_config(64, 4, 24, 128)  # 2048 tokens: 8 splits of 256
+    parts = 24 * 4 * 8 * 16
+    assert B.attn_decode_workspace_bytes(c) == (parts * 128 * 4 + 255) // 256 * 256 + parts * 8
+
+
+@pytest.mark.parametrize(
+    "kw,code",
+    [
+        (dict(n_q_heads=64, n_kv_heads=3), -1),  # not a multiple
+        (dict(n_q_heads=68, n_kv_heads=2), -2),  # 34 query heads per key/value head
+        (dict(n_q_heads=8, n_kv_heads=0), -1),
+        (dict(head_dim=64), -2),
+        (dict(page_size=32), -2),
+        (dict(max_batch=0), -1),
+        (dict(max_batch=5000), -1),
+        (dict(max_pages_per_seq=0), -1),
+    ],
+)
+def test_attention_invalid_configs_rejected(B, kw, code):
+    base = dict(n_q_heads=64, n_kv_heads=4, max_batch=8, max_pages_per_seq=16)
+    base.update(kw)
+    c = B.make_attn_config(**base)
+    assert B.attn_decode_workspace_bytes(c) == 0
+    with pytest.raises(B.MoEDecodeError) as e:
+        B.attn_decode_forward(c, 256, 1 << 20, None, 16, 32, 48, 1, 64, 64, 1, 0.1, 80)
+    assert e.value.status == code
+
+
+@pytest.mark.parametrize(
+    "change,needle",
+    [
+        (dict(batch=9), "batch"),
+        (dict(scale=0.0), "scale"),
+        (dict(scale=float("nan")), "scale"),
+        (dict(n_pages=0), "n_pages"),
+        (dict(q=0), "q is NULL"),
+        (dict(k_cache=24), "k_cache must be 16-byte aligned"),
+        (dict(out=16), "alias"),
+        (dict(block_table=0), "block_table"),
+        (dict(ctx_lens=2), "ctx_lens"),
+        (dict(workspace=0), "workspace"),
+        (dict(workspace_bytes=100), "workspace of 100 bytes"),
+    ],
+)
+def test_attention_forward_validates_before_launch(B, change, needle):
+    """Every check fails before a launch: no GPU is touched (the pointers are fake)."""
+    c = B.make_attn_config(64, 4, 8, 16)
+    args = dict(workspace=256, workspace_bytes=B.attn_decode_workspace_bytes(c), q=16, k_cache=32, v_cache=48,
+                n_pages=4, block_table=64, ctx_lens=68, batch=8, scale=0.1, out=80)
+    args.update(change)
+    with pytest.raises(B.MoEDecodeError) as e:
+        B.attn_decode_forward(c, args["workspace"], args["workspace_bytes"], None, args["q"], args["k_cache"],
+                              args["v_cache"], args["n_pages"], args["block_table"], args["ctx_lens"], args["batch"],
+                              args["scale"], args["out"])
+    assert needle in str(e.value)
+
+
+def test_attention_zero_batch_is_a_no_op(B):
+    c = B.make_attn_config(64, 4, 8, 16)
+    B.attn_decode_forward(c, 256, B.attn_decode_workspace_bytes(c), None, 16, 32, 48, 4, 64, 68, 0, 0.1, 80)
