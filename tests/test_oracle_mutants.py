@@ -16,6 +16,7 @@ from paper_2609_11133_amd import synth
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "moe_oracle.c")
+ATTN_SRC = os.path.join(ROOT, "oracle", "attn_oracle.c")  # linked unchanged: the loader binds its symbol too
 INIT = os.path.join(ROOT, "oracle", "__init__.py")
 
 MUTANTS = {
@@ -50,7 +51,7 @@ def build_variant(tmp_path, name, old, new):
     path.write_text(src.replace(old, new))
     so = tmp_path / f"lib{name}.so"
     subprocess.check_call(["gcc", "-O2", "-fPIC", "-shared", "-std=c11", "-pthread", "-ffp-contract=off", "-o",
-                           str(so), str(path), "-lm"])
+                           str(so), str(path), ATTN_SRC, "-lm"])
     spec = importlib.util.spec_from_file_location(f"oracle_{name}", INIT)
     mod = importlib.util.module_from_spec(spec)
     spec.loader.exec_module(mod)
