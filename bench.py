@@ -88,6 +88,8 @@ def parse():
     ap.add_argument("--stack", action="store_true",
                     help="also time the stack of 12 distinct 480B-shaped layers decoded back to back, T = 1..256")
     ap.add_argument("--stack-steps", type=int, default=20)
+    ap.add_argument("--screen-min-tokens", type=int, default=0,
+                    help="tokens per step from which routing screens the logits (0: library default, -1: never)")
     ap.add_argument("--mstar", type=int, default=0,
                     help="tokens per expert from which MFMA tiles are used (0: library default, -1: GEMV only)")
     return ap.parse_args()
@@ -165,7 +167,7 @@ def run_stack(args, dev):
                        W.to_device(hl.scales, dev)))
         del hl
         print(f"[stack] layer {li} resident ({time.time() - t0:.0f} s)", file=sys.stderr, flush=True)
-    m = B.MoEDecode(W.binding_config(cfg, max(cfg.tokens), args.mstar), device=dev)
+    m = B.MoEDecode(W.binding_config(cfg, max(cfg.tokens), args.mstar, args.screen_min_tokens), device=dev)
     stream = torch.cuda.current_stream(dev)
     Be = cfg.expert_bytes()
     out = {}
@@ -313,7 +315,7 @@ def main():
     scs = [sc0] + [sc0.clone() for _ in range(copies - 1)]
     setup_s = time.time() - t0
 
-    m = B.MoEDecode(W.binding_config(cfg, Tmax, args.mstar), device=dev)
+    m = B.MoEDecode(W.binding_config(cfg, Tmax, args.mstar, args.screen_min_tokens), device=dev)
     stream = torch.cuda.current_stream(dev)
     Be = cfg.expert_bytes()
     results = {}

@@ -96,7 +96,14 @@ typedef struct moe_decode_config {
                                 MFMA tiles, below it on the GEMV path; 0 = library default
                                 (1: MFMA for every expert, the faster path on MI355X at
                                 every measured token count), negative = never */
-    int32_t reserved[7];     /* must be zero */
+    int32_t screen_min_tokens; /* a forward step with at least this many tokens screens the
+                                router logits: bf16 matrix-core sums give every logit a
+                                rigorous bracket, and only the experts whose bracket can
+                                reach the top k get the exact logit (the selection is
+                                the same); needs bf16 x and router_w and H a multiple of
+                                256.  0 = library default (the smallest T with
+                                T*E*H >= 2^26 multiply-adds), negative = never */
+    int32_t reserved[6];     /* must be zero */
 } moe_decode_config;
 
 typedef struct moe_decode_stats {
@@ -104,6 +111,8 @@ typedef struct moe_decode_stats {
     int32_t n_active;        /* experts with at least one token in the last forward */
     int32_t n_active_mfma;   /* of those, experts that ran on MFMA tiles */
     int32_t n_fallback;      /* router logits that needed the exact (double-double) path */
+    int32_t n_exact_logits;  /* router logits computed exactly (T*E unless screened) */
+    int32_t route_screened;  /* 1 if the last forward screened the router logits */
     int64_t active_weight_bytes; /* unique expert weight + scale bytes the step streamed */
 } moe_decode_stats;
 

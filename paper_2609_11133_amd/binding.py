@@ -33,7 +33,8 @@ class moe_decode_config(ctypes.Structure):
         ("router_dtype", ctypes.c_int32),
         ("wfmt", ctypes.c_int32),
         ("mfma_min_tokens", ctypes.c_int32),
-        ("reserved", ctypes.c_int32 * 7),
+        ("screen_min_tokens", ctypes.c_int32),
+        ("reserved", ctypes.c_int32 * 6),
     ]
 
 
@@ -43,6 +44,8 @@ class moe_decode_stats(ctypes.Structure):
         ("n_active", ctypes.c_int32),
         ("n_active_mfma", ctypes.c_int32),
         ("n_fallback", ctypes.c_int32),
+        ("n_exact_logits", ctypes.c_int32),
+        ("route_screened", ctypes.c_int32),
         ("active_weight_bytes", ctypes.c_int64),
     ]
 
@@ -130,10 +133,12 @@ def _check(status: int, handle=None):
 
 
 def make_config(hidden, n_experts, inter, max_topk, max_tokens, act_dtype=MOE_DTYPE_BF16,
-                router_dtype=MOE_DTYPE_BF16, wfmt=MOE_WFMT_FP8_E4M3_B128, mfma_min_tokens=0) -> moe_decode_config:
+                router_dtype=MOE_DTYPE_BF16, wfmt=MOE_WFMT_FP8_E4M3_B128, mfma_min_tokens=0,
+                screen_min_tokens=0) -> moe_decode_config:
     c = moe_decode_config()
     c.hidden, c.n_experts, c.inter, c.max_topk, c.max_tokens = hidden, n_experts, inter, max_topk, max_tokens
     c.act_dtype, c.router_dtype, c.wfmt, c.mfma_min_tokens = act_dtype, router_dtype, wfmt, mfma_min_tokens
+    c.screen_min_tokens = screen_min_tokens
     return c
 
 

@@ -46,6 +46,12 @@ size_t carve_workspace(int H, int E, int I, int kmax, int Tmax, int wfmt, void *
         w.he_hi = (uint8_t *)take(P * I / 32);
         w.he_lo = (uint8_t *)take(P * I / 32);
     }
+    w.ks_max = screen_ks_max(H, E, Tmax);
+    if (w.ks_max) {
+        w.part = take((size_t)16 * w.ks_max * Tmax * E);
+        w.xmax = (float *)take(sizeof(float) * (size_t)w.ks_max * Tmax);
+        w.wmax = (float *)take(sizeof(float) * (size_t)w.ks_max * E);
+    }
     w.bytes = off;
     if (ws) *ws = w;
     return off;
@@ -60,6 +66,7 @@ struct moe_decode_s {
     Layer L;
     Workspace ws;
     int mstar;  // MFMA threshold in tokens per expert (<= 0: GEMV only)
+    int screen_min;  // screened routing from this many tokens per step (INT32_MAX: never)
     int synced;  // routing counters zeroed (by the first call on this handle)
     hipStream_t last_stream;
     int last_T;
@@ -86,7 +93,7 @@ static const int kDefaultMfmaMinTokens = 1;
 static moe_status check_config(const moe_decode_config *c, char *err)
 {
     if (!c) FAIL(err, MOE_ERR_INVALID, "config is NULL");
-    for (int i = 0; i < 7; ++i)
+    for (int i = 0; i < 6; ++i)
         if (c->reserved[i] != 0) FAIL(err, MOE_ERR_INVALID, "config.reserved[%d] must be zero", i);
     if (c->wfmt != MOE_WFMT_FP8_E4M3_B128 && c->wfmt != MOE_WFMT_MXFP4_E2M1_B32 && c->wfmt != MOE_WFMT_NVFP4_E2M1_B16)
         FAIL(err, MOE_ERR_INVALID, "unknown weight format %d", c->wfmt);
@@ -171,6 +178,15 @@ moe_status moe_decode_init(const moe_decode_config *cfg, void *workspace, size_t
     carve_workspace(cfg->hidden, cfg->n_experts, cfg->inter, cfg->max_topk, cfg->max_tokens, cfg->wfmt, workspace,
                     &h->ws);
     h->mstar = cfg->mfma_min_tokens == 0 ? kDefaultMfmaMinTokens : (cfg->mfma_min_tokens < 0 ? 0 : cfg->mfma_min_tokens);
+    {
+        // screened routing: bf16 x and router, H a multiple of 256 (ks_max > 0), E <= 1024
+        const long work = (long)cfg->n_experts * cfg->hidden;
+        const int dflt = (int)((kScreenMinMacs + work - 1) / work);
+        const bool able = h->ws.ks_max > 0 && h->L.act_bf16 && h->L.router_bf16;
+        h->screen_min = !able || cfg->screen_min_tokens < 0 ? INT32_MAX
+                        : cfg->screen_min_tokens == 0    ? dflt
+                                                         : cfg->screen_min_tokens;
+    }
     h->synced = 0;
     h->last_stream = nullptr;
     h->last_T = -1;
@@ -259,7 +275,13 @@ static RouteParams route_params(moe_decode_t h, const void *x, int T, int k, con
     P.xs_lo = w.xs_lo;
     P.xe_hi = w.xe_hi;
     P.xe_lo = w.xe_lo;
+    P.part = w.part;
+    P.xmax = w.xmax;
+    P.wmax = w.wmax;
+    P.ks_max = w.ks_max;
+    P.Tmax = h->cfg.max_tokens;
     P.mstar = h->mstar;
+    P.screen = T >= h->screen_min ? 1 : 0;
     P.do_group = group ? 1 : 0;
     P.max_chunks = max_mfma_chunks(h->L.E, h->cfg.max_tokens, h->cfg.max_topk);
     return P;
@@ -345,6 +367,8 @@ moe_status moe_decode_get_stats(moe_decode_t h, moe_decode_stats *out, int32_t *
     out->n_active = head[mi.n_active()];
     out->n_active_mfma = head[mi.n_mfma()];
     out->n_fallback = head[mi.n_fallback()];
+    out->n_exact_logits = head[mi.n_exact()];
+    out->route_screened = head[mi.screened()];
     out->active_weight_bytes = (int64_t)out->n_active * (int64_t)(h->L.expert_w_bytes + h->L.expert_s_bytes);
     if (counts_host)
         HIPCHECK(h, hipMemcpy(counts_host, h->ws.meta + mi.counts(), sizeof(int32_t) * h->L.E, hipMemcpyDeviceToHost));

@@ -23,6 +23,9 @@ struct Workspace {
     uint8_t *hs_hi, *hs_lo;  // [Tmax*kmax][I] 2-term FP8 split of h (MFMA path)
     uint8_t *he_hi, *he_lo;  // [Tmax*kmax][I/32]
     __bf16 *hb;              // [Tmax*kmax][I] bf16 SwiGLU activations (NVFP4 MFMA path)
+    void *part;              // screened routing: [ks_max][Tmax][E] (sum x*w, sum |x*w|) fp64 pairs
+    float *xmax, *wmax;      // [ks_max][Tmax], [ks_max][E] slice maxima of |x| and |w|
+    int ks_max;              // K slices the screened routing may use (0: path off)
     size_t bytes;
 };
 
@@ -38,6 +41,8 @@ struct MetaIdx {
     __host__ __device__ int n_mfma() const { return 2; }
     __host__ __device__ int n_fallback() const { return 3; }
     __host__ __device__ int n_mfma_chunks() const { return 4; }
+    __host__ __device__ int n_exact() const { return 5; }   // router logits computed exactly
+    __host__ __device__ int screened() const { return 6; }  // 1: the step screened its logits
     __host__ __device__ int counts() const { return 8; }        // [E]
     __host__ __device__ int offsets() const { return 8 + E; }   // [E+1]
     __host__ __device__ int gemv_rec() const { return ((8 + 2 * E + 1) + 3) & ~3; }  // int4 [E]
@@ -48,6 +53,23 @@ struct MetaIdx {
 __host__ __device__ inline int max_mfma_chunks(int E, int Tmax, int kmax) { return E + (Tmax * kmax + 31) / 32; }
 
 constexpr int kMfmaChunk = 32;      // tokens per MFMA pass (two 16-column tiles)
+// Screened routing by default from T*E*H >= 2^26 multiply-adds of exact logits: below
+// it the fixed costs of the extra pass outweigh the logits it saves.
+constexpr long kScreenMinMacs = 1L << 26;
+constexpr int kCandCounterOff = 32;  // int32 words from the fallback counter to the candidate counter
+
+// K slices of the screened routing's partial sums: at most 16 and H/256, and the
+// partials at most 4 Mi fp64 pairs (64 MB); 0 when H is not a multiple of 256.
+constexpr int kScreenMaxKS = 16;
+__host__ __device__ inline int screen_ks_max(int H, int E, int Tmax)
+{
+    if (H % 256) return 0;
+    long ks = H / 256;
+    ks = ks < kScreenMaxKS ? ks : kScreenMaxKS;
+    const long cap = (1L << 22) / ((long)Tmax * E);
+    ks = ks < cap ? ks : cap;
+    return ks < 1 ? 1 : (int)ks;
+}
 constexpr int kCounterStride = 64;  // int32 words between routing counters (256 bytes)
 
 // The FP8 split regions are carved for FP8 and MXFP4 weights, hb for NVFP4 weights
@@ -76,9 +98,13 @@ struct RouteParams {
     int32_t *meta, *slot_of, *tok_of;
     int32_t *cnt_tok, *cnt_all, *fb_acc;
     uint8_t *xs_hi, *xs_lo, *xe_hi, *xe_lo;  // NULL: no activation split
+    void *part;                               // screened routing buffers (Workspace)
+    float *xmax, *wmax;
+    int ks_max, Tmax;
     int mstar;
     int do_group;
     int max_chunks;
+    int screen;  // 1: screened routing for this step (forward with grouping only)
 };
 
 // ---- launchers (all enqueue on `st`, return hipGetLastError())

@@ -106,7 +106,7 @@ __device__ inline void load8<float>(const float *p, double (&v)[8])
 // Exact (double-double) logit of one (token, expert) pair, computed by one wave: the
 // slow path taken when the fp64 sum cannot certify its fp32 rounding.
 template <typename XT, typename WT>
-__device__ inline float wave_logit_exact(const XT *__restrict__ xr, const WT *__restrict__ wrow, double b, int H,
+__device__ __attribute__((always_inline)) inline float wave_logit_exact(const XT *__restrict__ xr, const WT *__restrict__ wrow, double b, int H,
                                          int lane)
 {
     double hi = 0.0, lo = 0.0;
@@ -198,7 +198,8 @@ __device__ inline double wave_sum_f64(double v)
 __device__ inline float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ inline float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
-// Canonical logits of one token row xr against router rows e0 .. e0+ne-1 (ne <= kEPW),
+// Canonical logits of one token row xr against router rows e0 .. e0+ne-1 (ne <= EPW),
+// or the rows elist[0 .. ne-1],
 // computed by one wave and written to lrow[e].  The lane's inputs are loaded once per
 // segment and reused for every expert; the next expert's router row is in flight
 // while the current one accumulates.  Returns the number of fallbacks taken.
@@ -215,9 +216,13 @@ __device__ inline float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0
 // EPW is the wave's expert capacity (ne <= EPW) and SEG the 8-input chunks per lane
 // held at once: one expert per wave loads a 4096-input row in one round trip.
 template <typename XT, typename WT, int EPW, int SEG>
-__device__ inline int wave_logits(const XT *__restrict__ xr, const WT *__restrict__ wr, const float *bias, int H,
-                                  int e0, int ne, int lane, float *lrow)
+__device__ __attribute__((always_inline)) inline int wave_logits(const XT *__restrict__ xr, const WT *__restrict__ wr, const float *bias, int H,
+                                  int e0, int ne, int lane, float *lrow, const int *elist = nullptr)
 {
+    // expert i of the call: elist[i] if a list is given, else e0 + i
+    int ex[EPW];
+#pragma unroll
+    for (int i = 0; i < EPW; ++i) ex[i] = elist ? elist[i < ne ? i : 0] : e0 + (i < ne ? i : 0);
     constexpr bool kBf16 = sizeof(XT) == 2 && sizeof(WT) == 2;
     const int nck = (H + 511) / 512;  // chunks of the lane with the most
     // Two accumulators per expert (even and odd chunks): each sums at most
@@ -261,7 +266,7 @@ __device__ inline int wave_logits(const XT *__restrict__ xr, const WT *__restric
         for (int i = 0; i < EPW; ++i)
 #pragma unroll
             for (int j = 0; j < SEG; ++j)
-                ld_chunk<WT>(wr + (size_t)(e0 + (i < ne ? i : 0)) * H + off[j], wc[i][j]);
+                ld_chunk<WT>(wr + (size_t)ex[i] * H + off[j], wc[i][j]);
 #pragma unroll
         for (int i = 0; i < EPW; ++i) {
             if (i < ne) {
@@ -290,7 +295,7 @@ __device__ inline int wave_logits(const XT *__restrict__ xr, const WT *__restric
         if (i < ne) {
             const double si = wave_sum_f64(s[i][0] + s[i][1]);
             const double ai = wave_sum_f64(kBf16 ? ((double)a32[i][0] + (double)a32[i][1]) * infl : a[i][0] + a[i][1]);
-            const int e = e0 + i;
+            const int e = ex[i];
             const double b = bias ? (double)bias[e] : 0.0;
             const double slack = kBf16 ? (double)H * 0x1p-148 : 0.0;
             float r;
@@ -441,15 +446,17 @@ __device__ inline uint64_t wave_max64(uint64_t v)
 // remaining key; lane j keeps choice j.  Weights are the softmax of the selected logits in
 // fp32 relative to the largest, normalised by their butterfly sum, which every lane
 // forms from the same pairs.
-template <int V>
-__device__ inline void wave_topk(const float *__restrict__ l, int E, int k, int32_t *ids, float *wts,
-                                 int32_t *ids_user, float *wts_user, int lane)
+template <int V, bool MASK>
+__device__ __attribute__((always_inline)) inline void wave_topk(const float *__restrict__ l, int E, int k, int32_t *ids, float *wts,
+                                 int32_t *ids_user, float *wts_user, int lane, const uint32_t *cand)
 {
     uint64_t key[V];
 #pragma unroll
     for (int v = 0; v < V; ++v) {
         const int e = 64 * v + lane;
-        key[v] = e < E ? ((uint64_t)ordered_bits(ld_dev(&l[e])) << 32) | (uint32_t)(~(uint32_t)e) : 0;
+        bool in = e < E;
+        if constexpr (MASK) in = in && ((cand[e >> 5] >> (e & 31)) & 1u);
+        key[v] = in ? ((uint64_t)ordered_bits(ld_dev(&l[e])) << 32) | (uint32_t)(~(uint32_t)e) : 0;
     }
     uint64_t mine = 0;  // lane j < k: key of choice j
     for (int j = 0; j < k; ++j) {
@@ -476,19 +483,22 @@ __device__ inline void wave_topk(const float *__restrict__ l, int E, int k, int3
     }
 }
 
-__device__ inline void token_topk(const float *__restrict__ l, int E, int k, int32_t *ids, float *wts,
-                                  int32_t *ids_user, float *wts_user, int lane)
+// MASK: only the experts of the bitmask `cand` may be selected (the others' logits need
+// not be valid).
+template <bool MASK = false>
+__device__ __attribute__((always_inline)) inline void token_topk(const float *__restrict__ l, int E, int k, int32_t *ids, float *wts,
+                                  int32_t *ids_user, float *wts_user, int lane, const uint32_t *cand = nullptr)
 {
     if (E <= 64)
-        wave_topk<1>(l, E, k, ids, wts, ids_user, wts_user, lane);
+        wave_topk<1, MASK>(l, E, k, ids, wts, ids_user, wts_user, lane, cand);
     else if (E <= 128)
-        wave_topk<2>(l, E, k, ids, wts, ids_user, wts_user, lane);
+        wave_topk<2, MASK>(l, E, k, ids, wts, ids_user, wts_user, lane, cand);
     else if (E <= 256)
-        wave_topk<4>(l, E, k, ids, wts, ids_user, wts_user, lane);
+        wave_topk<4, MASK>(l, E, k, ids, wts, ids_user, wts_user, lane, cand);
     else if (E <= 512)
-        wave_topk<8>(l, E, k, ids, wts, ids_user, wts_user, lane);
+        wave_topk<8, MASK>(l, E, k, ids, wts, ids_user, wts_user, lane, cand);
     else
-        wave_topk<16>(l, E, k, ids, wts, ids_user, wts_user, lane);
+        wave_topk<16, MASK>(l, E, k, ids, wts, ids_user, wts_user, lane, cand);
 }
 
 // ------------------------------------------------------------------ fused routing kernel
@@ -516,87 +526,46 @@ struct RouteArgs {
     uint8_t *xs_hi, *xs_lo, *xe_hi, *xe_lo;  // activation split (NULL: MFMA path off)
     int T, E, H, k, epw, bpt, mstar, do_group, max_chunks;
     int id_cache;  // the grouping keeps the choices in LDS (sized by the launch)
+    // screened routing (large T): per K slice ks, partial sums part[ks][t][e] =
+    // (sum x*w, sum |x*w|) and the slice's max |x[t,.]|, max |w[e,.]|
+    double2 *part;
+    float *xmax, *wmax;
+    int KS, Tmax;
 };
 
-template <typename XT, typename WT>
-__global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
+// The 2-term FP8 split of token t's activations (groups of 32 inputs, see fp8split.h),
+// groups first, first + stride, ... written by the calling thread.
+template <typename XT>
+__device__ __attribute__((always_inline)) inline void write_split(const RouteArgs &A, const XT *xr, int t, int first, int stride)
 {
-    extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
-    __shared__ int s_flag;
-    __shared__ int s_scan[16];
-    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
-    const int t = blockIdx.x / A.bpt;
-    const int q = blockIdx.x % A.bpt;
-    const int E = A.E, H = A.H;
-    const XT *xr = (const XT *)A.x + (size_t)t * H;
-
-    // 1. logits of this workgroup's experts
-    {
-        const int e0 = (q * 4 + wave) * A.epw;
-        const int ne = min(E, e0 + A.epw) - e0;
-        if (ne > 0) {
-            const WT *wr = (const WT *)A.wr;
-            float *lrow = A.logits + (size_t)t * E;
-            // one expert per wave: no loads for empty expert slots, and a row of up to
-            // 4096 bf16 inputs in one round trip
-            int nfb;
-            if (A.epw > 1)
-                nfb = wave_logits<XT, WT, kEPW, 4>(xr, wr, A.bias, H, e0, ne, lane, lrow);
-            else if (sizeof(XT) == 2 && H <= 8 * 512)
-                nfb = wave_logits<XT, WT, 1, 8>(xr, wr, A.bias, H, e0, ne, lane, lrow);
-            else
-                nfb = wave_logits<XT, WT, 1, 4>(xr, wr, A.bias, H, e0, ne, lane, lrow);
-            if (lane == 0 && nfb) atomicAdd(A.fb_acc, nfb);
-        }
+    const int H = A.H, G = H / 32;
+    for (int g = first; g < G; g += stride) {
+        float v[32], res[32];
+        uint32_t qh[8], ql[8];
+        load32_f32<XT>(xr + g * 32, v);
+        const int ch = exp_for_group(amax_of(v));
+        split_hi(v, ch, qh, res);
+        const int cl = exp_for_group(amax_of(res));
+        split_lo(res, cl, ql);
+        const size_t o = (size_t)t * H + g * 32;
+        reinterpret_cast<uint4 *>(A.xs_hi + o)[0] = make_uint4(qh[0], qh[1], qh[2], qh[3]);
+        reinterpret_cast<uint4 *>(A.xs_hi + o)[1] = make_uint4(qh[4], qh[5], qh[6], qh[7]);
+        reinterpret_cast<uint4 *>(A.xs_lo + o)[0] = make_uint4(ql[0], ql[1], ql[2], ql[3]);
+        reinterpret_cast<uint4 *>(A.xs_lo + o)[1] = make_uint4(ql[4], ql[5], ql[6], ql[7]);
+        A.xe_hi[(size_t)t * (H / 32) + g] = (uint8_t)ch;
+        A.xe_lo[(size_t)t * (H / 32) + g] = (uint8_t)cl;
     }
-    // Publish this workgroup's logits, then count it; the last workgroup of the token
-    // goes on.
-    wait_stores();
-    __syncthreads();
-    if (threadIdx.x == 0) s_flag = atomicAdd(&A.cnt_tok[t * kCounterStride], 1) == A.bpt - 1;
-    __syncthreads();
-    if (!s_flag) return;
+}
 
-    // 2. last workgroup of token t: top-k softmax in wave 0 while waves 1-3 write the
-    // token's 2-term activation split when the MFMA path is on (groups of 32 inputs)
-    if (wave == 0) {
-        token_topk(A.logits + (size_t)t * E, E, A.k, A.ids + (size_t)t * A.k, A.wts + (size_t)t * A.k,
-                   A.ids_user ? A.ids_user + (size_t)t * A.k : nullptr,
-                   A.wts_user ? A.wts_user + (size_t)t * A.k : nullptr, lane);
-    } else if (A.xs_hi) {
-        {
-            const int G = H / 32;
-            for (int g = threadIdx.x - kWave; g < G; g += blockDim.x - kWave) {
-                float v[32], res[32];
-                uint32_t qh[8], ql[8];
-                load32_f32<XT>(xr + g * 32, v);
-                const int ch = exp_for_group(amax_of(v));
-                split_hi(v, ch, qh, res);
-                const int cl = exp_for_group(amax_of(res));
-                split_lo(res, cl, ql);
-                const size_t o = (size_t)t * H + g * 32;
-                reinterpret_cast<uint4 *>(A.xs_hi + o)[0] = make_uint4(qh[0], qh[1], qh[2], qh[3]);
-                reinterpret_cast<uint4 *>(A.xs_hi + o)[1] = make_uint4(qh[4], qh[5], qh[6], qh[7]);
-                reinterpret_cast<uint4 *>(A.xs_lo + o)[0] = make_uint4(ql[0], ql[1], ql[2], ql[3]);
-                reinterpret_cast<uint4 *>(A.xs_lo + o)[1] = make_uint4(ql[4], ql[5], ql[6], ql[7]);
-                A.xe_hi[(size_t)t * (H / 32) + g] = (uint8_t)ch;
-                A.xe_lo[(size_t)t * (H / 32) + g] = (uint8_t)cl;
-            }
-        }
-    }
-    if (threadIdx.x == 0) st_dev(&A.cnt_tok[t * kCounterStride], 0);
-    if (!A.do_group) return;
-    wait_stores();
-    __syncthreads();
-    if (threadIdx.x == 0) s_flag = atomicAdd(A.cnt_all, 1) == A.T - 1;
-    __syncthreads();
-    if (!s_flag) return;
-
-    // 3. last token: group the T*k (token, choice) pairs by expert.  LDS holds one bit
-    // per (expert, token): expert e's tokens in token order.  counts = popcounts,
-    // offsets = exclusive prefix sum, slot of pair (t, j) choosing e = offsets[e] +
-    // (number of earlier tokens that chose e).  Experts with at least `mstar` tokens
-    // go to the MFMA list, the others to the GEMV list, each in expert order.
+// Last token of a step: group the T*k (token, choice) pairs by expert.  LDS holds one
+// bit per (expert, token): expert e's tokens in token order.  counts = popcounts,
+// offsets = exclusive prefix sum, slot of pair (t, j) choosing e = offsets[e] +
+// (number of earlier tokens that chose e).  Experts with at least `mstar` tokens go
+// to the MFMA list, the others to the GEMV list, each in expert order.  All threads
+// of the workgroup call it.
+__device__ __attribute__((always_inline)) inline void group_pairs(const RouteArgs &A, uint32_t *lds, int *s_scan)
+{
+    const int E = A.E;
     const int T = A.T, k = A.k, P = T * k;
     const int W = (T + 31) / 32;
     uint32_t *mask = lds;                        // [E][W]
@@ -604,8 +573,11 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
     int32_t *idc = offs + E;                     // [P] when the launch sized LDS for it: the choices, read once
     const bool cached = A.id_cache != 0;
     const MetaIdx mi{E, A.max_chunks};
-    int nfb_total = 0;
-    if (threadIdx.x == 0) nfb_total = atomicExch(A.fb_acc, 0);  // in flight during the grouping
+    int nfb_total = 0, n_exact = A.T * E;
+    if (threadIdx.x == 0) {  // in flight during the grouping; each counter is reset by its reader
+        nfb_total = atomicExch(A.fb_acc, 0);
+        if (A.KS) n_exact = atomicExch(A.fb_acc + kCandCounterOff, 0);
+    }
     for (int i = threadIdx.x; i < E * W; i += blockDim.x) mask[i] = 0u;
     __syncthreads();
     // this thread's choices, eight loads in flight at a time
@@ -678,6 +650,8 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
         A.meta[mi.n_mfma()] = tot[2];
         A.meta[mi.n_fallback()] = nfb_total;
         A.meta[mi.n_mfma_chunks()] = tot[3];
+        A.meta[mi.n_exact()] = n_exact;
+        A.meta[mi.screened()] = A.KS ? 1 : 0;
         st_dev(A.cnt_all, 0);
     }
     __syncthreads();
@@ -689,6 +663,324 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
         A.slot_of[p] = slot;
         A.tok_of[slot] = tt;
     }
+}
+
+template <typename XT, typename WT>
+__global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
+{
+    extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
+    __shared__ int s_flag;
+    __shared__ int s_scan[16];
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+    const int t = blockIdx.x / A.bpt;
+    const int q = blockIdx.x % A.bpt;
+    const int E = A.E, H = A.H;
+    const XT *xr = (const XT *)A.x + (size_t)t * H;
+
+    // 1. logits of this workgroup's experts
+    {
+        const int e0 = (q * 4 + wave) * A.epw;
+        const int ne = min(E, e0 + A.epw) - e0;
+        if (ne > 0) {
+            const WT *wr = (const WT *)A.wr;
+            float *lrow = A.logits + (size_t)t * E;
+            // one expert per wave: no loads for empty expert slots, and a row of up to
+            // 4096 bf16 inputs in one round trip
+            int nfb;
+            if (A.epw > 1)
+                nfb = wave_logits<XT, WT, kEPW, 4>(xr, wr, A.bias, H, e0, ne, lane, lrow);
+            else if (sizeof(XT) == 2 && H <= 8 * 512)
+                nfb = wave_logits<XT, WT, 1, 8>(xr, wr, A.bias, H, e0, ne, lane, lrow);
+            else
+                nfb = wave_logits<XT, WT, 1, 4>(xr, wr, A.bias, H, e0, ne, lane, lrow);
+            if (lane == 0 && nfb) atomicAdd(A.fb_acc, nfb);
+        }
+    }
+    // Publish this workgroup's logits, then count it; the last workgroup of the token
+    // goes on.
+    wait_stores();
+    __syncthreads();
+    if (threadIdx.x == 0) s_flag = atomicAdd(&A.cnt_tok[t * kCounterStride], 1) == A.bpt - 1;
+    __syncthreads();
+    if (!s_flag) return;
+
+    // 2. last workgroup of token t: top-k softmax in wave 0 while waves 1-3 write the
+    // token's 2-term activation split when the MFMA path is on (groups of 32 inputs)
+    if (wave == 0) {
+        token_topk(A.logits + (size_t)t * E, E, A.k, A.ids + (size_t)t * A.k, A.wts + (size_t)t * A.k,
+                   A.ids_user ? A.ids_user + (size_t)t * A.k : nullptr,
+                   A.wts_user ? A.wts_user + (size_t)t * A.k : nullptr, lane);
+    } else if (A.xs_hi) {
+        write_split<XT>(A, xr, t, threadIdx.x - kWave, blockDim.x - kWave);
+    }
+    if (threadIdx.x == 0) st_dev(&A.cnt_tok[t * kCounterStride], 0);
+    if (!A.do_group) return;
+    wait_stores();
+    __syncthreads();
+    if (threadIdx.x == 0) s_flag = atomicAdd(A.cnt_all, 1) == A.T - 1;
+    __syncthreads();
+    if (!s_flag) return;
+
+    group_pairs(A, lds, s_scan);
+}
+
+// ------------------------------------------------------------------ screened routing
+//
+// At large T the exact logits of every (token, expert) pair are the step's largest
+// vector-ALU cost.  Only the top-k of each token need them, so the screened path
+// first brackets every logit and then computes exactly only the experts whose
+// bracket can reach the top k:
+//   screen_kernel    bf16 MFMA sums of x.w and |x|.|w| over 256-input chunks (fp32
+//                    inside a chunk, fp64 across chunks), per K slice;
+//   route_cand_kernel per token: the bracket [lo_e, hi_e] of every canonical logit
+//                    l_e, LB = the k-th largest lo; e can be selected only if
+//                    hi_e >= LB (k experts f have l_f >= lo_f >= LB > hi_e >= l_e
+//                    otherwise); exact logits of those candidates (wave_logits), top-k
+//                    among them by (l desc, e asc), softmax; the last token groups.
+// Bracket.  A chunk of 256 exact products summed in fp32 in any order with any
+// rounding is within g = 256u/(1-256u), u = 2^-23, of its exact sum times the sum of
+// |products|; flushed denormal inputs, products or partial sums add at most
+// 2^-126 (max|x| + max|w| + 2) per product; the fp64 sums across chunks and slices
+// add at most 2^-40 of sum|products|; the bias add one fp64 rounding; the canonical
+// rounding to fp32 at most 2^-23 relative plus 2^-149.
+
+constexpr int kScreenChunk = 256;  // inputs per fp32 MFMA chunk
+constexpr int kMaxE = 1024;
+constexpr int kMaxKS = kScreenMaxKS;  // K slices of the screen at most
+constexpr size_t kCandStaticLds = 12800;  // bytes, at least route_cand_kernel's static LDS
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+constexpr uint32_t kScreenOOR = 0x80000000u;  // buffer offset past every resource: zeros, no request
+
+__device__ inline __amdgpu_buffer_rsrc_t screen_rsrc(const void *base, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// Grid (ceil(T/16), ceil(E/64), KS), 256 threads.  Wave w: experts e0 = 64y + 16w .. +16
+// (MFMA rows: A = router rows), tokens 16x .. +16 (columns: B = x rows), chunks of
+// slice z.  Writes part[z][t][e] = (sum x*w, sum |x*w|) and the slice's max |x|, max |w|.
+__global__ __launch_bounds__(256) void screen_kernel(RouteArgs A)
+{
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r = lane & 15, lg = lane >> 4;
+    const int T = A.T, E = A.E, H = A.H;
+    const int t0 = blockIdx.x * 16, e0 = blockIdx.y * 64 + wave * 16, ks = blockIdx.z;
+    const int nch = H / kScreenChunk, cps = (nch + A.KS - 1) / A.KS;
+    const int c0 = min(nch, ks * cps), c1 = min(nch, c0 + cps);
+    const __amdgpu_buffer_rsrc_t xr = screen_rsrc(A.x, (uint32_t)T * H * 2u);
+    const __amdgpu_buffer_rsrc_t wr = screen_rsrc(A.wr, (uint32_t)E * H * 2u);
+    const uint32_t xo = t0 + r < T ? (uint32_t)(t0 + r) * H * 2u : kScreenOOR;
+    const uint32_t wo = e0 + r < E ? (uint32_t)(e0 + r) * H * 2u : kScreenOOR;
+    double S[4] = {0.0, 0.0, 0.0, 0.0}, Aa[4] = {0.0, 0.0, 0.0, 0.0};
+    u16x2 mx = {0, 0}, mw = {0, 0};
+    u32x4v xa[2][8], wa[2][8];
+    auto load = [&](int b, int c) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t k2 = (uint32_t)(c * kScreenChunk + 32 * i + 8 * lg) * 2u;
+            xa[b][i] = __builtin_amdgcn_raw_buffer_load_b128(xr, xo + k2, 0, 0);
+            wa[b][i] = __builtin_amdgcn_raw_buffer_load_b128(wr, wo + k2, 0, 0);
+        }
+    };
+    auto compute = [&](int b) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f}, acca = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const u32x4v m = {0x7FFF7FFFu, 0x7FFF7FFFu, 0x7FFF7FFFu, 0x7FFF7FFFu};
+            const u32x4v xabs = xa[b][i] & m, wabs = wa[b][i] & m;
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wa[b][i]),
+                                                          __builtin_bit_cast(bf16x8, xa[b][i]), acc, 0, 0, 0);
+            acca = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wabs),
+                                                           __builtin_bit_cast(bf16x8, xabs), acca, 0, 0, 0);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {  // |bf16| bit patterns order like their values
+                mx = __builtin_elementwise_max(mx, __builtin_bit_cast(u16x2, xabs[q]));
+                mw = __builtin_elementwise_max(mw, __builtin_bit_cast(u16x2, wabs[q]));
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            S[j] += (double)acc[j];
+            Aa[j] += (double)acca[j];
+        }
+    };
+    if (c0 < c1) {
+        // chunk c sits in buffer (c - c0) % 2; loads of the next chunk are in flight
+        // while one is multiplied (the last chunk is reloaded past the end)
+        load(0, c0);
+        int c = c0;
+        for (; c + 2 <= c1; c += 2) {
+            load(1, c + 1);
+            compute(0);
+            load(0, min(c + 2, c1 - 1));
+            compute(1);
+        }
+        if (c < c1) compute(0);
+    }
+    // lane: experts e0 + 4lg + j (rows), token t0 + r (column)
+    const int t = t0 + r;
+    if (t < T) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int e = e0 + 4 * lg + j;
+            if (e < E) A.part[((size_t)ks * A.Tmax + t) * E + e] = make_double2(S[j], Aa[j]);
+        }
+    }
+    // slice maxima: lane (r, lg) saw row r of x and of the router block; combine the
+    // four lane groups
+    uint32_t m1 = max((uint32_t)mx.x, (uint32_t)mx.y), m2 = max((uint32_t)mw.x, (uint32_t)mw.y);
+    m1 = max(m1, (uint32_t)__shfl_xor((int)m1, 16));
+    m1 = max(m1, (uint32_t)__shfl_xor((int)m1, 32));
+    m2 = max(m2, (uint32_t)__shfl_xor((int)m2, 16));
+    m2 = max(m2, (uint32_t)__shfl_xor((int)m2, 32));
+    if (lg == 0) {
+        if (t < T) A.xmax[(size_t)ks * A.Tmax + t] = __uint_as_float(m1 << 16);
+        if (e0 + r < E) A.wmax[(size_t)ks * E + e0 + r] = __uint_as_float(m2 << 16);
+    }
+}
+
+// fp32 rounded down / up from fp64.
+__device__ inline float f32_down(double v)
+{
+    float f = (float)v;
+    return (double)f > v ? nextafterf(f, -INFINITY) : f;
+}
+__device__ inline float f32_up(double v)
+{
+    float f = (float)v;
+    return (double)f < v ? nextafterf(f, INFINITY) : f;
+}
+
+// k-th largest of v[0 .. E-1] (E <= 64 V) in the key order of the top-k (value desc,
+// index asc), by one wave: k rounds of the wave argmax.
+template <int V>
+__device__ __attribute__((always_inline)) inline float kth_largest(const float *v, int E, int k, int lane)
+{
+    uint64_t key[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) {
+        const int e = 64 * i + lane;
+        key[i] = e < E ? ((uint64_t)ordered_bits(v[e]) << 32) | (uint32_t)(~(uint32_t)e) : 0;
+    }
+    uint64_t best = 0;
+    for (int j = 0; j < k; ++j) {
+        best = key[0];
+#pragma unroll
+        for (int i = 1; i < V; ++i) best = key[i] > best ? key[i] : best;
+        best = wave_max64(best);
+#pragma unroll
+        for (int i = 0; i < V; ++i) key[i] = key[i] == best ? 0 : key[i];
+    }
+    return from_ordered((uint32_t)(best >> 32));
+}
+
+// One workgroup per token (grid T), 256 threads; dynamic LDS as route_kernel's grouping.
+__global__ __launch_bounds__(256) void route_cand_kernel(RouteArgs A)
+{
+    extern __shared__ __attribute__((aligned(16))) uint32_t lds[];
+    __shared__ float s_lo[kMaxE], s_hi[kMaxE];
+    __shared__ uint32_t s_cand[kMaxE / 32];
+    __shared__ int s_list[kMaxE];
+    __shared__ int s_n, s_flag;
+    __shared__ int s_scan[16];
+    static_assert(sizeof(float) * 2 * kMaxE + sizeof(uint32_t) * (kMaxE / 32) + sizeof(int) * (kMaxE + 2 + 16) <=
+                  kCandStaticLds);
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x >> 6;
+    const int t = blockIdx.x, E = A.E, H = A.H, k = A.k;
+    const uint16_t *xr = (const uint16_t *)A.x + (size_t)t * H;
+    const uint16_t *wr = (const uint16_t *)A.wr;
+
+    // 1. brackets of every expert's canonical logit
+    // (the slices' loads are issued together: KS <= kMaxKS, unrolled and predicated)
+    float xm[kMaxKS];
+#pragma unroll
+    for (int s2 = 0; s2 < kMaxKS; ++s2) xm[s2] = s2 < A.KS ? A.xmax[(size_t)s2 * A.Tmax + t] : 0.f;
+    float mxt = 0.f;
+#pragma unroll
+    for (int s2 = 0; s2 < kMaxKS; ++s2) mxt = fmaxf(mxt, xm[s2]);
+    const double u = 0x1p-23, g = kScreenChunk * u / (1.0 - kScreenChunk * u);
+    for (int e = threadIdx.x; e < E; e += blockDim.x) {
+        double2 d[kMaxKS];
+        float wm[kMaxKS];
+#pragma unroll
+        for (int s2 = 0; s2 < kMaxKS; ++s2) {
+            d[s2] = s2 < A.KS ? A.part[((size_t)s2 * A.Tmax + t) * E + e] : make_double2(0.0, 0.0);
+            wm[s2] = s2 < A.KS ? A.wmax[(size_t)s2 * E + e] : 0.f;
+        }
+        double S = 0.0, Aa = 0.0;
+        float mwe = 0.f;
+#pragma unroll
+        for (int s2 = 0; s2 < kMaxKS; ++s2) {
+            S += d[s2].x;
+            Aa += d[s2].y;
+            mwe = fmaxf(mwe, wm[s2]);
+        }
+        const double flush = (double)H * 0x1p-126 * ((double)mxt + (double)mwe + 2.0);
+        const double Ab = (Aa * (1.0 + 0x1p-40) + flush) / (1.0 - g);
+        const double Sb = S + (A.bias ? (double)A.bias[e] : 0.0);
+        const double dsum = (g + 0x1p-40) * Ab + flush;
+        const double D = dsum + fabs(Sb) * 0x1p-52 + (fabs(Sb) + dsum) * 0x1p-23 + 0x1p-149;
+        s_lo[e] = f32_down(Sb - D);
+        s_hi[e] = f32_up(Sb + D);
+    }
+    for (int i = threadIdx.x; i < kMaxE / 32; i += blockDim.x) s_cand[i] = 0u;
+    __syncthreads();
+
+    // 2. wave 0: LB = k-th largest lower bound, the candidates hi >= LB in expert
+    // order; waves 1-3: the token's activation split (MFMA path)
+    if (wave == 0) {
+        const int V = (E + 63) / 64;
+        const float LB = V <= 1   ? kth_largest<1>(s_lo, E, k, lane)
+                         : V <= 2 ? kth_largest<2>(s_lo, E, k, lane)
+                         : V <= 4 ? kth_largest<4>(s_lo, E, k, lane)
+                         : V <= 8 ? kth_largest<8>(s_lo, E, k, lane)
+                                  : kth_largest<16>(s_lo, E, k, lane);
+        int n = 0;
+        for (int v = 0; v < V; ++v) {
+            const int e = 64 * v + lane;
+            const bool c = e < E && !(s_hi[e] < LB);  // a NaN bracket or LB keeps e: n >= k always
+            const uint64_t bal = __ballot(c);
+            if (c) {
+                s_list[n + __popcll(bal & ((1ull << lane) - 1ull))] = e;
+                atomicOr(&s_cand[e >> 5], 1u << (e & 31));
+            }
+            n += __popcll(bal);
+        }
+        if (lane == 0) {
+            s_n = n;
+            atomicAdd(A.fb_acc + kCandCounterOff, n);
+        }
+    } else if (A.xs_hi) {
+        write_split<uint16_t>(A, xr, t, threadIdx.x - kWave, blockDim.x - kWave);
+    }
+    __syncthreads();
+
+    // 3. exact canonical logits of the candidates: an even share per wave, up to kEPW
+    // router rows in flight per call; they go to LDS over the lower bounds, which are
+    // no longer needed
+    float *lrow = s_lo;
+    int nfb = 0;
+    const int n = s_n, per = (n + 3) / 4, i0 = wave * per, i1 = min(n, i0 + per);
+    for (int i = i0; i < i1; i += kEPW)
+        nfb += wave_logits<uint16_t, uint16_t, kEPW, 4>(xr, wr, A.bias, H, 0, min(kEPW, i1 - i), lane, lrow, s_list + i);
+    if (lane == 0 && nfb) atomicAdd(A.fb_acc, nfb);
+    __syncthreads();
+
+    // 4. top-k among the candidates, softmax of the selected logits
+    if (wave == 0)
+        token_topk<true>(lrow, E, k, A.ids + (size_t)t * k, A.wts + (size_t)t * k,
+                   A.ids_user ? A.ids_user + (size_t)t * k : nullptr, A.wts_user ? A.wts_user + (size_t)t * k : nullptr,
+                   lane, s_cand);
+    wait_stores();
+    __syncthreads();
+    if (threadIdx.x == 0) s_flag = atomicAdd(A.cnt_all, 1) == A.T - 1;
+    __syncthreads();
+    if (!s_flag) return;
+    group_pairs(A, lds, s_scan);
 }
 
 __global__ void zero_kernel(int32_t *p, int n)
@@ -739,12 +1031,31 @@ hipError_t launch_route(const Layer &L, const RouteParams &P, hipStream_t st)
     A.mstar = P.mstar;
     A.do_group = P.do_group;
     A.max_chunks = P.max_chunks;
+    A.part = (double2 *)P.part;
+    A.xmax = P.xmax;
+    A.wmax = P.wmax;
+    A.Tmax = P.Tmax;
+    A.KS = 0;
     const int W = (P.T + 31) / 32;
     // grouping LDS: bitmasks [E][W] and offsets [E], plus the choices [T*k] while the
     // whole stays within 64 KiB
     const size_t base_words = (size_t)L.E * W + L.E, pairs = (size_t)P.T * P.k;
     A.id_cache = P.do_group && (base_words + pairs) * sizeof(uint32_t) <= 65536 ? 1 : 0;
     const size_t lds = P.do_group ? sizeof(uint32_t) * (base_words + (A.id_cache ? pairs : 0)) : 0;
+    // screened routing: bf16 activations and router, H a multiple of 256, enough work
+    if (P.do_group && P.screen && L.act_bf16 && L.router_bf16 && P.ks_max > 0 && L.E <= kMaxE) {
+        const int tiles = (P.T + 15) / 16, groups = (L.E + 63) / 64;
+        const int waves = tiles * groups * 4;
+        int ks = (2048 + waves - 1) / waves;  // about two waves per SIMD
+        ks = ks < 1 ? 1 : (ks > P.ks_max ? P.ks_max : ks);
+        A.KS = ks;
+        // route_cand_kernel's static arrays take about 12.3 KiB: keep the total within 64 KiB
+        A.id_cache = (base_words + pairs) * sizeof(uint32_t) + kCandStaticLds <= 65536 ? 1 : 0;
+        const size_t lds_c = sizeof(uint32_t) * (base_words + (A.id_cache ? pairs : 0));
+        screen_kernel<<<dim3(tiles, groups, ks), 256, 0, st>>>(A);
+        route_cand_kernel<<<dim3(P.T), 256, lds_c, st>>>(A);
+        return hipGetLastError();
+    }
     dim3 grid(P.T * bpt), block(256);
     if (L.act_bf16 && L.router_bf16)
         route_kernel<uint16_t, uint16_t><<<grid, block, lds, st>>>(A);

@@ -239,3 +239,17 @@ def test_attention_forward_validates_before_launch(B, change, needle):
 def test_attention_zero_batch_is_a_no_op(B):
     c = B.make_attn_config(64, 4, 8, 16)
     B.attn_decode_forward(c, 256, B.attn_decode_workspace_bytes(c), None, 16, 32, 48, 4, 64, 68, 0, 0.1, 80)
+
+
+def test_struct_sizes_match_header(B):
+    """The ctypes mirrors of the C structs: 16 int32 config words, stats of 6 int32 + int64."""
+    import ctypes
+
+    assert ctypes.sizeof(B.moe_decode_config) == 64
+    assert ctypes.sizeof(B.moe_decode_stats) == 32
+    assert B.moe_decode_stats.active_weight_bytes.offset == 24
+    c = cfg(B)
+    c.screen_min_tokens = -1
+    assert B.moe_decode_workspace_bytes(c) > 0
+    c.screen_min_tokens = 7
+    assert B.moe_decode_workspace_bytes(c) > 0

@@ -39,11 +39,11 @@ def dev():
 
 
 class Run:
-    def __init__(self, cfg, hl, dev, max_tokens, mfma_min_tokens=0):
+    def __init__(self, cfg, hl, dev, max_tokens, mfma_min_tokens=0, screen_min_tokens=0):
         from paper_2609_11133_amd import binding as B
 
         self.cfg, self.hl, self.dev = cfg, hl, dev
-        self.m = B.MoEDecode(W.binding_config(cfg, max_tokens, mfma_min_tokens), device=dev)
+        self.m = B.MoEDecode(W.binding_config(cfg, max_tokens, mfma_min_tokens, screen_min_tokens), device=dev)
         self.rw = W.to_device(hl.router_w, dev)
         self.bias = W.to_device(hl.bias, dev)
         self.ew = W.to_device(hl.expert_w, dev)
@@ -114,11 +114,17 @@ SMALL_F32_MX = LayerConfig("small-f32-mxfp4", 256, 8, 2, 256, "f32", "f32", "mxf
 SMALL_NV = LayerConfig("small-nvfp4", 512, 16, 4, 256, "bf16", "bf16", "nvfp4", "normal:0.5", [])
 
 
+@pytest.mark.parametrize("screen", [-1, 1], ids=["exact", "screened"])
 @pytest.mark.parametrize("T", [1, 5, 13, 32])
-def test_small_fp8_layer(dev, T):
+def test_small_fp8_layer(dev, T, screen):
+    """Both routing paths: every logit exact, or screened (bf16 matrix-core brackets,
+    exact logits only for the experts whose bracket can reach the top k)."""
     hl = W.host_layer(SMALL_FP8, seed=501)
-    run = Run(SMALL_FP8, hl, dev, max_tokens=32)
-    check_layer(run, W.host_x(SMALL_FP8, T, seed=501), label=f"small-fp8 T={T}")
+    run = Run(SMALL_FP8, hl, dev, max_tokens=32, screen_min_tokens=screen)
+    check_layer(run, W.host_x(SMALL_FP8, T, seed=501), label=f"small-fp8 T={T} screen={screen}")
+    st, _ = run.m.stats()
+    assert st.route_screened == (screen > 0)
+    assert (st.n_exact_logits < T * SMALL_FP8.n_experts) if screen > 0 else (st.n_exact_logits == T * 16)
 
 
 @pytest.mark.parametrize("T", [3, 13])
@@ -131,7 +137,7 @@ def test_small_mxfp4_layer(dev, T):
 @pytest.mark.parametrize("T", [1, 5, 13, 32])
 def test_small_nvfp4_layer(dev, T):
     hl = W.host_layer(SMALL_NV, seed=541)
-    run = Run(SMALL_NV, hl, dev, max_tokens=32)
+    run = Run(SMALL_NV, hl, dev, max_tokens=32, screen_min_tokens=13)
     check_layer(run, W.host_x(SMALL_NV, T, seed=541), label=f"small-nvfp4 T={T}")
 
 
@@ -174,20 +180,22 @@ def test_small_routing_bitwise(dev):
     check_routing(run, W.host_x(SMALL_FP8, 32, seed=504), label="small-fp8")
 
 
+@pytest.mark.parametrize("screen", [-1, 1], ids=["exact", "screened"])
 @pytest.mark.parametrize("k", [1, 16])
-def test_topk_extremes(dev, k):
+def test_topk_extremes(dev, k, screen):
     cfg = LayerConfig("k-extreme", 512, 16, 16, 256, "bf16", "bf16", "fp8", None, [])
     hl = W.host_layer(cfg, seed=505)
-    run = Run(cfg, hl, dev, max_tokens=8)
+    run = Run(cfg, hl, dev, max_tokens=8, screen_min_tokens=screen)
     check_layer(run, W.host_x(cfg, 5, seed=505), topk=k, label=f"k={k}")
 
 
-def test_single_expert_dense(dev):
+@pytest.mark.parametrize("screen", [-1, 1], ids=["exact", "screened"])
+def test_single_expert_dense(dev, screen):
     """E = 1, k = 1: every token routes to expert 0 with weight 1 and the layer is one
     dense SwiGLU block (the degenerate case of the method)."""
     cfg = LayerConfig("one-expert", 512, 1, 1, 512, "bf16", "bf16", "fp8", None, [])
     hl = W.host_layer(cfg, seed=511)
-    run = Run(cfg, hl, dev, max_tokens=40)
+    run = Run(cfg, hl, dev, max_tokens=40, screen_min_tokens=screen)
     ids, wts, _ = check_layer(run, W.host_x(cfg, 37, seed=511), label="E=1")
     assert np.all(ids == 0) and np.all(wts == 1.0)
 
@@ -196,12 +204,14 @@ def test_single_expert_dense(dev):
     (LayerConfig("wide-1024", 256, 1024, 64, 256, "bf16", "bf16", "fp8", "normal:0.5", []), 64),
     (LayerConfig("wide-600", 512, 600, 24, 512, "bf16", "bf16", "mxfp4", "zipf:1.1", []), 24),
 ], ids=["E1024-k64", "E600-k24"])
-def test_many_experts(dev, cfg, k):
+@pytest.mark.parametrize("screen", [-1, 1], ids=["exact", "screened"])
+def test_many_experts(dev, cfg, k, screen):
     """The largest expert counts and top-k the library accepts (16 keys per lane in
     the wave top-k, the widest grouping bitmasks)."""
     hl = W.host_layer(cfg, seed=512)
-    run = Run(cfg, hl, dev, max_tokens=48)
-    check_layer(run, W.host_x(cfg, 33, seed=512), topk=k, label=f"{cfg.name} k={k}")
+    run = Run(cfg, hl, dev, max_tokens=48, screen_min_tokens=screen)
+    check_layer(run, W.host_x(cfg, 33, seed=512), topk=k, label=f"{cfg.name} k={k} screen={screen}")
+    assert run.m.stats()[0].route_screened == (screen > 0)
     check_routing(run, W.host_x(cfg, 9, seed=513), topk=k, label=f"{cfg.name} k={k}")
 
 
@@ -218,6 +228,40 @@ def test_zero_input_and_ties(dev):
     ids, wts, y = check_layer(run, x, label="zero+ties")
     assert list(ids[3]) == [0, 1, 2, 3] and np.all(wts[3] == 0.25) and np.all(y[3] == 0)
     check_routing(run, x, label="zero+ties")
+
+
+def test_screened_routing_degenerate(dev):
+    """The screened forward step brackets every logit with matrix-core sums and
+    computes exactly only the experts that can reach the top k.  Degenerate inputs
+    make every expert a candidate: a zero row (all logits +0), duplicate router rows
+    (ties to the lower index), and logits on fp32 rounding midpoints (double-double
+    fallback); the selection must still be the oracle's."""
+    hl = W.host_layer(SMALL_FP8, seed=514)
+    hl.bias = None
+    hl.router_w[9] = hl.router_w[2]
+    hl.router_w[11] = hl.router_w[2]
+    run = Run(SMALL_FP8, hl, dev, max_tokens=64, screen_min_tokens=1)
+    x = W.host_x(SMALL_FP8, 40, seed=514)
+    x[3] = 0
+    x[17] = 0
+    ids, wts, y = check_layer(run, x, label="screened zero+ties")
+    assert list(ids[3]) == [0, 1, 2, 3] and np.all(wts[3] == 0.25) and np.all(y[3] == 0)
+
+    cfg = LayerConfig("midpoint-screened", 512, 16, 4, 256, "bf16", "bf16", "fp8", None, [])
+    hl = W.host_layer(cfg, seed=515)
+    one, tiny24, tiny80 = 0x3F80, 0x3380, 0x1780  # 1.0, 2^-24, 2^-80 in bf16
+    hl.router_w[:] = 0
+    hl.router_w[:, 0] = one
+    hl.router_w[5, 1] = tiny24  # l = 1 + 2^-24: tie -> 1.0
+    hl.router_w[6, 1] = tiny24  # l = 1 + 2^-24 + 2^-80: above the tie -> 1 + 2^-23
+    hl.router_w[6, 2] = tiny80
+    x = np.zeros((36, cfg.hidden), np.uint16)
+    x[:, 0] = x[:, 1] = x[:, 2] = one
+    run = Run(cfg, hl, dev, max_tokens=64, screen_min_tokens=1)
+    ids, _, _ = check_layer(run, x, label="screened midpoint")
+    assert np.all(ids[:, 0] == 6)
+    st, _ = run.m.stats()
+    assert st.route_screened and st.n_fallback >= 36 and st.n_exact_logits == 36 * 16
 
 
 def test_exact_fallback_path(dev):
@@ -269,11 +313,13 @@ def test_zero_tokens_leaves_output_untouched(dev):
     assert torch.all(y == 7.0)
 
 
-def test_max_tokens(dev):
+@pytest.mark.parametrize("screen", [-1, 1], ids=["exact", "screened"])
+def test_max_tokens(dev, screen):
     cfg = LayerConfig("maxT", 512, 16, 4, 256, "bf16", "bf16", "fp8", "normal:0.5", [])
     hl = W.host_layer(cfg, seed=510)
-    run = Run(cfg, hl, dev, max_tokens=1024)
-    check_layer(run, W.host_x(cfg, 1024, seed=510), tokens=[0, 511, 1023], label="T=1024")
+    run = Run(cfg, hl, dev, max_tokens=1024, screen_min_tokens=screen)
+    tokens = None if screen > 0 else [0, 511, 1023]  # the screened run: every token
+    check_layer(run, W.host_x(cfg, 1024, seed=510), tokens=tokens, label=f"T=1024 screen={screen}")
 
 
 # LDS-staged MFMA kernels (K spanning a multiple of four 128-input blocks; the down
@@ -318,7 +364,7 @@ def test_random_small_layers(dev, i):
     cfg, T = _random_layer(i)
     assert 4 * max(cfg.hidden, cfg.inter) * (2 if cfg.act == "bf16" else 4) <= 65536  # accepted shapes
     hl = W.host_layer(cfg, seed=700 + i)
-    run = Run(cfg, hl, dev, max_tokens=T, mfma_min_tokens=[0, -1, 2][i % 3])
+    run = Run(cfg, hl, dev, max_tokens=T, mfma_min_tokens=[0, -1, 2][i % 3], screen_min_tokens=[1, -1][(i // 2) % 2])
     say(f"[random] {cfg}")
     check_layer(run, W.host_x(cfg, T, seed=700 + i), label=f"random {i}")
 
@@ -339,7 +385,7 @@ def _random_nvfp4_layer(i):
 def test_random_nvfp4_layers(dev, i):
     cfg, T = _random_nvfp4_layer(i)
     hl = W.host_layer(cfg, seed=750 + i)
-    run = Run(cfg, hl, dev, max_tokens=T, mfma_min_tokens=[0, -1, 2][i % 3])
+    run = Run(cfg, hl, dev, max_tokens=T, mfma_min_tokens=[0, -1, 2][i % 3], screen_min_tokens=[1, -1][i % 2])
     say(f"[random] {cfg}")
     check_layer(run, W.host_x(cfg, T, seed=750 + i), label=f"random nvfp4 {i}")
 
@@ -358,19 +404,25 @@ def full_480b(dev):
     return W.host_layer(C.QWEN3_480B)
 
 
-def _full(run, cfg, T, batch):
+def _full(run, cfg, T, batch, screened=None):
     x = W.host_x(cfg, T, batch=batch)
     tokens = sorted({0, T // 2, T - 1})
     ids, wts, y = check_layer(run, x, tokens=tokens, label=f"{cfg.name} T={T}")
     # routing of every token
     io = np.stack([oracle.route_token(x[t], run.hl.router_w, run.hl.bias, cfg.topk)[1] for t in range(T)])
     assert np.array_equal(ids, io)
+    st = run.m.stats()[0]
+    if screened is None:  # the library default: screened from T*E*H >= 2^26 multiply-adds
+        screened = T * cfg.n_experts * cfg.hidden >= 1 << 26
+    say(f"[route] screened={st.route_screened} exact logits {st.n_exact_logits} of {T * cfg.n_experts}")
+    assert st.route_screened == screened
 
 
+@pytest.mark.parametrize("screen", [0, 1], ids=["default", "screened"])
 @pytest.mark.parametrize("T", C.QWEN3_235B.tokens)
-def test_full_235b(dev, full_235b, T):
-    run = Run(C.QWEN3_235B, full_235b, dev, max_tokens=max(C.QWEN3_235B.tokens))
-    _full(run, C.QWEN3_235B, T, batch=T)
+def test_full_235b(dev, full_235b, T, screen):
+    run = Run(C.QWEN3_235B, full_235b, dev, max_tokens=max(C.QWEN3_235B.tokens), screen_min_tokens=screen)
+    _full(run, C.QWEN3_235B, T, batch=T, screened=True if screen else None)
 
 
 @pytest.mark.parametrize("T", C.QWEN3_480B.tokens)
