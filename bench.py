@@ -85,6 +85,9 @@ def parse():
     ap.add_argument("--attn", action="store_true",
                     help="decode attention over a paged KV cache instead of the MoE layer: one JSON line per "
                          "workload of attn_workload.ATTN_CONFIGS")
+    ap.add_argument("--attn-merge-max-splits", type=int, default=0,
+                    help="with --attn: contexts of at most this many 256-token splits are merged inside the split "
+                         "kernel (0: library default, -1: always by a second kernel)")
     ap.add_argument("--stack", action="store_true",
                     help="also time the stack of 12 distinct 480B-shaped layers decoded back to back, T = 1..256")
     ap.add_argument("--stack-steps", type=int, default=20)
@@ -233,7 +236,8 @@ def run_attn(args, dev):
             d0 = A.to_device(h, dev)
             dd.append([d0] + [dict(d0, k_cache=d0["k_cache"].clone(), v_cache=d0["v_cache"].clone())
                               for _ in range(copies - 1)])
-        m = B.AttnDecode(B.make_attn_config(cfg.n_q_heads, cfg.n_kv_heads, cfg.batch, mp), device=dev)
+        m = B.AttnDecode(B.make_attn_config(cfg.n_q_heads, cfg.n_kv_heads, cfg.batch, mp,
+                                            fused_merge_max_splits=args.attn_merge_max_splits), device=dev)
         out = torch.empty((cfg.batch, cfg.n_q_heads, 128), dtype=torch.int16, device=dev)
         scale = 1 / math.sqrt(128)
 

@@ -55,17 +55,31 @@ typedef struct attn_decode_config {
     int32_t page_size;         /* P: 16 */
     int32_t max_batch;         /* largest B of any call, 1..4096 */
     int32_t max_pages_per_seq; /* block-table row length, 1..65536 */
-    int32_t reserved[4];       /* must be zero */
+    int32_t fused_merge_max_splits; /* the context is split into 256-token pieces; when a
+                                  row of max_pages_per_seq pages needs at most this many,
+                                  the split kernel merges them itself (its last workgroup
+                                  per sequence and key/value head), else a second kernel
+                                  does.  0 = library default 16, negative = never, at most
+                                  16.  The result is the same bits either way. */
+    int32_t reserved[3];       /* must be zero */
 } attn_decode_config;
 
-/* Bytes of device workspace forward needs for this configuration (split partials);
- * 0 if the configuration is invalid. */
+/* Bytes of device workspace forward needs for this configuration (split partials and
+ * one merge counter per sequence and key/value head); 0 if the configuration is
+ * invalid. */
 size_t attn_decode_workspace_bytes(const attn_decode_config *cfg);
+
+/* Enqueue on `stream` the clearing of a workspace's merge counters: once, before the
+ * workspace's first forward (each forward leaves them cleared again; after a forward
+ * that did not complete, clear them again).  Same workspace rules and status codes as
+ * attn_decode_forward. */
+int attn_decode_workspace_init(const attn_decode_config *cfg, void *workspace, size_t workspace_bytes, void *stream);
 
 /* One decode step of attention for `batch` sequences (0 <= batch <= max_batch; 0 is a
  * no-op).  `scale` multiplies the scores (1/sqrt(D) for standard attention) and must
  * be finite and positive.  `workspace` holds at least attn_decode_workspace_bytes(cfg)
- * bytes of device memory owned by the caller. */
+ * bytes of device memory owned by the caller, initialised once by
+ * attn_decode_workspace_init. */
 int attn_decode_forward(const attn_decode_config *cfg, void *workspace, size_t workspace_bytes, void *stream,
                         const void *q, const void *k_cache, const void *v_cache, int64_t n_pages,
                         const int32_t *block_table, const int32_t *ctx_lens, int32_t batch, float scale,

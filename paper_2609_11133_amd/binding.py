@@ -58,7 +58,8 @@ class attn_decode_config(ctypes.Structure):
         ("page_size", ctypes.c_int32),
         ("max_batch", ctypes.c_int32),
         ("max_pages_per_seq", ctypes.c_int32),
-        ("reserved", ctypes.c_int32 * 4),
+        ("fused_merge_max_splits", ctypes.c_int32),
+        ("reserved", ctypes.c_int32 * 3),
     ]
 
 
@@ -110,6 +111,8 @@ def lib():
         acfgp = ctypes.POINTER(attn_decode_config)
         L.attn_decode_workspace_bytes.restype = SZ
         L.attn_decode_workspace_bytes.argtypes = [acfgp]
+        L.attn_decode_workspace_init.restype = ctypes.c_int
+        L.attn_decode_workspace_init.argtypes = [acfgp, P, SZ, P]
         L.attn_decode_forward.restype = ctypes.c_int
         L.attn_decode_forward.argtypes = [acfgp, P, SZ, P, P, P, P, ctypes.c_int64, P, P, I32, ctypes.c_float, P]
         L.attn_decode_last_error.restype = ctypes.c_char_p
@@ -256,8 +259,16 @@ class MoEDecode:
 # ---------------------------------------------------------------- decode attention
 
 
-def make_attn_config(n_q_heads, n_kv_heads, max_batch, max_pages_per_seq, head_dim=128, page_size=16):
-    return attn_decode_config(n_q_heads, n_kv_heads, head_dim, page_size, max_batch, max_pages_per_seq)
+def make_attn_config(n_q_heads, n_kv_heads, max_batch, max_pages_per_seq, head_dim=128, page_size=16,
+                     fused_merge_max_splits=0):
+    return attn_decode_config(n_q_heads, n_kv_heads, head_dim, page_size, max_batch, max_pages_per_seq,
+                              fused_merge_max_splits)
+
+
+def attn_decode_workspace_init(cfg, workspace, workspace_bytes, stream):
+    st = lib().attn_decode_workspace_init(ctypes.byref(cfg), _addr(workspace), workspace_bytes, stream)
+    if st != 0:
+        raise MoEDecodeError(st, lib().attn_decode_last_error().decode() or "attn_decode_workspace_init failed")
 
 
 def attn_decode_workspace_bytes(cfg: attn_decode_config) -> int:
@@ -287,6 +298,7 @@ class AttnDecode:
         self.workspace = torch.empty(self.nbytes + 256, dtype=torch.uint8, device=device)
         self._ws_addr = (self.workspace.data_ptr() + 255) // 256 * 256
         self.device = self.workspace.device
+        attn_decode_workspace_init(cfg, self._ws_addr, self.nbytes, torch.cuda.current_stream(self.device).cuda_stream)
 
     def forward(self, q, k_cache, v_cache, n_pages, block_table, ctx_lens, batch, scale, out):
         import torch

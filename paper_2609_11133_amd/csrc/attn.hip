@@ -14,8 +14,11 @@
 //                        transpose; the values are read dimension-major (a page stores
 //                        V as [D][16]), four contiguous tokens per tile.
 // The workgroup shares one score maximum per head (through LDS), so its four waves' P.V
-// partials add directly; it writes (max, sum, O) of its split, and a second kernel
-// merges the splits of each (sequence, query head) in split order.
+// partials add directly; it writes (max, sum, O) of its split, and the splits of each
+// (sequence, query head) are merged in split order: by the last of the sequence's
+// workgroups for that key/value head (a device-scope counter, the partials written and
+// read with device-coherent accesses) when a sequence has at most kFusedSplits splits,
+// else by a second kernel.  A sequence with one split writes its output directly.
 //
 // Operand layout of v_mfma_f32_16x16x32_bf16 (checked on the device): lane l holds
 // row/column l%16 and K [8g, 8g+8) with g = l/16; the result gives lane l rows
@@ -47,6 +50,21 @@ constexpr int kChunk = kWaves * kWaveTok;  // tokens per split
 constexpr int kDT = kD / 16;               // 16-column tiles of the output
 constexpr float kLog2e = 1.44269504088896340736f;
 constexpr int kRawBufferWord3 = 0x00020000;  // untyped 32-bit data format, no swizzle
+constexpr int kFusedSplits = 16;             // splits merged inside the split kernel, at most
+
+// Device-coherent accesses for the hand-off between workgroups (relaxed atomics at agent
+// scope bypass the per-XCD L2), and a wait for this thread's stores.
+template <typename T>
+__device__ inline void st_dev(T *p, T v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+template <typename T>
+__device__ inline T ld_dev(const T *p) { return __hip_atomic_load(const_cast<T *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+__device__ inline void wait_stores() { __builtin_amdgcn_s_waitcnt(0); }
+
+__device__ inline uint16_t to_bf16(float y)
+{
+    const bf16x2 yb = __builtin_convertvector((f32x2){y, 0.f}, bf16x2);
+    return __builtin_bit_cast(uint16_t, yb.x);
+}
 
 // A raw buffer over `bytes` bytes at `base`: loads past the end return zeros and make
 // no memory request, so a page the kernel must not read gets bytes = 0.
@@ -59,22 +77,33 @@ __device__ inline bf16x8 as_bf16x8(const u32x4v &u) { return __builtin_bit_cast(
 
 // Split kernel: partial (max, sum, O) of one 256-token split for one (sequence, key/value
 // head) and its query heads.  Grid (splits, Hkv, B), 256 threads.  Scores are kept in
-// log2 units (scale * log2 e folded in), so p = exp2(s - m).
+// log2 units (scale * log2 e folded in), so p = exp2(s - m).  FUSED: the merge of the
+// splits happens here (S <= kFusedSplits; `cnt` holds one zeroed counter per (b, g),
+// left at zero again), and `out` is written here.
+template <bool FUSED>
 __global__ __launch_bounds__(256) void attn_split_kernel(const uint16_t *__restrict__ q,
                                                          const uint16_t *__restrict__ kc,
                                                          const uint16_t *__restrict__ vc, int64_t n_pages,
                                                          const int32_t *__restrict__ block_table, int max_pages,
                                                          const int32_t *__restrict__ ctx, int Hkv, int G,
                                                          float scale_log2, float *__restrict__ po,
-                                                         float *__restrict__ pml, int S)
+                                                         float *__restrict__ pml, int S, int32_t *__restrict__ cnt,
+                                                         uint16_t *__restrict__ out)
 {
     __shared__ float s_max[kWaves][16], s_sum[kWaves][16];
     __shared__ f32x4 red[kWaves][kDT][64];
+    __shared__ float s_w[FUSED ? kFusedSplits : 1][16], s_den[16];
+    __shared__ int s_last;
     const int c = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
     const int L = min(max(ctx[b], 0), max_pages * kP);
     const int t0 = c * kChunk;
-    if (t0 >= L) return;  // uniform over the workgroup
     const int tid = threadIdx.x, lane = tid & 63;
+    uint16_t *orow = out + ((size_t)b * Hkv + g) * G * kD;  // the group's [G][D] outputs
+    if (t0 >= L) {  // uniform over the workgroup
+        if (FUSED && c == 0)  // empty context: zeros
+            for (int e = tid; e < G * kD; e += 256) orow[e] = 0;
+        return;
+    }
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int r = lane & 15, lg = lane >> 4;
 
@@ -181,18 +210,121 @@ __global__ __launch_bounds__(256) void attn_split_kernel(const uint16_t *__restr
 #pragma unroll
     for (int j = 0; j < kDT; ++j) red[wave][j][lane] = o[j];
     __syncthreads();
-    const size_t part = ((size_t)b * Hkv + g) * S + c;
+    const int ns = (L + kChunk - 1) / kChunk;  // splits of this sequence
+    if (FUSED && ns == 1) {
+        // the only split: out = O / l (what the merge of one split gives)
+#pragma unroll
+        for (int k = 0; k < 16 * kD / 256; ++k) {
+            const int e = tid + 256 * k;  // (head n, dim d); n is uniform over a wave
+            const int n = e / kD, d = e % kD;
+            if (n < G) {
+                const int j = d / 16, ln = 16 * (n / 4) + d % 16, comp = n % 4;
+                const float v = ((red[0][j][ln][comp] + red[1][j][ln][comp]) + red[2][j][ln][comp]) + red[3][j][ln][comp];
+                const float l = ((s_sum[0][n] + s_sum[1][n]) + s_sum[2][n]) + s_sum[3][n];
+                orow[e] = to_bf16(fmaf(1.f, v, 0.f) / fmaf(1.f, l, 0.f));
+            }
+        }
+        return;
+    }
+    const size_t part0 = ((size_t)b * Hkv + g) * S, part = part0 + c;
 #pragma unroll
     for (int k = 0; k < 16 * kD / 256; ++k) {
         const int e = tid + 256 * k;  // (head n, dim d)
         const int n = e / kD, d = e % kD;
         const int j = d / 16, ln = 16 * (n / 4) + d % 16, comp = n % 4;
         const float v = ((red[0][j][ln][comp] + red[1][j][ln][comp]) + red[2][j][ln][comp]) + red[3][j][ln][comp];
-        po[part * 16 * kD + e] = v;
+        if (FUSED)
+            st_dev(&po[part * 16 * kD + e], v);
+        else
+            po[part * 16 * kD + e] = v;
     }
-    if (tid < 16)
-        reinterpret_cast<f32x2 *>(pml)[part * 16 + tid] =
-            (f32x2){m, ((s_sum[0][tid] + s_sum[1][tid]) + s_sum[2][tid]) + s_sum[3][tid]};
+    if (tid < 16) {
+        const float l = ((s_sum[0][tid] + s_sum[1][tid]) + s_sum[2][tid]) + s_sum[3][tid];
+        if (FUSED) {
+            st_dev(&pml[(part * 16 + tid) * 2], m);
+            st_dev(&pml[(part * 16 + tid) * 2 + 1], l);
+        } else {
+            reinterpret_cast<f32x2 *>(pml)[part * 16 + tid] = (f32x2){m, l};
+        }
+    }
+    if constexpr (FUSED) {
+        // the last of the sequence's workgroups for head g merges its ns splits
+        wait_stores();
+        __syncthreads();
+        int32_t *ctr = cnt + (size_t)b * Hkv + g;
+        if (tid == 0) s_last = atomicAdd(ctr, 1) == ns - 1;
+        __syncthreads();
+        if (!s_last) return;
+        if (tid == 0) st_dev(ctr, 0);
+        // thread: element pairs (2 e2, 2 e2 + 1), e2 = tid + 256 k2, of head e2 / 64 (uniform
+        // over a wave); eight splits' 64-bit loads in flight per round, the first round
+        // issued before the weights are formed
+        constexpr int kRound = 8;
+        const uint64_t *po2 = reinterpret_cast<const uint64_t *>(po);
+        uint64_t v[kRound][4];
+        auto load_round = [&](int c0) {
+#pragma unroll
+            for (int u = 0; u < kRound; ++u)
+#pragma unroll
+                for (int k2 = 0; k2 < 4; ++k2) {
+                    const int e2 = tid + 256 * k2;
+                    v[u][k2] = c0 + u < ns && e2 / 64 < G ? ld_dev(&po2[(part0 + c0 + u) * (16 * kD / 2) + e2]) : 0;
+                }
+        };
+        load_round(0);
+        // weights 2^(m_c - M) and the denominator per head, splits in ascending order
+        if (tid < 16) {
+            float mc[kFusedSplits], lc[kFusedSplits];
+#pragma unroll
+            for (int cc = 0; cc < kFusedSplits; ++cc) {
+                const size_t pc = (part0 + min(cc, ns - 1)) * 16 + tid;
+                mc[cc] = ld_dev(&pml[pc * 2]);
+                lc[cc] = ld_dev(&pml[pc * 2 + 1]);
+            }
+            float M = -INFINITY;
+#pragma unroll
+            for (int cc = 0; cc < kFusedSplits; ++cc) M = fmaxf(M, mc[cc]);  // repeats of the last split
+            float den = 0.f;
+#pragma unroll
+            for (int cc = 0; cc < kFusedSplits; ++cc)
+                if (cc < ns) {
+                    const float w = exp2f(mc[cc] - M);
+                    den = fmaf(w, lc[cc], den);
+                    s_w[cc][tid] = w;
+                }
+            s_den[tid] = den;
+        }
+        __syncthreads();
+        float num[4][2];
+#pragma unroll
+        for (int k2 = 0; k2 < 4; ++k2) num[k2][0] = num[k2][1] = 0.f;
+        for (int c0 = 0; c0 < ns; c0 += kRound) {
+            if (c0) load_round(c0);
+#pragma unroll
+            for (int u = 0; u < kRound; ++u)
+                if (c0 + u < ns)
+#pragma unroll
+                    for (int k2 = 0; k2 < 4; ++k2) {
+                        const float w = s_w[c0 + u][(tid + 256 * k2) / 64];
+                        num[k2][0] = fmaf(w, __uint_as_float((uint32_t)v[u][k2]), num[k2][0]);
+                        num[k2][1] = fmaf(w, __uint_as_float((uint32_t)(v[u][k2] >> 32)), num[k2][1]);
+                    }
+        }
+#pragma unroll
+        for (int k2 = 0; k2 < 4; ++k2) {
+            const int e2 = tid + 256 * k2, n = e2 / 64;
+            if (n < G) {
+                const uint32_t lo = to_bf16(num[k2][0] / s_den[n]), hi = to_bf16(num[k2][1] / s_den[n]);
+                reinterpret_cast<uint32_t *>(orow)[e2] = lo | (hi << 16);
+            }
+        }
+    }
+}
+
+// Counters of the fused merge: zero.
+__global__ void attn_zero_kernel(int32_t *p, int n)
+{
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0;
 }
 
 // Combine kernel: out[b][g*G + n][d] = sum_c 2^(m_c - M) O_c[n][d] / sum_c 2^(m_c - M) l_c
@@ -237,8 +369,7 @@ __global__ __launch_bounds__(128) void attn_combine_kernel(const float *__restri
             }
     }
     const float y = ns ? num / den : 0.f;
-    const bf16x2 yb = __builtin_convertvector((f32x2){y, 0.f}, bf16x2);
-    out[(((size_t)b * Hkv + g) * G + n) * kD + d] = __builtin_bit_cast(uint16_t, yb.x);
+    out[(((size_t)b * Hkv + g) * G + n) * kD + d] = to_bf16(y);
 }
 
 thread_local char g_err[256];
@@ -255,8 +386,10 @@ int fail(int code, const char *fmt, ...)
 int check_config(const attn_decode_config *c)
 {
     if (!c) return fail(ATTN_ERR_INVALID, "config is NULL");
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 3; ++i)
         if (c->reserved[i] != 0) return fail(ATTN_ERR_INVALID, "config.reserved[%d] must be zero", i);
+    if (c->fused_merge_max_splits > kFusedSplits)
+        return fail(ATTN_ERR_INVALID, "fused_merge_max_splits=%d exceeds %d", c->fused_merge_max_splits, kFusedSplits);
     if (c->n_kv_heads < 1) return fail(ATTN_ERR_INVALID, "n_kv_heads=%d must be positive", c->n_kv_heads);
     if (c->n_q_heads < 1 || c->n_q_heads % c->n_kv_heads)
         return fail(ATTN_ERR_INVALID, "n_q_heads=%d must be a positive multiple of n_kv_heads=%d", c->n_q_heads,
@@ -280,6 +413,20 @@ size_t partial_o_bytes(const attn_decode_config *c)
     return ((size_t)c->max_batch * c->n_kv_heads * max_splits(c) * 16 * kD * 4 + 255) & ~(size_t)255;
 }
 
+size_t partial_ml_bytes(const attn_decode_config *c)
+{
+    return ((size_t)c->max_batch * c->n_kv_heads * max_splits(c) * 16 * 8 + 255) & ~(size_t)255;
+}
+
+size_t counter_words(const attn_decode_config *c) { return (size_t)c->max_batch * c->n_kv_heads; }
+
+// The split kernel merges the splits itself when every sequence has at most this many.
+bool fused(const attn_decode_config *c)
+{
+    const int lim = c->fused_merge_max_splits == 0 ? kFusedSplits : c->fused_merge_max_splits;
+    return max_splits(c) <= lim;
+}
+
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 
 }  // namespace
@@ -289,7 +436,26 @@ extern "C" size_t attn_decode_workspace_bytes(const attn_decode_config *cfg)
 {
     using namespace attn;
     if (check_config(cfg) != ATTN_OK) return 0;
-    return partial_o_bytes(cfg) + (size_t)cfg->max_batch * cfg->n_kv_heads * max_splits(cfg) * 16 * 8;
+    return partial_o_bytes(cfg) + partial_ml_bytes(cfg) + counter_words(cfg) * 4;
+}
+
+extern "C" int attn_decode_workspace_init(const attn_decode_config *cfg, void *workspace, size_t workspace_bytes,
+                                          void *stream)
+{
+    using namespace attn;
+    g_err[0] = 0;
+    const int rc = check_config(cfg);
+    if (rc != ATTN_OK) return rc;
+    if (!workspace || !aligned(workspace, 256)) return fail(ATTN_ERR_WORKSPACE, "workspace is NULL or not 256-byte aligned");
+    if (workspace_bytes < attn_decode_workspace_bytes(cfg))
+        return fail(ATTN_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes,
+                    attn_decode_workspace_bytes(cfg));
+    int32_t *cnt = (int32_t *)((char *)workspace + partial_o_bytes(cfg) + partial_ml_bytes(cfg));
+    const int n = (int)counter_words(cfg);
+    attn_zero_kernel<<<(n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024, 256, 0, (hipStream_t)stream>>>(cnt, n);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(ATTN_ERR_HIP, "zero kernel launch: %s", hipGetErrorString(e));
+    return ATTN_OK;
 }
 
 extern "C" int attn_decode_forward(const attn_decode_config *cfg, void *workspace, size_t workspace_bytes, void *stream,
@@ -321,11 +487,19 @@ extern "C" int attn_decode_forward(const attn_decode_config *cfg, void *workspac
     const int Hkv = cfg->n_kv_heads, G = cfg->n_q_heads / Hkv, S = max_splits(cfg);
     float *po = (float *)workspace;
     float *pml = (float *)((char *)workspace + partial_o_bytes(cfg));
+    int32_t *cnt = (int32_t *)((char *)workspace + partial_o_bytes(cfg) + partial_ml_bytes(cfg));
     hipStream_t st = (hipStream_t)stream;
-    attn_split_kernel<<<dim3(S, Hkv, batch), 256, 0, st>>>((const uint16_t *)q, (const uint16_t *)k_cache,
-                                                          (const uint16_t *)v_cache, n_pages, block_table,
-                                                          cfg->max_pages_per_seq, ctx_lens, Hkv, G,
-                                                          scale * kLog2e, po, pml, S);
+    if (fused(cfg)) {
+        attn_split_kernel<true><<<dim3(S, Hkv, batch), 256, 0, st>>>(
+            (const uint16_t *)q, (const uint16_t *)k_cache, (const uint16_t *)v_cache, n_pages, block_table,
+            cfg->max_pages_per_seq, ctx_lens, Hkv, G, scale * kLog2e, po, pml, S, cnt, (uint16_t *)out);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return fail(ATTN_ERR_HIP, "split kernel launch: %s", hipGetErrorString(e));
+        return ATTN_OK;
+    }
+    attn_split_kernel<false><<<dim3(S, Hkv, batch), 256, 0, st>>>(
+        (const uint16_t *)q, (const uint16_t *)k_cache, (const uint16_t *)v_cache, n_pages, block_table,
+        cfg->max_pages_per_seq, ctx_lens, Hkv, G, scale * kLog2e, po, pml, S, cnt, (uint16_t *)out);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(ATTN_ERR_HIP, "split kernel launch: %s", hipGetErrorString(e));
     attn_combine_kernel<<<dim3(G, Hkv, batch), 128, 0, st>>>(po, pml, ctx_lens, cfg->max_pages_per_seq, Hkv, G, S,

@@ -172,7 +172,8 @@ ATTN_HEADER = os.path.join(ROOT, "include", "attn_decode.h")
 def test_every_attention_symbol_is_exported(B):
     src = re.sub(r"/\*.*?\*/", "", open(ATTN_HEADER).read(), flags=re.S)
     names = sorted(set(re.findall(r"\b(attn_decode_\w+)\s*\(", src)))
-    assert names == ["attn_decode_forward", "attn_decode_last_error", "attn_decode_workspace_bytes"]
+    assert names == ["attn_decode_forward", "attn_decode_last_error", "attn_decode_workspace_bytes",
+                     "attn_decode_workspace_init"]
     lib = ctypes.CDLL(B.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -181,7 +182,8 @@ def test_every_attention_symbol_is_exported(B):
 def test_attention_workspace_bytes(B):
     c = B.make_attn_config(64, 4, 24, 128)  # 2048 tokens: 8 splits of 256
     parts = 24 * 4 * 8 * 16
-    assert B.attn_decode_workspace_bytes(c) == (parts * 128 * 4 + 255) // 256 * 256 + parts * 8
+    rnd = lambda n: (n + 255) // 256 * 256  # noqa: E731
+    assert B.attn_decode_workspace_bytes(c) == rnd(parts * 128 * 4) + rnd(parts * 8) + 24 * 4 * 4
 
 
 @pytest.mark.parametrize(
@@ -195,6 +197,7 @@ def test_attention_workspace_bytes(B):
         (dict(max_batch=0), -1),
         (dict(max_batch=5000), -1),
         (dict(max_pages_per_seq=0), -1),
+        (dict(fused_merge_max_splits=17), -1),
     ],
 )
 def test_attention_invalid_configs_rejected(B, kw, code):
@@ -234,6 +237,31 @@ def test_attention_forward_validates_before_launch(B, change, needle):
                               args["v_cache"], args["n_pages"], args["block_table"], args["ctx_lens"], args["batch"],
                               args["scale"], args["out"])
     assert needle in str(e.value)
+
+
+@pytest.mark.parametrize(
+    "change,needle",
+    [
+        (dict(workspace=0), "workspace"),
+        (dict(workspace=300), "workspace"),
+        (dict(workspace_bytes=100), "workspace of 100 bytes"),
+    ],
+)
+def test_attention_workspace_init_validates(B, change, needle):
+    c = B.make_attn_config(64, 4, 8, 16)
+    args = dict(workspace=256, workspace_bytes=B.attn_decode_workspace_bytes(c))
+    args.update(change)
+    with pytest.raises(B.MoEDecodeError) as e:
+        B.attn_decode_workspace_init(c, args["workspace"], args["workspace_bytes"], None)
+    assert needle in str(e.value)
+
+
+def test_attention_config_struct(B):
+    assert ctypes.sizeof(B.attn_decode_config) == 40
+    c = B.make_attn_config(64, 4, 8, 16, fused_merge_max_splits=-1)
+    assert B.attn_decode_workspace_bytes(c) > 0
+    c.reserved[2] = 1
+    assert B.attn_decode_workspace_bytes(c) == 0
 
 
 def test_attention_zero_batch_is_a_no_op(B):

@@ -5,9 +5,10 @@ is derived from the arithmetic: the output is rounded once to bf16 (2^-9 relativ
 the probabilities enter the P.V product rounded to bf16 (2^-9 relative each, averaging
 out over the context), with fp32 accumulation; 1e-2 leaves about a fivefold margin.
 Small cases cover every split/page boundary and ragged tail, empty contexts, group
-sizes 1-16, bytes past the contexts holding NaN, and page indices outside the cache;
-the full-size agentic steps of both models are compared on every row, the 32K-token
-long-context step on sampled sequences."""
+sizes 1-16, bytes past the contexts holding NaN, and page indices outside the cache,
+with the splits merged inside the split kernel and by the second kernel (the two give
+the same bits); the full-size agentic steps of both models are compared on every row,
+the 32K-token long-context step on sampled sequences."""
 import sys
 
 import numpy as np
@@ -41,16 +42,16 @@ def bf16_to_f64(t):
     return (t.cpu().numpy().view(np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
 
 
-def run_gpu(cfg, h, dev, scale, max_pages=None):
+def run_gpu(cfg, h, dev, scale, max_pages=None, fused=0):
     from paper_2609_11133_amd import binding as B
 
     mp = h.block_table.shape[1] if max_pages is None else max_pages
-    acfg = B.make_attn_config(cfg.n_q_heads, cfg.n_kv_heads, cfg.batch, mp)
+    acfg = B.make_attn_config(cfg.n_q_heads, cfg.n_kv_heads, cfg.batch, mp, fused_merge_max_splits=fused)
     m = B.AttnDecode(acfg, device=dev)
     d = A.to_device(h, dev)
     out = torch.full((cfg.batch, cfg.n_q_heads, 128), 0x7FC1, dtype=torch.int16, device=dev)
     say(f"[attn] {cfg.name} B={cfg.batch} Hq={cfg.n_q_heads} Hkv={cfg.n_kv_heads} max_pages={mp} "
-        f"L=[{int(h.ctx.min())}, {int(h.ctx.max())}]")
+        f"L=[{int(h.ctx.min())}, {int(h.ctx.max())}] fused_merge_max_splits={fused}")
     m.forward(d["q"], d["k_cache"], d["v_cache"], h.n_pages, d["block_table"], d["ctx"], cfg.batch, scale, out)
     torch.cuda.synchronize(dev)
     return out, m, d
@@ -81,9 +82,33 @@ def test_small_cases(dev, hq, hkv):
     cfg = A.AttnConfig(f"small-{hq}x{hkv}", hq, hkv, len(SMALL_LENS), "standard")
     h = A.host_attn(cfg, seed=301 + hq, ctx=np.array(SMALL_LENS, np.int32))
     scale = 1 / np.sqrt(128)
-    out, _, _ = run_gpu(cfg, h, dev, scale)
+    out, _, _ = run_gpu(cfg, h, dev, scale)  # 5 splits at most: merged in the split kernel
     ref = oracle.attn_decode(h.q, h.k_cache, h.v_cache, h.block_table, h.ctx, scale)
     check(bf16_to_f64(out), ref, label=cfg.name)
+    out2, _, _ = run_gpu(cfg, h, dev, scale, fused=-1)  # merged by the second kernel
+    assert torch.equal(out, out2), "the two merges differ"
+
+
+@pytest.mark.parametrize("name", ["qwen3-235b-a22b-attn-agentic", "qwen3-coder-480b-a35b-tp4-attn-agentic"])
+def test_fused_merge_matches_two_kernels(dev, name):
+    """Full-size steps: the in-kernel merge (last workgroup per sequence and key/value
+    head) and the second kernel give the same bits; two further steps on the same
+    workspace, the second with fewer sequences, reuse the counters the first left at
+    zero."""
+    cfg = A.ATTN_BY_NAME[name]
+    h = A.host_attn(cfg, draw=4)
+    scale = 1 / np.sqrt(128)
+    out, m, d = run_gpu(cfg, h, dev, scale)
+    out2, _, _ = run_gpu(cfg, h, dev, scale, fused=-1)
+    assert torch.equal(out, out2)
+    out3 = torch.empty_like(out)
+    m.forward(d["q"], d["k_cache"], d["v_cache"], h.n_pages, d["block_table"], d["ctx"], cfg.batch, scale, out3)
+    nb = cfg.batch // 3
+    out4 = torch.full_like(out, 0x7FC1)
+    m.forward(d["q"], d["k_cache"], d["v_cache"], h.n_pages, d["block_table"], d["ctx"], nb, scale, out4)
+    torch.cuda.synchronize(dev)
+    assert torch.equal(out3, out) and torch.equal(out4[:nb], out[:nb])
+    assert torch.all(out4[nb:] == 0x7FC1)  # rows past the batch untouched
 
 
 def test_block_table_wider_than_contexts(dev):
