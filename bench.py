@@ -349,6 +349,16 @@ def main():
         end.record(stream)
         torch.cuda.synchronize(dev)
         ms = start.elapsed_time(end) / args.steps
+        # repetitions: five more timed regions of K steps each (median and spread)
+        reps = []
+        for _ in range(5):
+            r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            r0.record(stream)
+            for i in range(args.steps):
+                step(i)
+            r1.record(stream)
+            torch.cuda.synchronize(dev)
+            reps.append(r0.elapsed_time(r1) / args.steps)
         # per-kernel durations: K more steps with the library's stage events recording
         # each kernel on the same stream
         B.moe_decode_profile_enable(m.handle, args.steps)
@@ -368,6 +378,7 @@ def main():
         results[T] = dict(
             tokens_per_s=T / (ms * 1e-3),
             ms_per_step=ms,
+            reps_ms_per_step=dict(n=len(reps), median=statistics.median(reps), stdev=statistics.stdev(reps)),
             n_active_mean=statistics.mean(acts),
             bytes_per_step=bytes_step,
             layer_GBs=bytes_step / (ms * 1e-3) / 1e9,
@@ -379,7 +390,8 @@ def main():
             experts_frac=exp_gbs / PEAK_HBM_GBS,
             w13_bytes_per_launch=w13_bytes,
         )
-        print(f"[bench] T={T}: {results[T]['tokens_per_s']:.0f} tok/s, {ms * 1e3:.1f} us/step, layer "
+        print(f"[bench] T={T}: {results[T]['tokens_per_s']:.0f} tok/s, {ms * 1e3:.1f} us/step "
+              f"(5 reps: median {statistics.median(reps) * 1e3:.1f} +- {statistics.stdev(reps) * 1e3:.1f}), layer "
               f"{results[T]['layer_GBs']:.0f} GB/s, experts {exp_gbs:.0f} GB/s, stages(us) "
               + " ".join(f"{n}={v * 1e3:.1f}" for n, v in zip(B.STAGE_NAMES, st_ms)), file=sys.stderr, flush=True)
 

@@ -73,6 +73,12 @@ QWEN3_235B = LayerConfig("qwen3-235b-a22b", 4096, 128, 8, 1536, "bf16", "bf16", 
 QWEN3_480B = LayerConfig(
     "qwen3-coder-480b-a35b", 6144, 160, 8, 2560, "bf16", "bf16", "fp8", "normal:0.5", [1, 16, 64, 128]
 )
+# One GPU's share of the 480B layer in the paper's TP4 decode lane (Experimental Setup):
+# every expert's intermediate dimension split four ways, I = 2560 / 4 = 640 (5 blocks of
+# 128); T up to the lane's decode concurrency of 48 and beyond.
+QWEN3_480B_TP4 = LayerConfig(
+    "qwen3-coder-480b-a35b-tp4", 6144, 160, 8, 640, "bf16", "bf16", "fp8", "normal:0.5", [1, 16, 48, 64, 128]
+)
 QWEN3_480B_X12 = LayerConfig(
     "qwen3-coder-480b-a35b-x12",
     6144,
@@ -96,5 +102,5 @@ QWEN3_235B_NVFP4_ZIPF = LayerConfig(
     "qwen3-235b-a22b-nvfp4-zipf", 4096, 128, 8, 1536, "bf16", "bf16", "nvfp4", "zipf:1.1", [256]
 )
 
-ALL = [TINY, QWEN3_235B, QWEN3_480B, QWEN3_480B_X12, QWEN3_235B_MXFP4, QWEN3_235B_NVFP4, QWEN3_235B_NVFP4_ZIPF]
+ALL = [TINY, QWEN3_235B, QWEN3_480B, QWEN3_480B_TP4, QWEN3_480B_X12, QWEN3_235B_MXFP4, QWEN3_235B_NVFP4, QWEN3_235B_NVFP4_ZIPF]
 BY_NAME = {c.name: c for c in ALL}

@@ -431,6 +431,17 @@ def test_full_480b(dev, full_480b, T):
     _full(run, C.QWEN3_480B, T, batch=T)
 
 
+@pytest.mark.parametrize("T", [1, 48])
+def test_full_480b_tp4_shard(dev, T):
+    """One GPU's share of the 480B layer in a TP4 decode lane (I = 640, five 128-blocks):
+    the down projection's K spans five blocks, the gate/up projection's 48."""
+    cfg = C.QWEN3_480B_TP4
+    say("[gen] qwen3-coder-480b-a35b tp4 shard")
+    hl = W.host_layer(cfg)
+    run = Run(cfg, hl, dev, max_tokens=max(cfg.tokens))
+    _full(run, cfg, T, batch=T)
+
+
 def test_stack_480b_back_to_back(dev, full_480b):
     """Twelve 480B-shaped layers decoded back to back at T=256 on one handle and one
     stream with no synchronisation between them: expert weights at twelve distinct
