@@ -91,6 +91,9 @@ def parse():
     ap.add_argument("--stack", action="store_true",
                     help="also time the stack of 12 distinct 480B-shaped layers decoded back to back, T = 1..256")
     ap.add_argument("--stack-steps", type=int, default=20)
+    ap.add_argument("--layout", choices=["packed", "row-major"], default=None,
+                    help="expert weight layout: packed 16-row tiles (default for FP8 and MXFP4; converted once at "
+                         "setup by moe_decode_pack_weights) or row-major (always for NVFP4)")
     ap.add_argument("--screen-min-tokens", type=int, default=0,
                     help="tokens per step from which routing screens the logits (0: library default, -1: never)")
     ap.add_argument("--mstar", type=int, default=0,
@@ -315,11 +318,18 @@ def main():
     xs = {T: [W.to_device(W.host_x(cfg, T, batch=b), dev) for b in range(pool)] for T in sweep_T}
     rw, bias = W.to_device(hl.router_w, dev), W.to_device(hl.bias, dev)
     ew0, sc0 = W.to_device(hl.expert_w, dev), W.to_device(hl.scales, dev)
+    layout = 1 if (args.layout or ("row-major" if cfg.wfmt == "nvfp4" else "packed")) == "packed" else 0
+    bcfg = W.binding_config(cfg, Tmax, args.mstar, args.screen_min_tokens, layout)
+    if layout:  # weights converted once, as at load time
+        packed = torch.empty_like(ew0)
+        B.moe_decode_pack_weights(bcfg, torch.cuda.current_stream(dev).cuda_stream, ew0, packed, cfg.n_experts)
+        torch.cuda.synchronize(dev)
+        ew0 = packed
     ews = [ew0] + [ew0.clone() for _ in range(copies - 1)]
     scs = [sc0] + [sc0.clone() for _ in range(copies - 1)]
     setup_s = time.time() - t0
 
-    m = B.MoEDecode(W.binding_config(cfg, Tmax, args.mstar, args.screen_min_tokens), device=dev)
+    m = B.MoEDecode(bcfg, device=dev)
     stream = torch.cuda.current_stream(dev)
     Be = cfg.expert_bytes()
     results = {}
@@ -495,7 +505,8 @@ def main():
                         f"T={T_main} tokens per step",
             "tokens_per_step": T_main,
             "weights": {"fp8": "fp8-e4m3, fp32 scale per 128x128 block", "mxfp4": "mxfp4 (e2m1 + e8m0/32)",
-                        "nvfp4": "nvfp4 (e2m1 + e4m3/16 + fp32/matrix)"}[cfg.wfmt],
+                        "nvfp4": "nvfp4 (e2m1 + e4m3/16 + fp32/matrix)"}[cfg.wfmt]
+                       + (", packed 16-row tiles" if layout else ", row-major"),
             "activations": cfg.act,
             "cold_cache": f"{copies} weight copies x 16 token batches cycled",
         },

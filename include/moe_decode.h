@@ -83,6 +83,19 @@ typedef enum {
                                     needs bf16 activations */
 } moe_wfmt;
 
+typedef enum {
+    MOE_WLAYOUT_ROW_MAJOR = 0, /* every matrix [rows][K], K contiguous (the layout above) */
+    MOE_WLAYOUT_TILED16 = 1    /* packed 16-row tiles: each tile of 16 rows keeps its offset
+                                  and size, and inside it each 128-input K block is one
+                                  contiguous piece of the tile's 16 row segments in the
+                                  matrix cores' operand order (FP8: 2 KB, the bytes K
+                                  [16g, 16g+16) of row l%16 at 16 l and K [64+16g, +16) at
+                                  1024 + 16 l, g = l/16, l < 64; MXFP4: 1 KB, K [32g, 32g+32)
+                                  of row l%16 at 16 l).  Written by moe_decode_pack_weights.
+                                  FP8 and MXFP4 only, with MFMA tiles for every expert
+                                  (mfma_min_tokens 0 or 1); scales are unchanged. */
+} moe_wlayout;
+
 typedef struct moe_decode_config {
     int32_t hidden;          /* H: multiple of 128 (FP8) or 256 (MXFP4, NVFP4) */
     int32_t n_experts;       /* E: 1..1024 */
@@ -96,6 +109,7 @@ typedef struct moe_decode_config {
                                 MFMA tiles, below it on the GEMV path; 0 = library default
                                 (1: MFMA for every expert, the faster path on MI355X at
                                 every measured token count), negative = never */
+    int32_t weight_layout;   /* moe_wlayout of expert_w */
     int32_t screen_min_tokens; /* a forward step with at least this many tokens screens the
                                 router logits: bf16 matrix-core sums give every logit a
                                 rigorous bracket, and only the experts whose bracket can
@@ -103,7 +117,7 @@ typedef struct moe_decode_config {
                                 the same); needs bf16 x and router_w and H a multiple of
                                 256.  0 = library default (the smallest T with
                                 T*E*H >= 2^26 multiply-adds), negative = never */
-    int32_t reserved[6];     /* must be zero */
+    int32_t reserved[5];     /* must be zero */
 } moe_decode_config;
 
 typedef struct moe_decode_stats {
@@ -148,6 +162,16 @@ moe_status moe_decode_forward(moe_decode_t h, void *stream, const void *x, int32
                               const float *router_bias, const void *expert_w, const void *scales, int32_t topk,
                               void *y, int32_t *topk_ids, float *topk_weights);
 
+/* Enqueue on `stream` the conversion of n_experts consecutive experts' weights from
+ * the row-major layout (src) to packed 16-row tiles (dst), for a handle whose
+ * configuration has weight_layout = MOE_WLAYOUT_TILED16 (the other fields as for that
+ * handle; weight_layout itself is not read).  src and dst are device buffers of
+ * n_experts * moe_decode_expert_weight_bytes(cfg) bytes, 16-byte aligned, owned by the
+ * caller, not overlapping.  FP8 and MXFP4 weights; scales need no conversion.  Errors
+ * as for moe_decode_init (message in moe_decode_last_error(NULL)). */
+moe_status moe_decode_pack_weights(const moe_decode_config *cfg, void *stream, const void *src, void *dst,
+                                   int32_t n_experts);
+
 /* Steps 1-2 only (router logits and top-k softmax).  `logits` [T][E] fp32 receives
  * the canonical logits if not NULL; topk_ids / topk_weights as in forward. */
 moe_status moe_decode_route(moe_decode_t h, void *stream, const void *x, int32_t n_tokens, const void *router_w,
@@ -176,7 +200,7 @@ void moe_decode_free(moe_decode_t h);
 const char *moe_decode_status_string(moe_status s);
 
 /* Text of the last error on this handle ("" if none); for a NULL handle, the last
- * error of a failed moe_decode_init in this thread. */
+ * error of a failed moe_decode_init or moe_decode_pack_weights in this thread. */
 const char *moe_decode_last_error(moe_decode_t h);
 
 #ifdef __cplusplus

@@ -19,6 +19,7 @@ MOE_OK, MOE_ERR_INVALID, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP = 0
 MOE_DTYPE_F32, MOE_DTYPE_BF16 = 0, 1
 MOE_WFMT_FP8_E4M3_B128, MOE_WFMT_MXFP4_E2M1_B32, MOE_WFMT_NVFP4_E2M1_B16 = 0, 1, 2
 MOE_STAGE_ROUTE, MOE_STAGE_W13, MOE_STAGE_W2, MOE_STAGE_COMBINE, MOE_N_STAGES = 0, 1, 2, 3, 4
+MOE_WLAYOUT_ROW_MAJOR, MOE_WLAYOUT_TILED16 = 0, 1
 STAGE_NAMES = ["route", "w13", "w2", "combine"]
 
 
@@ -33,8 +34,9 @@ class moe_decode_config(ctypes.Structure):
         ("router_dtype", ctypes.c_int32),
         ("wfmt", ctypes.c_int32),
         ("mfma_min_tokens", ctypes.c_int32),
+        ("weight_layout", ctypes.c_int32),
         ("screen_min_tokens", ctypes.c_int32),
-        ("reserved", ctypes.c_int32 * 6),
+        ("reserved", ctypes.c_int32 * 5),
     ]
 
 
@@ -94,6 +96,8 @@ def lib():
         L.moe_decode_init.argtypes = [cfgp, P, SZ, ctypes.POINTER(P)]
         L.moe_decode_forward.restype = ctypes.c_int
         L.moe_decode_forward.argtypes = [P, P, P, I32, P, P, P, P, I32, P, P, P]
+        L.moe_decode_pack_weights.restype = ctypes.c_int
+        L.moe_decode_pack_weights.argtypes = [cfgp, P, P, P, I32]
         L.moe_decode_route.restype = ctypes.c_int
         L.moe_decode_route.argtypes = [P, P, P, I32, P, P, I32, P, P, P]
         L.moe_decode_get_stats.restype = ctypes.c_int
@@ -137,11 +141,12 @@ def _check(status: int, handle=None):
 
 def make_config(hidden, n_experts, inter, max_topk, max_tokens, act_dtype=MOE_DTYPE_BF16,
                 router_dtype=MOE_DTYPE_BF16, wfmt=MOE_WFMT_FP8_E4M3_B128, mfma_min_tokens=0,
-                screen_min_tokens=0) -> moe_decode_config:
+                screen_min_tokens=0, weight_layout=0) -> moe_decode_config:
     c = moe_decode_config()
     c.hidden, c.n_experts, c.inter, c.max_topk, c.max_tokens = hidden, n_experts, inter, max_topk, max_tokens
     c.act_dtype, c.router_dtype, c.wfmt, c.mfma_min_tokens = act_dtype, router_dtype, wfmt, mfma_min_tokens
     c.screen_min_tokens = screen_min_tokens
+    c.weight_layout = weight_layout
     return c
 
 
@@ -168,6 +173,11 @@ def moe_decode_forward(h, stream, x, n_tokens, router_w, router_bias, expert_w, 
     _check(lib().moe_decode_forward(h, stream, _addr(x), n_tokens, _addr(router_w), _addr(router_bias),
                                     _addr(expert_w), _addr(scales), topk, _addr(y), _addr(topk_ids),
                                     _addr(topk_weights)), h)
+
+
+def moe_decode_pack_weights(cfg: moe_decode_config, stream, src, dst, n_experts: int):
+    """Enqueue the row-major -> packed 16-row tile conversion of n_experts experts."""
+    _check(lib().moe_decode_pack_weights(ctypes.byref(cfg), stream, _addr(src), _addr(dst), n_experts))
 
 
 def moe_decode_route(h, stream, x, n_tokens, router_w, router_bias, topk, logits=None, topk_ids=None,

@@ -93,7 +93,7 @@ static const int kDefaultMfmaMinTokens = 1;
 static moe_status check_config(const moe_decode_config *c, char *err)
 {
     if (!c) FAIL(err, MOE_ERR_INVALID, "config is NULL");
-    for (int i = 0; i < 6; ++i)
+    for (int i = 0; i < 5; ++i)
         if (c->reserved[i] != 0) FAIL(err, MOE_ERR_INVALID, "config.reserved[%d] must be zero", i);
     if (c->wfmt != MOE_WFMT_FP8_E4M3_B128 && c->wfmt != MOE_WFMT_MXFP4_E2M1_B32 && c->wfmt != MOE_WFMT_NVFP4_E2M1_B16)
         FAIL(err, MOE_ERR_INVALID, "unknown weight format %d", c->wfmt);
@@ -111,6 +111,12 @@ static moe_status check_config(const moe_decode_config *c, char *err)
         FAIL(err, MOE_ERR_INVALID, "unknown act_dtype %d", c->act_dtype);
     if (c->router_dtype != MOE_DTYPE_F32 && c->router_dtype != MOE_DTYPE_BF16)
         FAIL(err, MOE_ERR_INVALID, "unknown router_dtype %d", c->router_dtype);
+    if (c->weight_layout != MOE_WLAYOUT_ROW_MAJOR && c->weight_layout != MOE_WLAYOUT_TILED16)
+        FAIL(err, MOE_ERR_INVALID, "unknown weight_layout %d", c->weight_layout);
+    if (c->weight_layout == MOE_WLAYOUT_TILED16 && c->wfmt == MOE_WFMT_NVFP4_E2M1_B16)
+        FAIL(err, MOE_ERR_UNSUPPORTED, "packed 16-row tiles are for FP8 and MXFP4 weights");
+    if (c->weight_layout == MOE_WLAYOUT_TILED16 && c->mfma_min_tokens != 0 && c->mfma_min_tokens != 1)
+        FAIL(err, MOE_ERR_UNSUPPORTED, "packed 16-row tiles need MFMA tiles for every expert (mfma_min_tokens 0 or 1)");
     if (c->wfmt == MOE_WFMT_NVFP4_E2M1_B16 && c->act_dtype != MOE_DTYPE_BF16)
         FAIL(err, MOE_ERR_UNSUPPORTED, "NVFP4 weights need bf16 activations (the bf16 matrix cores take x as it is)");
     {
@@ -173,6 +179,7 @@ moe_status moe_decode_init(const moe_decode_config *cfg, void *workspace, size_t
     h->L.wfmt = cfg->wfmt;
     h->L.act_bf16 = cfg->act_dtype == MOE_DTYPE_BF16;
     h->L.router_bf16 = cfg->router_dtype == MOE_DTYPE_BF16;
+    h->L.wlayout = cfg->weight_layout;
     h->L.expert_w_bytes = moe_decode_expert_weight_bytes(cfg);
     h->L.expert_s_bytes = moe_decode_expert_scale_bytes(cfg);
     carve_workspace(cfg->hidden, cfg->n_experts, cfg->inter, cfg->max_topk, cfg->max_tokens, cfg->wfmt, workspace,
@@ -194,6 +201,32 @@ moe_status moe_decode_init(const moe_decode_config *cfg, void *workspace, size_t
     h->prof_cap = h->prof_n = 0;
     h->prof_ev = nullptr;
     *out = h;
+    return MOE_OK;
+}
+
+moe_status moe_decode_pack_weights(const moe_decode_config *cfg, void *stream, const void *src, void *dst,
+                                   int32_t n_experts)
+{
+    g_init_err[0] = 0;
+    moe_status s = check_config(cfg, g_init_err);
+    if (s != MOE_OK) return s;
+    if (cfg->wfmt == MOE_WFMT_NVFP4_E2M1_B16)
+        FAIL(g_init_err, MOE_ERR_UNSUPPORTED, "packed 16-row tiles are for FP8 and MXFP4 weights");
+    if (n_experts < 1 || n_experts > cfg->n_experts)
+        FAIL(g_init_err, MOE_ERR_INVALID, "n_experts=%d outside 1..%d", n_experts, cfg->n_experts);
+    if (!src || !dst) FAIL(g_init_err, MOE_ERR_INVALID, "src or dst is NULL");
+    if ((uintptr_t)src % 16 || (uintptr_t)dst % 16) FAIL(g_init_err, MOE_ERR_INVALID, "src and dst must be 16-byte aligned");
+    const size_t bytes = (size_t)n_experts * moe_decode_expert_weight_bytes(cfg);
+    const uintptr_t a = (uintptr_t)src, b = (uintptr_t)dst;
+    if (a < b + bytes && b < a + bytes) FAIL(g_init_err, MOE_ERR_INVALID, "src and dst overlap");
+    Layer L = {};
+    L.H = cfg->hidden;
+    L.E = cfg->n_experts;
+    L.I = cfg->inter;
+    L.wfmt = cfg->wfmt;
+    L.expert_w_bytes = moe_decode_expert_weight_bytes(cfg);
+    if (launch_pack_weights(L, src, dst, n_experts, (hipStream_t)stream) != hipSuccess)
+        FAIL(g_init_err, MOE_ERR_HIP, "pack kernel launch failed");
     return MOE_OK;
 }
 

@@ -83,6 +83,7 @@ struct Layer {
                     // 2 NVFP4 (E4M3 per 16 + fp32 per matrix)
     int act_bf16;   // activations bf16 (1) or fp32 (0)
     int router_bf16;
+    int wlayout;    // expert weights: 0 row-major, 1 packed 16-row tiles (FP8, MXFP4)
     size_t expert_w_bytes;  // per expert
     size_t expert_s_bytes;  // per expert
 };
@@ -110,6 +111,7 @@ struct RouteParams {
 // ---- launchers (all enqueue on `st`, return hipGetLastError())
 hipError_t launch_zero(int32_t *p, int n, hipStream_t st);
 hipError_t launch_route(const Layer &L, const RouteParams &P, hipStream_t st);
+hipError_t launch_pack_weights(const Layer &L, const void *src, void *dst, int n_experts, hipStream_t st);
 hipError_t launch_w13(const Layer &L, const void *expert_w, const void *scales, const void *x, int T, int k,
                       const int32_t *meta, const int32_t *tok_of, float *h, hipStream_t st);
 hipError_t launch_w2(const Layer &L, const void *expert_w, const void *scales, int T, int k, const int32_t *meta,

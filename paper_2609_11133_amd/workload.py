@@ -76,7 +76,8 @@ def y_to_f64(y) -> np.ndarray:
     return y.detach().to("cpu", torch.float64).numpy()
 
 
-def binding_config(cfg: LayerConfig, max_tokens: int, mfma_min_tokens: int = 0, screen_min_tokens: int = 0):
+def binding_config(cfg: LayerConfig, max_tokens: int, mfma_min_tokens: int = 0, screen_min_tokens: int = 0,
+                   weight_layout: int = 0):
     from . import binding as B
 
     return B.make_config(
@@ -84,4 +85,5 @@ def binding_config(cfg: LayerConfig, max_tokens: int, mfma_min_tokens: int = 0, 
         act_dtype=B.MOE_DTYPE_BF16 if cfg.act == "bf16" else B.MOE_DTYPE_F32,
         router_dtype=B.MOE_DTYPE_BF16 if cfg.router == "bf16" else B.MOE_DTYPE_F32,
         wfmt=cfg.wfmt_id, mfma_min_tokens=mfma_min_tokens, screen_min_tokens=screen_min_tokens,
+        weight_layout=weight_layout,
     )

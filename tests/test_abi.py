@@ -281,3 +281,49 @@ def test_struct_sizes_match_header(B):
     assert B.moe_decode_workspace_bytes(c) > 0
     c.screen_min_tokens = 7
     assert B.moe_decode_workspace_bytes(c) > 0
+
+
+# ---------------------------------------------------------------- packed 16-row tile layout
+
+@pytest.mark.parametrize(
+    "kw,code",
+    [
+        (dict(weight_layout=2), -1),
+        (dict(weight_layout=1, wfmt=2), -2),  # NVFP4 weights stay row-major
+        (dict(weight_layout=1, mfma_min_tokens=-1), -2),  # the GEMV path reads row-major weights
+        (dict(weight_layout=1, mfma_min_tokens=4), -2),
+    ],
+)
+def test_weight_layout_checks(B, kw, code):
+    c = cfg(B, **kw)
+    assert B.moe_decode_workspace_bytes(c) == 0
+    with pytest.raises(B.MoEDecodeError) as e:
+        B.moe_decode_init(c, 256, 1 << 30)
+    assert e.value.status == code
+
+
+def test_weight_layout_accepted(B):
+    for wfmt in (0, 1):
+        for mm in (0, 1):
+            assert B.moe_decode_workspace_bytes(cfg(B, weight_layout=1, wfmt=wfmt, mfma_min_tokens=mm)) > 0
+
+
+@pytest.mark.parametrize(
+    "change,needle",
+    [
+        (dict(n_experts=0), "n_experts"),
+        (dict(n_experts=17), "n_experts"),
+        (dict(src=0), "NULL"),
+        (dict(dst=8), "aligned"),
+        (dict(dst=256 + 1024), "overlap"),
+        (dict(wfmt=2), "FP8 and MXFP4"),
+    ],
+)
+def test_pack_validates_before_launch(B, change, needle):
+    """Every check of moe_decode_pack_weights fails before a launch (fake pointers)."""
+    args = dict(n_experts=2, src=256, dst=1 << 30, wfmt=0)
+    args.update(change)
+    c = cfg(B, wfmt=args["wfmt"])
+    with pytest.raises(B.MoEDecodeError) as e:
+        B.moe_decode_pack_weights(c, None, args["src"], args["dst"], args["n_experts"])
+    assert needle in str(e.value)

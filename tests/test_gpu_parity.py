@@ -39,15 +39,21 @@ def dev():
 
 
 class Run:
-    def __init__(self, cfg, hl, dev, max_tokens, mfma_min_tokens=0, screen_min_tokens=0):
+    def __init__(self, cfg, hl, dev, max_tokens, mfma_min_tokens=0, screen_min_tokens=0, weight_layout=0):
         from paper_2609_11133_amd import binding as B
 
         self.cfg, self.hl, self.dev = cfg, hl, dev
-        self.m = B.MoEDecode(W.binding_config(cfg, max_tokens, mfma_min_tokens, screen_min_tokens), device=dev)
+        bc = W.binding_config(cfg, max_tokens, mfma_min_tokens, screen_min_tokens, weight_layout)
+        self.m = B.MoEDecode(bc, device=dev)
         self.rw = W.to_device(hl.router_w, dev)
         self.bias = W.to_device(hl.bias, dev)
         self.ew = W.to_device(hl.expert_w, dev)
         self.sc = W.to_device(hl.scales, dev)
+        if weight_layout == 1:  # the library's own conversion of the row-major weights
+            packed = torch.empty_like(self.ew)
+            B.moe_decode_pack_weights(bc, torch.cuda.current_stream(dev).cuda_stream, self.ew, packed, cfg.n_experts)
+            torch.cuda.synchronize(dev)
+            self.ew = packed
 
     def forward(self, x, topk=None):
         k = topk or self.cfg.topk
@@ -344,6 +350,80 @@ def test_lds_staged_kernels(dev, cfg, T):
 # Seeded random small layers across the accepted shapes: weight formats, activation
 # and router dtypes, bias recipes, K extents that take the staged or the two-tile
 # kernels, top-k up to 16 and ragged token counts.
+# ---------------------------------------------------------------- packed 16-row tile layout
+
+def pack_reference(expert_w, cfg):
+    """Packed 16-row tiles from row-major expert weights (uint8 [E][bytes]), written
+    from the layout's definition: per matrix [rows][K] and per (16-row tile, 128-input
+    K block), lane l's operand bytes of row l%16 in lane order."""
+    fp4 = cfg.wfmt == "mxfp4"
+    H, I = cfg.hidden, cfg.inter
+    ew = expert_w.reshape(cfg.n_experts, -1)
+    out = np.empty_like(ew)
+    for rows, K, off in ((2 * I, H, 0), (H, I, 2 * I * H // (2 if fp4 else 1))):
+        rowb = K // 2 if fp4 else K
+        m = ew[:, off: off + rows * rowb].reshape(cfg.n_experts, rows // 16, 16, K // 128, 64 if fp4 else 128)
+        if fp4:  # [E][tile][r][kb][g*16+i] -> [E][tile][kb][g][r][i]
+            v = m.reshape(cfg.n_experts, rows // 16, 16, K // 128, 4, 16).transpose(0, 1, 3, 4, 2, 5)
+        else:  # [E][tile][r][kb][half*64+g*16+i] -> [E][tile][kb][half][g][r][i]
+            v = m.reshape(cfg.n_experts, rows // 16, 16, K // 128, 2, 4, 16).transpose(0, 1, 3, 4, 5, 2, 6)
+        out[:, off: off + rows * rowb] = v.reshape(cfg.n_experts, -1)
+    return out.reshape(expert_w.shape)
+
+
+@pytest.mark.parametrize("cfg", [SMALL_FP8, SMALL_MX], ids=["fp8", "mxfp4"])
+def test_pack_matches_layout_definition(dev, cfg):
+    from paper_2609_11133_amd import binding as B
+
+    hl = W.host_layer(cfg, seed=560)
+    bc = W.binding_config(cfg, 8, weight_layout=1)
+    src = W.to_device(hl.expert_w, dev)
+    dst = torch.zeros_like(src)
+    B.moe_decode_pack_weights(bc, torch.cuda.current_stream(dev).cuda_stream, src, dst, cfg.n_experts)
+    torch.cuda.synchronize(dev)
+    got = dst.cpu().numpy().view(np.uint8).reshape(hl.expert_w.view(np.uint8).shape)
+    assert np.array_equal(got, pack_reference(hl.expert_w.view(np.uint8), cfg))
+
+
+# every kernel variant on packed weights: FP8 staged gate/up (H/128 a multiple of 4) and
+# two-tile gate/up (H = 384), two-tile down (I/128 < 16) and staged down (I = 2048);
+# E2M1 staged (H, I multiples of 512) and two-tile (H = I = 768) kernels
+PACKED_CFGS = [
+    LayerConfig("pk-fp8", 512, 16, 4, 256, "bf16", "bf16", "fp8", "normal:0.5", []),
+    LayerConfig("pk-fp8-h384", 384, 16, 4, 2048, "bf16", "bf16", "fp8", None, []),
+    LayerConfig("pk-mx", 512, 16, 4, 512, "bf16", "bf16", "mxfp4", "zipf:1.1", []),
+    LayerConfig("pk-mx-768", 768, 16, 4, 768, "bf16", "bf16", "mxfp4", None, []),
+    LayerConfig("pk-f32-mx", 256, 8, 2, 256, "f32", "f32", "mxfp4", None, []),
+]
+
+
+@pytest.mark.parametrize("cfg", PACKED_CFGS, ids=[c.name for c in PACKED_CFGS])
+@pytest.mark.parametrize("T", [1, 13, 40])
+def test_packed_layout_layers(dev, cfg, T):
+    hl = W.host_layer(cfg, seed=561)
+    run = Run(cfg, hl, dev, max_tokens=40, weight_layout=1)
+    check_layer(run, W.host_x(cfg, T, seed=561), label=f"{cfg.name} packed T={T}")
+
+
+@pytest.mark.parametrize("T", [1, 64])
+def test_full_235b_packed(dev, full_235b, T):
+    """The 235B-shaped layer on packed weights (staged gate/up, the 12-block down)."""
+    run = Run(C.QWEN3_235B, full_235b, dev, max_tokens=64, weight_layout=1)
+    _full(run, C.QWEN3_235B, T, batch=T)
+
+
+def test_full_480b_packed(dev, full_480b):
+    run = Run(C.QWEN3_480B, full_480b, dev, max_tokens=128, weight_layout=1)
+    _full(run, C.QWEN3_480B, 128, batch=5)
+
+
+def test_full_mxfp4_zipf_packed(dev):
+    cfg = C.QWEN3_235B_MXFP4
+    hl = W.host_layer(cfg)
+    run = Run(cfg, hl, dev, max_tokens=256, weight_layout=1)
+    _full(run, cfg, 256, batch=6)
+
+
 def _random_layer(i):
     rng = np.random.default_rng(9000 + i)
     wfmt = ["fp8", "mxfp4"][i % 2]
