@@ -8,6 +8,11 @@
 //          tiles     16-row x 128-byte tiles of 4096-byte rows, each lane two 16-byte
 //                    pieces (the FP8 MFMA operand shape), rows streamed in K order
 //          tiles_nt  the same with non-temporal loads
+//          deep_nt   contiguous, each workgroup sixteen 4 KB pieces in flight (16 loads per
+//                    lane), non-temporal, 512 workgroups walking the buffer
+//          packed_nt 16-row tiles stored as contiguous 2 KB K blocks (the packed weight
+//                    layout): each lane 16 bytes at 16l and 1024 + 16l of a block, eight
+//                    blocks in flight, non-temporal
 //          copy      contiguous 16-byte copy (reads and writes MiB each)
 // Prints one line: mode, bytes moved per launch, mean ms, GB/s.
 #include <hip/hip_runtime.h>
@@ -59,6 +64,46 @@ __global__ __launch_bounds__(256) void tiles_kernel(const uint8_t *__restrict__ 
     if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9E3779B9u) sink[0] = 1;
 }
 
+// Workgroup b of G takes pieces b, b+G, ... of U*256 16-byte elements, all U loads of
+// a piece in flight together.
+template <int U>
+__global__ __launch_bounds__(256) void deep_kernel(const u32x4 *__restrict__ a, size_t n, uint32_t *__restrict__ sink)
+{
+    const size_t per = (size_t)U * 256, pieces = n / per;
+    u32x4 acc = {0, 0, 0, 0};
+    for (size_t pc = blockIdx.x; pc < pieces; pc += gridDim.x) {
+        const u32x4 *q = a + pc * per + threadIdx.x;
+        u32x4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = ld<true>(q + 256 * u);
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc ^= v[u];
+    }
+    if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9E3779B9u) sink[0] = 1;
+}
+
+// Each wave streams one packed tile (64 KB: 32 K blocks of 2 KB), eight blocks in flight.
+__global__ __launch_bounds__(256) void packed_kernel(const uint8_t *__restrict__ a, size_t n_tiles,
+                                                     uint32_t *__restrict__ sink)
+{
+    const int lane = threadIdx.x & 63;
+    u32x4 acc = {0, 0, 0, 0};
+    for (size_t t = (size_t)blockIdx.x * 4 + (threadIdx.x >> 6); t < n_tiles; t += (size_t)gridDim.x * 4) {
+        const uint8_t *tile = a + t * 16 * 4096 + 16 * lane;
+        for (int kb0 = 0; kb0 < 32; kb0 += 8) {
+            u32x4 v[8][2];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                v[u][0] = ld<true>(reinterpret_cast<const u32x4 *>(tile + (kb0 + u) * 2048));
+                v[u][1] = ld<true>(reinterpret_cast<const u32x4 *>(tile + (kb0 + u) * 2048 + 1024));
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u) acc ^= v[u][0] ^ v[u][1];
+        }
+    }
+    if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9E3779B9u) sink[0] = 1;
+}
+
 __global__ __launch_bounds__(256) void copy_kernel(const u32x4 *__restrict__ a, u32x4 *__restrict__ b, size_t n)
 {
     const size_t stride = (size_t)gridDim.x * blockDim.x;
@@ -77,7 +122,7 @@ __global__ __launch_bounds__(256) void copy_kernel(const u32x4 *__restrict__ a, 
 int main(int argc, char **argv)
 {
     if (argc < 4) {
-        fprintf(stderr, "usage: %s read|read_nt|tiles|tiles_nt|copy MiB iters\n", argv[0]);
+        fprintf(stderr, "usage: %s read|read_nt|tiles|tiles_nt|deep_nt|packed_nt|copy MiB iters\n", argv[0]);
         return 2;
     }
     const char *mode = argv[1];
@@ -110,6 +155,10 @@ int main(int argc, char **argv)
             tiles_kernel<false><<<grid, 256>>>(a, n_tiles, sink);
         else if (!strcmp(mode, "tiles_nt"))
             tiles_kernel<true><<<grid, 256>>>(a, n_tiles, sink);
+        else if (!strcmp(mode, "deep_nt"))
+            deep_kernel<16><<<512, 256>>>((const u32x4 *)a, n16, sink);
+        else if (!strcmp(mode, "packed_nt"))
+            packed_kernel<<<cus * 4, 256>>>(a, n_tiles, sink);
         else if (copy)
             copy_kernel<<<grid, 256>>>((const u32x4 *)a, (u32x4 *)b, n16);
         else {
