@@ -165,15 +165,22 @@ def run_stack(args, dev):
     from paper_2609_11133_amd import workload as W
 
     cfg = C.QWEN3_480B_X12
+    layout = 0 if args.layout == "row-major" else 1
+    bcfg = W.binding_config(cfg, max(cfg.tokens), args.mstar, args.screen_min_tokens, layout)
     t0 = time.time()
     layers = []
     for li in range(cfg.layers):
         hl = W.host_layer(cfg, layer=li)
-        layers.append((W.to_device(hl.router_w, dev), W.to_device(hl.bias, dev), W.to_device(hl.expert_w, dev),
-                       W.to_device(hl.scales, dev)))
+        ew = W.to_device(hl.expert_w, dev)
+        if layout:  # converted once per layer, as at load time
+            packed = torch.empty_like(ew)
+            B.moe_decode_pack_weights(bcfg, torch.cuda.current_stream(dev).cuda_stream, ew, packed, cfg.n_experts)
+            torch.cuda.synchronize(dev)
+            ew = packed
+        layers.append((W.to_device(hl.router_w, dev), W.to_device(hl.bias, dev), ew, W.to_device(hl.scales, dev)))
         del hl
         print(f"[stack] layer {li} resident ({time.time() - t0:.0f} s)", file=sys.stderr, flush=True)
-    m = B.MoEDecode(W.binding_config(cfg, max(cfg.tokens), args.mstar, args.screen_min_tokens), device=dev)
+    m = B.MoEDecode(bcfg, device=dev)
     stream = torch.cuda.current_stream(dev)
     Be = cfg.expert_bytes()
     out = {}
@@ -211,7 +218,8 @@ def run_stack(args, dev):
     del layers
     torch.cuda.empty_cache()
     return dict(workload=f"{cfg.layers} distinct {cfg.name[:-4]}-shaped layers (H {cfg.hidden}, {cfg.n_experts} "
-                         f"experts, top-{cfg.topk}, I {cfg.inter}, fp8), back to back, "
+                         f"experts, top-{cfg.topk}, I {cfg.inter}, fp8, "
+                         f"{'packed 16-row tiles' if layout else 'row-major'}), back to back, "
                          f"{cfg.layers * cfg.n_experts * Be / 1e9:.1f} GB of expert weights",
                 steps=args.stack_steps, by_tokens=out)
 
