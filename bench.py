@@ -92,8 +92,8 @@ def parse():
                     help="also time the stack of 12 distinct 480B-shaped layers decoded back to back, T = 1..256")
     ap.add_argument("--stack-steps", type=int, default=20)
     ap.add_argument("--layout", choices=["packed", "row-major"], default=None,
-                    help="expert weight layout: packed 16-row tiles (default for FP8 and MXFP4; converted once at "
-                         "setup by moe_decode_pack_weights) or row-major (always for NVFP4)")
+                    help="expert weight layout: packed 16-row tiles (default; converted once at setup by "
+                         "moe_decode_pack_weights) or row-major")
     ap.add_argument("--screen-min-tokens", type=int, default=0,
                     help="tokens per step from which routing screens the logits (0: library default, -1: never)")
     ap.add_argument("--mstar", type=int, default=0,
@@ -326,7 +326,7 @@ def main():
     xs = {T: [W.to_device(W.host_x(cfg, T, batch=b), dev) for b in range(pool)] for T in sweep_T}
     rw, bias = W.to_device(hl.router_w, dev), W.to_device(hl.bias, dev)
     ew0, sc0 = W.to_device(hl.expert_w, dev), W.to_device(hl.scales, dev)
-    layout = 1 if (args.layout or ("row-major" if cfg.wfmt == "nvfp4" else "packed")) == "packed" else 0
+    layout = 0 if args.layout == "row-major" else 1
     bcfg = W.binding_config(cfg, Tmax, args.mstar, args.screen_min_tokens, layout)
     if layout:  # weights converted once, as at load time
         packed = torch.empty_like(ew0)

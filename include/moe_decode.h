@@ -91,9 +91,11 @@ typedef enum {
                                   matrix cores' operand order (FP8: 2 KB, the bytes K
                                   [16g, 16g+16) of row l%16 at 16 l and K [64+16g, +16) at
                                   1024 + 16 l, g = l/16, l < 64; MXFP4: 1 KB, K [32g, 32g+32)
-                                  of row l%16 at 16 l).  Written by moe_decode_pack_weights.
-                                  FP8 and MXFP4 only, with MFMA tiles for every expert
-                                  (mfma_min_tokens 0 or 1); scales are unchanged. */
+                                  of row l%16 at 16 l; NVFP4: 256-input blocks of 2 KB,
+                                  row l%16's bytes [32g, 32g+16) at 16 l and [32g+16,
+                                  32g+32) at 1024 + 16 l).  Written by
+                                  moe_decode_pack_weights.  Needs MFMA tiles for every
+                                  expert (mfma_min_tokens 0 or 1); scales are unchanged. */
 } moe_wlayout;
 
 typedef struct moe_decode_config {
@@ -167,7 +169,7 @@ moe_status moe_decode_forward(moe_decode_t h, void *stream, const void *x, int32
  * configuration has weight_layout = MOE_WLAYOUT_TILED16 (the other fields as for that
  * handle; weight_layout itself is not read).  src and dst are device buffers of
  * n_experts * moe_decode_expert_weight_bytes(cfg) bytes, 16-byte aligned, owned by the
- * caller, not overlapping.  FP8 and MXFP4 weights; scales need no conversion.  Errors
+ * caller, not overlapping.  Scales need no conversion.  Errors
  * as for moe_decode_init (message in moe_decode_last_error(NULL)). */
 moe_status moe_decode_pack_weights(const moe_decode_config *cfg, void *stream, const void *src, void *dst,
                                    int32_t n_experts);

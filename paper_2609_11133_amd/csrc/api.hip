@@ -113,8 +113,6 @@ static moe_status check_config(const moe_decode_config *c, char *err)
         FAIL(err, MOE_ERR_INVALID, "unknown router_dtype %d", c->router_dtype);
     if (c->weight_layout != MOE_WLAYOUT_ROW_MAJOR && c->weight_layout != MOE_WLAYOUT_TILED16)
         FAIL(err, MOE_ERR_INVALID, "unknown weight_layout %d", c->weight_layout);
-    if (c->weight_layout == MOE_WLAYOUT_TILED16 && c->wfmt == MOE_WFMT_NVFP4_E2M1_B16)
-        FAIL(err, MOE_ERR_UNSUPPORTED, "packed 16-row tiles are for FP8 and MXFP4 weights");
     if (c->weight_layout == MOE_WLAYOUT_TILED16 && c->mfma_min_tokens != 0 && c->mfma_min_tokens != 1)
         FAIL(err, MOE_ERR_UNSUPPORTED, "packed 16-row tiles need MFMA tiles for every expert (mfma_min_tokens 0 or 1)");
     if (c->wfmt == MOE_WFMT_NVFP4_E2M1_B16 && c->act_dtype != MOE_DTYPE_BF16)
@@ -210,8 +208,6 @@ moe_status moe_decode_pack_weights(const moe_decode_config *cfg, void *stream, c
     g_init_err[0] = 0;
     moe_status s = check_config(cfg, g_init_err);
     if (s != MOE_OK) return s;
-    if (cfg->wfmt == MOE_WFMT_NVFP4_E2M1_B16)
-        FAIL(g_init_err, MOE_ERR_UNSUPPORTED, "packed 16-row tiles are for FP8 and MXFP4 weights");
     if (n_experts < 1 || n_experts > cfg->n_experts)
         FAIL(g_init_err, MOE_ERR_INVALID, "n_experts=%d outside 1..%d", n_experts, cfg->n_experts);
     if (!src || !dst) FAIL(g_init_err, MOE_ERR_INVALID, "src or dst is NULL");

@@ -852,12 +852,15 @@ hipError_t w2_launch(const Layer &L, const uint8_t *ew, const uint8_t *es, int T
 
 // Row-major expert weights -> packed 16-row tiles (the layout above), one thread per
 // 16-byte piece of the destination.  Per expert: the [2I][K = H] gate/up rows, then
-// the [H][K = I] down rows; FP8 one byte per input, E2M1 half a byte.
+// the [H][K = I] down rows; FP8 one byte per input, E2M1 half a byte.  fmt 0 FP8
+// (128-input blocks), 1 MXFP4 (128-input blocks), 2 NVFP4 (256-input blocks of the
+// bf16 kernels: lane l's bytes [32g, 32g+16) at 16l, [32g+16, 32g+32) at 1024 + 16l).
 __global__ void pack_kernel(const uint8_t *__restrict__ src, uint8_t *__restrict__ dst, int64_t n_pieces, int H,
-                            int I, int fp4, int64_t expert_bytes)
+                            int I, int fmt, int64_t expert_bytes)
 {
-    const int blk = fp4 ? 1024 : 2048;          // bytes of a (16-row tile, K block) piece
-    const int kbb = fp4 ? 64 : 128;             // bytes of a row per K block
+    const bool fp4 = fmt != 0;
+    const int blk = fmt == 1 ? 1024 : 2048;     // bytes of a (16-row tile, K block) piece
+    const int kbb = fmt == 1 ? 64 : 128;        // bytes of a row per K block
     const int64_t w13 = (int64_t)2 * I * H / (fp4 ? 2 : 1);  // gate/up bytes of an expert
     for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n_pieces; p += (int64_t)gridDim.x * blockDim.x) {
         const int64_t off = p * 16;                     // destination byte
@@ -868,9 +871,10 @@ __global__ void pack_kernel(const uint8_t *__restrict__ src, uint8_t *__restrict
         const int64_t tile = mo / (16 * rowb), to = mo % (16 * rowb);
         const int64_t kb = to / blk;
         const int q = (int)(to % blk) / 16;             // piece within the block
-        const int half = fp4 ? 0 : q / 64, l = q % 64;  // FP8: second 1 KB holds K + 64
+        const int half = fmt == 1 ? 0 : q / 64, l = q % 64;  // 2 KB pieces: two halves of 1 KB
         const int r = l & 15, g = l >> 4;
-        const int64_t so = e * expert_bytes + (down ? w13 : 0) + (tile * 16 + r) * rowb + kb * kbb + 16 * g + 64 * half;
+        const int lb = fmt == 2 ? 32 * g + 16 * half : 16 * g + 64 * half;  // byte within the row's block
+        const int64_t so = e * expert_bytes + (down ? w13 : 0) + (tile * 16 + r) * rowb + kb * kbb + lb;
         *reinterpret_cast<uint4 *>(dst + off) = *reinterpret_cast<const uint4 *>(src + so);
     }
 }
@@ -904,7 +908,7 @@ hipError_t launch_pack_weights(const Layer &L, const void *src, void *dst, int n
     const int64_t pieces = (int64_t)n_experts * (int64_t)L.expert_w_bytes / 16;
     const int64_t blocks = (pieces + 255) / 256;
     pack_kernel<<<(unsigned)(blocks < 16384 ? blocks : 16384), 256, 0, st>>>(
-        (const uint8_t *)src, (uint8_t *)dst, pieces, L.H, L.I, L.wfmt == 1, (int64_t)L.expert_w_bytes);
+        (const uint8_t *)src, (uint8_t *)dst, pieces, L.H, L.I, L.wfmt, (int64_t)L.expert_w_bytes);
     return hipGetLastError();
 }
 

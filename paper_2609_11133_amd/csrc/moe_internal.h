@@ -83,7 +83,7 @@ struct Layer {
                     // 2 NVFP4 (E4M3 per 16 + fp32 per matrix)
     int act_bf16;   // activations bf16 (1) or fp32 (0)
     int router_bf16;
-    int wlayout;    // expert weights: 0 row-major, 1 packed 16-row tiles (FP8, MXFP4)
+    int wlayout;    // expert weights: 0 row-major, 1 packed 16-row tiles
     size_t expert_w_bytes;  // per expert
     size_t expert_s_bytes;  // per expert
 };

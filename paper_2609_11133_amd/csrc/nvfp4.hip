@@ -18,6 +18,12 @@
 // the inputs [64g + 8q, 64g + 8q + 8), so a lane's 32 contiguous weight bytes (inputs
 // [64g, 64g+64)) feed all eight and one 32-bit load brings their four block scales.
 //
+// Weights are row-major or packed in 16-row tiles (PK): each 256-input block of a tile
+// is one contiguous 2 KB piece, lane l's weight bytes [32g, 32g+16) of row l%16 at 16l and
+// [32g+16, 32g+32) at 1024 + 16l, read with non-temporal buffer loads off the tile (a
+// wave-uniform resource), so each load instruction of a wave reads 1 KB of contiguous
+// bytes.  The E4M3 scales stay row-major.
+//
 // Work items follow the FP8 staged kernels (mfma.hip): one workgroup of W waves per
 // (chunk of <= 32 tokens of one expert, rows), one 16-row weight tile per wave through
 // a four-deep register ring, the chunk's activations staged once per workgroup in LDS
@@ -38,6 +44,7 @@ typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
 
 constexpr uint32_t kOutOfRange = 0x80000000u;
 constexpr int kRawBufferWord3 = 0x00020000;  // untyped 32-bit data format, no swizzle
+constexpr int kNonTemporal = 2;              // cache policy of a non-temporal buffer load
 
 constexpr int kBlk = 256;                 // inputs per K block
 constexpr int kSegBlk = 2;                // K blocks per staged segment
@@ -127,7 +134,8 @@ __device__ inline void dequant(const u32x4v &w, float s0, float s1, bf16x8 (&a)[
 // `srow`) over KB 256-input blocks against NT staged token tiles.  All W waves of the
 // workgroup call it together; it synchronises them once per staged segment.  On
 // return every wave has passed a barrier after its last read of either buffer.
-template <int NT, int W>
+//   arow  row-major: this lane's weight row; packed: the wave's 16-row tile
+template <int NT, int W, bool PK>
 __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__ arow,
                                    const uint8_t *__restrict__ srow, int KB, __amdgpu_buffer_rsrc_t rs,
                                    Stager<NT, W> &st, Seg (&seg)[2], int lane)
@@ -136,10 +144,22 @@ __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__
     const int nseg = (KB + kSegBlk - 1) / kSegBlk;
     u32x4v A[4][2];
     uint32_t S[4];
+    __amdgpu_buffer_rsrc_t tr;
+    if constexpr (PK) {
+        const uint64_t a = (uint64_t)arow;
+        const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+        const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+        tr = __builtin_amdgcn_make_buffer_rsrc((void *)(((uint64_t)hi << 32) | lo), (short)0, -1, kRawBufferWord3);
+    }
     auto loadA = [&](int slot, int kb) {
-        const uint8_t *p = arow + (size_t)kb * (kBlk / 2) + 32 * g;
-        A[slot][0] = *reinterpret_cast<const u32x4v *>(p);
-        A[slot][1] = *reinterpret_cast<const u32x4v *>(p + 16);
+        if constexpr (PK) {
+            A[slot][0] = __builtin_amdgcn_raw_buffer_load_b128(tr, 16u * lane, kb * 2048, kNonTemporal);
+            A[slot][1] = __builtin_amdgcn_raw_buffer_load_b128(tr, 16u * lane + 1024u, kb * 2048, kNonTemporal);
+        } else {
+            const uint8_t *p = arow + (size_t)kb * (kBlk / 2) + 32 * g;
+            A[slot][0] = *reinterpret_cast<const u32x4v *>(p);
+            A[slot][1] = *reinterpret_cast<const u32x4v *>(p + 16);
+        }
         S[slot] = *reinterpret_cast<const uint32_t *>(srow + (size_t)kb * (kBlk / 16) + 4 * g);
     };
     // Each half block's activation fragments are read from LDS before its weights are
@@ -214,7 +234,7 @@ __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__
 // gate waves through LDS (seg[1], free once stream_tile returns; the next item first
 // writes it after its first barrier), and the gate waves form h = silu(g) * u, round
 // it to bf16 and store it.
-template <int NT, int W>
+template <int NT, int W, bool PK>
 __device__ inline void w13_item(const uint8_t *__restrict__ we, const uint8_t *__restrict__ se, int H, int I, int i0,
                                 int slot0, int mc, const int32_t *__restrict__ tok_of, __amdgpu_buffer_rsrc_t xr,
                                 __bf16 *__restrict__ hb, Seg (&seg)[2], int wave, int lane, int tid)
@@ -223,12 +243,12 @@ __device__ inline void w13_item(const uint8_t *__restrict__ we, const uint8_t *_
     const int r = lane & 15, g = lane >> 4;
     const bool up = wave >= HW;
     const int rr = i0 + 16 * (wave % HW) + r;  // this lane's intermediate row
-    const uint8_t *arow = we + (size_t)((up ? I : 0) + rr) * (H / 2);
+    const uint8_t *arow = we + (size_t)((up ? I : 0) + rr - (PK ? r : 0)) * (H / 2);
     const uint8_t *srow = se + 16 + (size_t)((up ? I : 0) + rr) * (H / 16);
     Stager<NT, W> st;
     st.init(tok_of, slot0, mc, H, tid);
     f32x4 acc[NT];
-    stream_tile<NT, W>(acc, arow, srow, H / kBlk, xr, st, seg, lane);
+    stream_tile<NT, W, PK>(acc, arow, srow, H / kBlk, xr, st, seg, lane);
     f32x4 *red = reinterpret_cast<f32x4 *>(&seg[1].row[0][0]);
     static_assert(sizeof(f32x4) * (W / 2) * 2 * 64 <= sizeof(Seg), "reduction buffer");
     if (up) {
@@ -257,7 +277,7 @@ __device__ inline void w13_item(const uint8_t *__restrict__ we, const uint8_t *_
     }
 }
 
-template <int W>
+template <int W, bool PK>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) void w13_nvfp4_kernel(const uint8_t *__restrict__ ew,
                                                            const uint8_t *__restrict__ es,
                                                            const int32_t *__restrict__ meta,
@@ -279,26 +299,26 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
         const uint8_t *we = ew + (size_t)rec.x * ewb;
         const uint8_t *se = es + (size_t)rec.x * esb;
         if (rec.z > 16)
-            w13_item<2, W>(we, se, H, I, i0, rec.y, rec.z, tok_of, xr, hb, seg, wave, lane, tid);
+            w13_item<2, W, PK>(we, se, H, I, i0, rec.y, rec.z, tok_of, xr, hb, seg, wave, lane, tid);
         else
-            w13_item<1, W>(we, se, H, I, i0, rec.y, rec.z, tok_of, xr, hb, seg, wave, lane, tid);
+            w13_item<1, W, PK>(we, se, H, I, i0, rec.y, rec.z, tok_of, xr, hb, seg, wave, lane, tid);
     }
 }
 
 // down: item = (chunk, rows [n0, n0 + 16W)); wave w streams rows n0 + 16w.
-template <int NT, int W>
+template <int NT, int W, bool PK>
 __device__ inline void w2_item(const uint8_t *__restrict__ we, const uint8_t *__restrict__ se, int H, int I, int n0,
                                int slot0, int mc, __amdgpu_buffer_rsrc_t hr, float *__restrict__ obuf, Seg (&seg)[2],
                                int wave, int lane, int tid)
 {
     const int r = lane & 15, g = lane >> 4;
     const int row0 = n0 + 16 * wave;
-    const uint8_t *arow = we + (size_t)I * H + (size_t)(row0 + r) * (I / 2);
+    const uint8_t *arow = we + (size_t)I * H + (size_t)(row0 + (PK ? 0 : r)) * (I / 2);
     const uint8_t *srow = se + 16 + (size_t)2 * I * (H / 16) + (size_t)(row0 + r) * (I / 16);
     Stager<NT, W> st;
     st.init(nullptr, slot0, mc, I, tid);
     f32x4 acc[NT];
-    stream_tile<NT, W>(acc, arow, srow, I / kBlk, hr, st, seg, lane);
+    stream_tile<NT, W, PK>(acc, arow, srow, I / kBlk, hr, st, seg, lane);
     const float td = reinterpret_cast<const float *>(se)[2];
 #pragma unroll
     for (int j = 0; j < NT; ++j)
@@ -306,7 +326,7 @@ __device__ inline void w2_item(const uint8_t *__restrict__ we, const uint8_t *__
             *reinterpret_cast<f32x4 *>(obuf + ((size_t)slot0 + 16 * j + r) * H + row0 + 4 * g) = td * acc[j];
 }
 
-template <int W>
+template <int W, bool PK>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) void w2_nvfp4_kernel(const uint8_t *__restrict__ ew,
                                                           const uint8_t *__restrict__ es,
                                                           const int32_t *__restrict__ meta,
@@ -327,9 +347,9 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
         const uint8_t *we = ew + (size_t)rec.x * ewb;
         const uint8_t *se = es + (size_t)rec.x * esb;
         if (rec.z > 16)
-            w2_item<2, W>(we, se, H, I, n0, rec.y, rec.z, hr, obuf, seg, wave, lane, tid);
+            w2_item<2, W, PK>(we, se, H, I, n0, rec.y, rec.z, hr, obuf, seg, wave, lane, tid);
         else
-            w2_item<1, W>(we, se, H, I, n0, rec.y, rec.z, hr, obuf, seg, wave, lane, tid);
+            w2_item<1, W, PK>(we, se, H, I, n0, rec.y, rec.z, hr, obuf, seg, wave, lane, tid);
     }
 }
 
@@ -351,9 +371,14 @@ hipError_t launch_w13_nvfp4(const Layer &L, const void *expert_w, const void *sc
                             const int32_t *meta, const int32_t *tok_of, const Workspace &ws, hipStream_t st)
 {
     dim3 grid(nvfp4_grid(L, T, k, L.I / (8 * kWaves))), block(64 * kWaves);
-    w13_nvfp4_kernel<kWaves><<<grid, block, 0, st>>>((const uint8_t *)expert_w, (const uint8_t *)scales, meta, tok_of,
-                                                     (const __bf16 *)x, (__bf16 *)ws.hb, T, L.H, L.I, L.E,
-                                                     L.expert_w_bytes, L.expert_s_bytes);
+    if (L.wlayout)
+        w13_nvfp4_kernel<kWaves, true><<<grid, block, 0, st>>>(
+            (const uint8_t *)expert_w, (const uint8_t *)scales, meta, tok_of, (const __bf16 *)x, (__bf16 *)ws.hb, T,
+            L.H, L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
+    else
+        w13_nvfp4_kernel<kWaves, false><<<grid, block, 0, st>>>(
+            (const uint8_t *)expert_w, (const uint8_t *)scales, meta, tok_of, (const __bf16 *)x, (__bf16 *)ws.hb, T,
+            L.H, L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
     return hipGetLastError();
 }
 
@@ -361,9 +386,14 @@ hipError_t launch_w2_nvfp4(const Layer &L, const void *expert_w, const void *sca
                            const int32_t *meta, const Workspace &ws, hipStream_t st)
 {
     dim3 grid(nvfp4_grid(L, T, k, L.H / (16 * kWaves))), block(64 * kWaves);
-    w2_nvfp4_kernel<kWaves><<<grid, block, 0, st>>>((const uint8_t *)expert_w, (const uint8_t *)scales, meta,
-                                                    (const __bf16 *)ws.hb, ws.o, T * k, L.H, L.I, L.E,
-                                                    L.expert_w_bytes, L.expert_s_bytes);
+    if (L.wlayout)
+        w2_nvfp4_kernel<kWaves, true><<<grid, block, 0, st>>>((const uint8_t *)expert_w, (const uint8_t *)scales,
+                                                              meta, (const __bf16 *)ws.hb, ws.o, T * k, L.H, L.I, L.E,
+                                                              L.expert_w_bytes, L.expert_s_bytes);
+    else
+        w2_nvfp4_kernel<kWaves, false><<<grid, block, 0, st>>>((const uint8_t *)expert_w, (const uint8_t *)scales,
+                                                               meta, (const __bf16 *)ws.hb, ws.o, T * k, L.H, L.I,
+                                                               L.E, L.expert_w_bytes, L.expert_s_bytes);
     return hipGetLastError();
 }
 

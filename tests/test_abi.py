@@ -289,7 +289,6 @@ def test_struct_sizes_match_header(B):
     "kw,code",
     [
         (dict(weight_layout=2), -1),
-        (dict(weight_layout=1, wfmt=2), -2),  # NVFP4 weights stay row-major
         (dict(weight_layout=1, mfma_min_tokens=-1), -2),  # the GEMV path reads row-major weights
         (dict(weight_layout=1, mfma_min_tokens=4), -2),
     ],
@@ -303,7 +302,7 @@ def test_weight_layout_checks(B, kw, code):
 
 
 def test_weight_layout_accepted(B):
-    for wfmt in (0, 1):
+    for wfmt in (0, 1, 2):
         for mm in (0, 1):
             assert B.moe_decode_workspace_bytes(cfg(B, weight_layout=1, wfmt=wfmt, mfma_min_tokens=mm)) > 0
 
@@ -316,7 +315,6 @@ def test_weight_layout_accepted(B):
         (dict(src=0), "NULL"),
         (dict(dst=8), "aligned"),
         (dict(dst=256 + 1024), "overlap"),
-        (dict(wfmt=2), "FP8 and MXFP4"),
     ],
 )
 def test_pack_validates_before_launch(B, change, needle):

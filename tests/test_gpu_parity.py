@@ -356,22 +356,24 @@ def pack_reference(expert_w, cfg):
     """Packed 16-row tiles from row-major expert weights (uint8 [E][bytes]), written
     from the layout's definition: per matrix [rows][K] and per (16-row tile, 128-input
     K block), lane l's operand bytes of row l%16 in lane order."""
-    fp4 = cfg.wfmt == "mxfp4"
-    H, I = cfg.hidden, cfg.inter
-    ew = expert_w.reshape(cfg.n_experts, -1)
+    fp4 = cfg.wfmt != "fp8"
+    H, I, E = cfg.hidden, cfg.inter, cfg.n_experts
+    ew = expert_w.reshape(E, -1)
     out = np.empty_like(ew)
     for rows, K, off in ((2 * I, H, 0), (H, I, 2 * I * H // (2 if fp4 else 1))):
         rowb = K // 2 if fp4 else K
-        m = ew[:, off: off + rows * rowb].reshape(cfg.n_experts, rows // 16, 16, K // 128, 64 if fp4 else 128)
-        if fp4:  # [E][tile][r][kb][g*16+i] -> [E][tile][kb][g][r][i]
-            v = m.reshape(cfg.n_experts, rows // 16, 16, K // 128, 4, 16).transpose(0, 1, 3, 4, 2, 5)
+        m = ew[:, off: off + rows * rowb]
+        if cfg.wfmt == "mxfp4":  # [E][tile][r][kb][g*16+i] -> [E][tile][kb][g][r][i]
+            v = m.reshape(E, rows // 16, 16, K // 128, 4, 16).transpose(0, 1, 3, 4, 2, 5)
+        elif cfg.wfmt == "nvfp4":  # 256-input blocks: [E][tile][r][kb][g*32+half*16+i] -> [..][kb][half][g][r][i]
+            v = m.reshape(E, rows // 16, 16, K // 256, 4, 2, 16).transpose(0, 1, 3, 5, 4, 2, 6)
         else:  # [E][tile][r][kb][half*64+g*16+i] -> [E][tile][kb][half][g][r][i]
-            v = m.reshape(cfg.n_experts, rows // 16, 16, K // 128, 2, 4, 16).transpose(0, 1, 3, 4, 5, 2, 6)
-        out[:, off: off + rows * rowb] = v.reshape(cfg.n_experts, -1)
+            v = m.reshape(E, rows // 16, 16, K // 128, 2, 4, 16).transpose(0, 1, 3, 4, 5, 2, 6)
+        out[:, off: off + rows * rowb] = v.reshape(E, -1)
     return out.reshape(expert_w.shape)
 
 
-@pytest.mark.parametrize("cfg", [SMALL_FP8, SMALL_MX], ids=["fp8", "mxfp4"])
+@pytest.mark.parametrize("cfg", [SMALL_FP8, SMALL_MX, SMALL_NV], ids=["fp8", "mxfp4", "nvfp4"])
 def test_pack_matches_layout_definition(dev, cfg):
     from paper_2609_11133_amd import binding as B
 
@@ -394,6 +396,8 @@ PACKED_CFGS = [
     LayerConfig("pk-mx", 512, 16, 4, 512, "bf16", "bf16", "mxfp4", "zipf:1.1", []),
     LayerConfig("pk-mx-768", 768, 16, 4, 768, "bf16", "bf16", "mxfp4", None, []),
     LayerConfig("pk-f32-mx", 256, 8, 2, 256, "f32", "f32", "mxfp4", None, []),
+    LayerConfig("pk-nv", 512, 16, 4, 256, "bf16", "bf16", "nvfp4", "normal:0.5", []),
+    LayerConfig("pk-nv-odd", 1280, 16, 4, 768, "bf16", "bf16", "nvfp4", "zipf:1.1", []),
 ]
 
 
@@ -415,6 +419,12 @@ def test_full_235b_packed(dev, full_235b, T):
 def test_full_480b_packed(dev, full_480b):
     run = Run(C.QWEN3_480B, full_480b, dev, max_tokens=128, weight_layout=1)
     _full(run, C.QWEN3_480B, 128, batch=5)
+
+
+@pytest.mark.parametrize("T", [1, 64])
+def test_full_235b_nvfp4_packed(dev, full_235b_nv, T):
+    run = Run(C.QWEN3_235B_NVFP4, full_235b_nv, dev, max_tokens=64, weight_layout=1)
+    _full(run, C.QWEN3_235B_NVFP4, T, batch=T)
 
 
 def test_full_mxfp4_zipf_packed(dev):
