@@ -328,11 +328,16 @@ def main():
     ew0, sc0 = W.to_device(hl.expert_w, dev), W.to_device(hl.scales, dev)
     layout = 0 if args.layout == "row-major" else 1
     bcfg = W.binding_config(cfg, Tmax, args.mstar, args.screen_min_tokens, layout)
-    if layout:  # weights converted once, as at load time
+    if layout:  # weights (and NVFP4 scales) converted once, as at load time
         packed = torch.empty_like(ew0)
-        B.moe_decode_pack_weights(bcfg, torch.cuda.current_stream(dev).cuda_stream, ew0, packed, cfg.n_experts)
+        nv = cfg.wfmt == "nvfp4"
+        psc = torch.empty_like(sc0) if nv else None
+        B.moe_decode_pack_weights(bcfg, torch.cuda.current_stream(dev).cuda_stream, ew0, packed, cfg.n_experts,
+                                  sc0 if nv else None, psc)
         torch.cuda.synchronize(dev)
         ew0 = packed
+        if nv:
+            sc0 = psc
     ews = [ew0] + [ew0.clone() for _ in range(copies - 1)]
     scs = [sc0] + [sc0.clone() for _ in range(copies - 1)]
     setup_s = time.time() - t0

@@ -93,9 +93,13 @@ typedef enum {
                                   1024 + 16 l, g = l/16, l < 64; MXFP4: 1 KB, K [32g, 32g+32)
                                   of row l%16 at 16 l; NVFP4: 256-input blocks of 2 KB,
                                   row l%16's bytes [32g, 32g+16) at 16 l and [32g+16,
-                                  32g+32) at 1024 + 16 l).  Written by
+                                  32g+32) at 1024 + 16 l, and the E4M3 scales packed
+                                  the same way: per tile and 256-input block one 256-byte
+                                  piece, scales [4g, 4g+4) of row l%16 at 4 l; the 16
+                                  bytes of matrix scales stay first).  FP8 and MXFP4
+                                  scales are unchanged.  Written by
                                   moe_decode_pack_weights.  Needs MFMA tiles for every
-                                  expert (mfma_min_tokens 0 or 1); scales are unchanged. */
+                                  expert (mfma_min_tokens 0 or 1). */
 } moe_wlayout;
 
 typedef struct moe_decode_config {
@@ -164,15 +168,17 @@ moe_status moe_decode_forward(moe_decode_t h, void *stream, const void *x, int32
                               const float *router_bias, const void *expert_w, const void *scales, int32_t topk,
                               void *y, int32_t *topk_ids, float *topk_weights);
 
-/* Enqueue on `stream` the conversion of n_experts consecutive experts' weights from
- * the row-major layout (src) to packed 16-row tiles (dst), for a handle whose
- * configuration has weight_layout = MOE_WLAYOUT_TILED16 (the other fields as for that
- * handle; weight_layout itself is not read).  src and dst are device buffers of
- * n_experts * moe_decode_expert_weight_bytes(cfg) bytes, 16-byte aligned, owned by the
- * caller, not overlapping.  Scales need no conversion.  Errors
- * as for moe_decode_init (message in moe_decode_last_error(NULL)). */
+/* Enqueue on `stream` the conversion of n_experts consecutive experts' weights (and,
+ * for NVFP4, their scales) from the row-major layout (src) to packed 16-row tiles (dst),
+ * for a handle whose configuration has weight_layout = MOE_WLAYOUT_TILED16 (the other
+ * fields as for that handle; weight_layout itself is not read).  src and dst are device
+ * buffers of n_experts * moe_decode_expert_weight_bytes(cfg) bytes, 16-byte aligned;
+ * src_scales and dst_scales of n_experts * moe_decode_expert_scale_bytes(cfg) bytes,
+ * 4-byte aligned, for NVFP4 weights, NULL for FP8 and MXFP4 ones (their scales keep their
+ * layout).  All owned by the caller; a source and its destination must not overlap.
+ * Errors as for moe_decode_init (message in moe_decode_last_error(NULL)). */
 moe_status moe_decode_pack_weights(const moe_decode_config *cfg, void *stream, const void *src, void *dst,
-                                   int32_t n_experts);
+                                   const void *src_scales, void *dst_scales, int32_t n_experts);
 
 /* Steps 1-2 only (router logits and top-k softmax).  `logits` [T][E] fp32 receives
  * the canonical logits if not NULL; topk_ids / topk_weights as in forward. */

@@ -97,7 +97,7 @@ def lib():
         L.moe_decode_forward.restype = ctypes.c_int
         L.moe_decode_forward.argtypes = [P, P, P, I32, P, P, P, P, I32, P, P, P]
         L.moe_decode_pack_weights.restype = ctypes.c_int
-        L.moe_decode_pack_weights.argtypes = [cfgp, P, P, P, I32]
+        L.moe_decode_pack_weights.argtypes = [cfgp, P, P, P, P, P, I32]
         L.moe_decode_route.restype = ctypes.c_int
         L.moe_decode_route.argtypes = [P, P, P, I32, P, P, I32, P, P, P]
         L.moe_decode_get_stats.restype = ctypes.c_int
@@ -175,9 +175,12 @@ def moe_decode_forward(h, stream, x, n_tokens, router_w, router_bias, expert_w, 
                                     _addr(topk_weights)), h)
 
 
-def moe_decode_pack_weights(cfg: moe_decode_config, stream, src, dst, n_experts: int):
-    """Enqueue the row-major -> packed 16-row tile conversion of n_experts experts."""
-    _check(lib().moe_decode_pack_weights(ctypes.byref(cfg), stream, _addr(src), _addr(dst), n_experts))
+def moe_decode_pack_weights(cfg: moe_decode_config, stream, src, dst, n_experts: int, src_scales=None,
+                            dst_scales=None):
+    """Enqueue the row-major -> packed 16-row tile conversion of n_experts experts
+    (scales too for NVFP4 weights)."""
+    _check(lib().moe_decode_pack_weights(ctypes.byref(cfg), stream, _addr(src), _addr(dst), _addr(src_scales),
+                                         _addr(dst_scales), n_experts))
 
 
 def moe_decode_route(h, stream, x, n_tokens, router_w, router_bias, topk, logits=None, topk_ids=None,

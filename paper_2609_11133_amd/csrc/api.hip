@@ -36,6 +36,8 @@ size_t carve_workspace(int H, int E, int I, int kmax, int Tmax, int wfmt, void *
     w.sync = (int32_t *)take(sizeof(int32_t) * ((size_t)Tmax + 2) * kCounterStride);
     if (wfmt == MOE_WFMT_NVFP4_E2M1_B16) {
         w.hb = (__bf16 *)take(2 * P * I);
+        w.x16 = (_Float16 *)take((size_t)2 * Tmax * H);
+        w.xk = (int32_t *)take(sizeof(int32_t) * (size_t)Tmax);
     } else {
         w.xs_hi = (uint8_t *)take((size_t)Tmax * H);
         w.xs_lo = (uint8_t *)take((size_t)Tmax * H);
@@ -202,8 +204,14 @@ moe_status moe_decode_init(const moe_decode_config *cfg, void *workspace, size_t
     return MOE_OK;
 }
 
+static bool overlap(const void *p, const void *q, size_t bytes)
+{
+    const uintptr_t a = (uintptr_t)p, b = (uintptr_t)q;
+    return a < b + bytes && b < a + bytes;
+}
+
 moe_status moe_decode_pack_weights(const moe_decode_config *cfg, void *stream, const void *src, void *dst,
-                                   int32_t n_experts)
+                                   const void *src_scales, void *dst_scales, int32_t n_experts)
 {
     g_init_err[0] = 0;
     moe_status s = check_config(cfg, g_init_err);
@@ -213,16 +221,28 @@ moe_status moe_decode_pack_weights(const moe_decode_config *cfg, void *stream, c
     if (!src || !dst) FAIL(g_init_err, MOE_ERR_INVALID, "src or dst is NULL");
     if ((uintptr_t)src % 16 || (uintptr_t)dst % 16) FAIL(g_init_err, MOE_ERR_INVALID, "src and dst must be 16-byte aligned");
     const size_t bytes = (size_t)n_experts * moe_decode_expert_weight_bytes(cfg);
-    const uintptr_t a = (uintptr_t)src, b = (uintptr_t)dst;
-    if (a < b + bytes && b < a + bytes) FAIL(g_init_err, MOE_ERR_INVALID, "src and dst overlap");
+    if (overlap(src, dst, bytes)) FAIL(g_init_err, MOE_ERR_INVALID, "src and dst overlap");
+    const bool nv = cfg->wfmt == MOE_WFMT_NVFP4_E2M1_B16;
+    if (nv) {
+        if (!src_scales || !dst_scales) FAIL(g_init_err, MOE_ERR_INVALID, "NVFP4 scales need src_scales and dst_scales");
+        if ((uintptr_t)src_scales % 4 || (uintptr_t)dst_scales % 4)
+            FAIL(g_init_err, MOE_ERR_INVALID, "src_scales and dst_scales must be 4-byte aligned");
+        if (overlap(src_scales, dst_scales, (size_t)n_experts * moe_decode_expert_scale_bytes(cfg)))
+            FAIL(g_init_err, MOE_ERR_INVALID, "src_scales and dst_scales overlap");
+    } else if (src_scales || dst_scales) {
+        FAIL(g_init_err, MOE_ERR_INVALID, "FP8 and MXFP4 scales keep their layout: pass NULL scale pointers");
+    }
     Layer L = {};
     L.H = cfg->hidden;
     L.E = cfg->n_experts;
     L.I = cfg->inter;
     L.wfmt = cfg->wfmt;
     L.expert_w_bytes = moe_decode_expert_weight_bytes(cfg);
+    L.expert_s_bytes = moe_decode_expert_scale_bytes(cfg);
     if (launch_pack_weights(L, src, dst, n_experts, (hipStream_t)stream) != hipSuccess)
         FAIL(g_init_err, MOE_ERR_HIP, "pack kernel launch failed");
+    if (nv && launch_pack_scales(L, src_scales, dst_scales, n_experts, (hipStream_t)stream) != hipSuccess)
+        FAIL(g_init_err, MOE_ERR_HIP, "scale pack kernel launch failed");
     return MOE_OK;
 }
 
@@ -300,7 +320,9 @@ static RouteParams route_params(moe_decode_t h, const void *x, int T, int k, con
     P.cnt_tok = w.sync;
     P.cnt_all = w.sync + (size_t)h->cfg.max_tokens * kCounterStride;
     P.fb_acc = w.sync + ((size_t)h->cfg.max_tokens + 1) * kCounterStride;
-    P.xs_hi = split ? w.xs_hi : nullptr;
+    P.xs_hi = split && w.xs_hi ? w.xs_hi : nullptr;
+    P.x16 = split && w.x16 ? w.x16 : nullptr;
+    P.xk = w.xk;
     P.xs_lo = w.xs_lo;
     P.xe_hi = w.xe_hi;
     P.xe_lo = w.xe_lo;
@@ -356,14 +378,14 @@ moe_status moe_decode_forward(moe_decode_t h, void *stream, const void *x, int32
     const bool gemv = h->mstar != 1;
     CHECK(ensure_synced(h, st));
     if (prof) prof_mark(h, 0, st);
-    // NVFP4 MFMA kernels read x as it is; FP8 and MXFP4 ones read its 2-term FP8 split,
-    // which the routing kernel writes.
+    // The MFMA kernels read x as the routing kernel rewrites it: FP8 and MXFP4 ones its
+    // 2-term FP8 split, NVFP4 ones an f16 copy scaled per token by a power of two.
     const bool nv = L.wfmt == MOE_WFMT_NVFP4_E2M1_B16;
-    const RouteParams P = route_params(h, x, T, k, router_w, router_bias, topk_ids, topk_weights, mfma && !nv, true);
+    const RouteParams P = route_params(h, x, T, k, router_w, router_bias, topk_ids, topk_weights, mfma, true);
     HIPCHECK(h, launch_route(L, P, st));
     if (prof) prof_mark(h, 1, st);
     if (gemv) HIPCHECK(h, launch_w13(L, expert_w, scales, x, T, k, w.meta, w.tok_of, w.h, st));
-    if (mfma && nv) HIPCHECK(h, launch_w13_nvfp4(L, expert_w, scales, x, T, k, w.meta, w.tok_of, w, st));
+    if (mfma && nv) HIPCHECK(h, launch_w13_nvfp4(L, expert_w, scales, T, k, w.meta, w.tok_of, w, st));
     if (mfma && !nv) HIPCHECK(h, launch_w13_mfma(L, expert_w, scales, T, k, w.meta, w.tok_of, w, st));
     if (prof) prof_mark(h, 2, st);
     if (gemv) HIPCHECK(h, launch_w2(L, expert_w, scales, T, k, w.meta, w.h, w.o, st));

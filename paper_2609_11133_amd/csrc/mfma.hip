@@ -881,6 +881,35 @@ __global__ void pack_kernel(const uint8_t *__restrict__ src, uint8_t *__restrict
     }
 }
 
+// NVFP4 E4M3 scales, row-major -> packed 16-row tiles: per matrix [rows][K/16] bytes
+// after each expert's 16 bytes of matrix scales; per (16-row tile, 256-input block) one
+// 256-byte piece, lane l's 4 bytes (scales [4g, 4g+4) of row l%16) at 4l.  One thread
+// per 4-byte word of the destination.
+__global__ void pack_scales_kernel(const uint8_t *__restrict__ src, uint8_t *__restrict__ dst, int64_t n_words, int H,
+                                   int I, int64_t expert_bytes)
+{
+    const int64_t w13 = (int64_t)2 * I * (H / 16);  // gate/up scale bytes of an expert
+    const int64_t body = w13 + (int64_t)H * (I / 16);
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n_words; p += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t off = p * 4;                       // byte within the experts' scale bodies
+        const int64_t e = off / body, eo = off % body;
+        const bool down = eo >= w13;
+        const int64_t mo = down ? eo - w13 : eo;
+        const int64_t rowb = (down ? I : H) / 16;        // scale bytes per row
+        const int64_t tile = mo / (16 * rowb), to = mo % (16 * rowb);
+        const int64_t kb = to / 256;
+        const int l = (int)(to % 256) / 4, r = l & 15, g = l >> 4;
+        const int64_t base = e * expert_bytes + 16 + (down ? w13 : 0);
+        *reinterpret_cast<uint32_t *>(dst + base + mo) =
+            *reinterpret_cast<const uint32_t *>(src + base + (tile * 16 + r) * rowb + kb * 16 + 4 * g);
+    }
+    // the 16 bytes of matrix scales of each expert, unchanged
+    const int64_t n_e = n_words * 4 / body;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n_e * 4; p += (int64_t)gridDim.x * blockDim.x)
+        *reinterpret_cast<uint32_t *>(dst + (p / 4) * expert_bytes + (p % 4) * 4) =
+            *reinterpret_cast<const uint32_t *>(src + (p / 4) * expert_bytes + (p % 4) * 4);
+}
+
 }  // namespace
 
 hipError_t launch_w13_mfma(const Layer &L, const void *expert_w, const void *scales, int T, int k,
@@ -903,6 +932,16 @@ hipError_t launch_w2_mfma(const Layer &L, const void *expert_w, const void *scal
                          : w2_launch<0, false>(L, ew, es, T, k, meta, ws, st);
     return L.wlayout ? w2_launch<1, true>(L, ew, es, T, k, meta, ws, st)
                      : w2_launch<1, false>(L, ew, es, T, k, meta, ws, st);
+}
+
+hipError_t launch_pack_scales(const Layer &L, const void *src, void *dst, int n_experts, hipStream_t st)
+{
+    const int64_t body = (int64_t)2 * L.I * (L.H / 16) + (int64_t)L.H * (L.I / 16);
+    const int64_t words = (int64_t)n_experts * body / 4;
+    const int64_t blocks = (words + 255) / 256;
+    pack_scales_kernel<<<(unsigned)(blocks < 16384 ? blocks : 16384), 256, 0, st>>>(
+        (const uint8_t *)src, (uint8_t *)dst, words, L.H, L.I, (int64_t)L.expert_s_bytes);
+    return hipGetLastError();
 }
 
 hipError_t launch_pack_weights(const Layer &L, const void *src, void *dst, int n_experts, hipStream_t st)

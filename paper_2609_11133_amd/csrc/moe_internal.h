@@ -23,6 +23,8 @@ struct Workspace {
     uint8_t *hs_hi, *hs_lo;  // [Tmax*kmax][I] 2-term FP8 split of h (MFMA path)
     uint8_t *he_hi, *he_lo;  // [Tmax*kmax][I/32]
     __bf16 *hb;              // [Tmax*kmax][I] bf16 SwiGLU activations (NVFP4 MFMA path)
+    _Float16 *x16;           // [Tmax][H] x * 2^-k in f16 (NVFP4 MFMA path)
+    int32_t *xk;             // [Tmax] the power k of each token
     void *part;              // screened routing: [ks_max][Tmax][E] (sum x*w, sum |x*w|) fp64 pairs
     float *xmax, *wmax;      // [ks_max][Tmax], [ks_max][E] slice maxima of |x| and |w|
     int ks_max;              // K slices the screened routing may use (0: path off)
@@ -99,6 +101,8 @@ struct RouteParams {
     int32_t *meta, *slot_of, *tok_of;
     int32_t *cnt_tok, *cnt_all, *fb_acc;
     uint8_t *xs_hi, *xs_lo, *xe_hi, *xe_lo;  // NULL: no activation split
+    _Float16 *x16;                           // NULL: no f16 copy of x (NVFP4 MFMA path)
+    int32_t *xk;
     void *part;                               // screened routing buffers (Workspace)
     float *xmax, *wmax;
     int ks_max, Tmax;
@@ -112,6 +116,7 @@ struct RouteParams {
 hipError_t launch_zero(int32_t *p, int n, hipStream_t st);
 hipError_t launch_route(const Layer &L, const RouteParams &P, hipStream_t st);
 hipError_t launch_pack_weights(const Layer &L, const void *src, void *dst, int n_experts, hipStream_t st);
+hipError_t launch_pack_scales(const Layer &L, const void *src, void *dst, int n_experts, hipStream_t st);
 hipError_t launch_w13(const Layer &L, const void *expert_w, const void *scales, const void *x, int T, int k,
                       const int32_t *meta, const int32_t *tok_of, float *h, hipStream_t st);
 hipError_t launch_w2(const Layer &L, const void *expert_w, const void *scales, int T, int k, const int32_t *meta,
@@ -120,7 +125,7 @@ hipError_t launch_w13_mfma(const Layer &L, const void *expert_w, const void *sca
                            const int32_t *meta, const int32_t *tok_of, const Workspace &ws, hipStream_t st);
 hipError_t launch_w2_mfma(const Layer &L, const void *expert_w, const void *scales, int T, int k,
                           const int32_t *meta, const Workspace &ws, hipStream_t st);
-hipError_t launch_w13_nvfp4(const Layer &L, const void *expert_w, const void *scales, const void *x, int T, int k,
+hipError_t launch_w13_nvfp4(const Layer &L, const void *expert_w, const void *scales, int T, int k,
                             const int32_t *meta, const int32_t *tok_of, const Workspace &ws, hipStream_t st);
 hipError_t launch_w2_nvfp4(const Layer &L, const void *expert_w, const void *scales, int T, int k,
                            const int32_t *meta, const Workspace &ws, hipStream_t st);

@@ -10,6 +10,14 @@
 // itself and, for the down projection, h rounded once to bf16; the 16x16x32 bf16 MFMA
 // accumulates in fp32 and the matrix scales multiply the accumulators.
 //
+// The gate/up projection runs on f16 operands instead, which halves the conversion
+// work that bounds it: an E2M1 pair converts to f16 with the block scale's power of
+// two applied by the conversion, and one packed f16 multiply applies the scale's
+// mantissa 1 + j/8 (every product has at most 5 significant bits and lies in
+// [2^-13, 2688]: exact).  x enters as the routing kernel's f16 copy x * 2^-k (k per
+// token, so that every value at least 2^-10 of the token's maximum converts exactly),
+// and the accumulators are multiplied by 2^k.
+//
 // Operand layout of v_mfma_f32_16x16x32_bf16 (checked on the device): lane l holds
 // row/column l%16 and K [8g, 8g+8) with g = l/16; the result gives lane l rows
 // 4g..4g+3 of column l%16.  The K order inside one instruction is free as long as
@@ -22,7 +30,9 @@
 // is one contiguous 2 KB piece, lane l's weight bytes [32g, 32g+16) of row l%16 at 16l and
 // [32g+16, 32g+32) at 1024 + 16l, read with non-temporal buffer loads off the tile (a
 // wave-uniform resource), so each load instruction of a wave reads 1 KB of contiguous
-// bytes.  The E4M3 scales stay row-major.
+// bytes.  The E4M3 scales are packed the same way: a block's 16 rows x 16 scales are one
+// 256-byte piece, lane l's four (scales [4g, 4g+4) of row l%16) at 4l.  Read row by row,
+// the scales were the packed kernels' bound (16 segments of 16 bytes per load).
 //
 // Work items follow the FP8 staged kernels (mfma.hip): one workgroup of W waves per
 // (chunk of <= 32 tokens of one expert, rows), one 16-row weight tile per wave through
@@ -38,6 +48,8 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
@@ -130,12 +142,46 @@ __device__ inline void dequant(const u32x4v &w, float s0, float s1, bf16x8 (&a)[
     }
 }
 
+// A raw buffer over memory the whole wave addresses from one base (scalar registers).
+__device__ inline __amdgpu_buffer_rsrc_t uniform_rsrc(const void *p)
+{
+    const uint64_t a = (uint64_t)p;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+    return __builtin_amdgcn_make_buffer_rsrc((void *)(((uint64_t)hi << 32) | lo), (short)0, -1, kRawBufferWord3);
+}
+
+// The f16 form of dequant: E2M1 pairs to f16 with the power of two of the scale applied
+// by the conversion, then the scale's mantissa (exact in f16) by one packed multiply.
+__device__ inline void dequant16(const u32x4v &w, float s0, float s1, f16x8 (&a)[4])
+{
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const uint32_t sb = __float_as_uint(q < 2 ? s0 : s1);
+        const float p2 = __uint_as_float(sb & 0xFF800000u);                      // 2^e (0 for a zero scale)
+        const _Float16 mh = (_Float16)__uint_as_float((sb & 0x007FFFFFu) | 0x3F800000u);  // 1 + j/8
+        const f16x2 m2 = {mh, mh};
+        f16x2 v[4];
+        v[0] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w[q], p2, 0) * m2;
+        v[1] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w[q], p2, 1) * m2;
+        v[2] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w[q], p2, 2) * m2;
+        v[3] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w[q], p2, 3) * m2;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            a[q][2 * b] = v[b].x;
+            a[q][2 * b + 1] = v[b].y;
+        }
+    }
+}
+
 // Streams this wave's 16-row weight tile (this lane's row `arow`, its E4M3 scale row
 // `srow`) over KB 256-input blocks against NT staged token tiles.  All W waves of the
 // workgroup call it together; it synchronises them once per staged segment.  On
 // return every wave has passed a barrier after its last read of either buffer.
 //   arow  row-major: this lane's weight row; packed: the wave's 16-row tile
-template <int NT, int W, bool PK>
+//   srow  row-major: this lane's scale row; packed: the tile's scales
+//   F16   f16 operands (the staged activations are f16), else bf16
+template <int NT, int W, bool PK, bool F16>
 __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__ arow,
                                    const uint8_t *__restrict__ srow, int KB, __amdgpu_buffer_rsrc_t rs,
                                    Stager<NT, W> &st, Seg (&seg)[2], int lane)
@@ -144,23 +190,22 @@ __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__
     const int nseg = (KB + kSegBlk - 1) / kSegBlk;
     u32x4v A[4][2];
     uint32_t S[4];
-    __amdgpu_buffer_rsrc_t tr;
+    __amdgpu_buffer_rsrc_t tr, sr;
     if constexpr (PK) {
-        const uint64_t a = (uint64_t)arow;
-        const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
-        const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
-        tr = __builtin_amdgcn_make_buffer_rsrc((void *)(((uint64_t)hi << 32) | lo), (short)0, -1, kRawBufferWord3);
+        tr = uniform_rsrc(arow);
+        sr = uniform_rsrc(srow);
     }
     auto loadA = [&](int slot, int kb) {
         if constexpr (PK) {
             A[slot][0] = __builtin_amdgcn_raw_buffer_load_b128(tr, 16u * lane, kb * 2048, kNonTemporal);
             A[slot][1] = __builtin_amdgcn_raw_buffer_load_b128(tr, 16u * lane + 1024u, kb * 2048, kNonTemporal);
+            S[slot] = __builtin_amdgcn_raw_buffer_load_b32(sr, 4u * lane, kb * 256, 0);
         } else {
             const uint8_t *p = arow + (size_t)kb * (kBlk / 2) + 32 * g;
             A[slot][0] = *reinterpret_cast<const u32x4v *>(p);
             A[slot][1] = *reinterpret_cast<const u32x4v *>(p + 16);
+            S[slot] = *reinterpret_cast<const uint32_t *>(srow + (size_t)kb * (kBlk / 16) + 4 * g);
         }
-        S[slot] = *reinterpret_cast<const uint32_t *>(srow + (size_t)kb * (kBlk / 16) + 4 * g);
     };
     // Each half block's activation fragments are read from LDS before its weights are
     // dequantised, so the LDS latency hides behind that VALU work; instructions q
@@ -171,22 +216,34 @@ __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__
         const f32x2 s23 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(S[slot], 1.0f, true);
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-            bf16x8 b[4][NT];
+            u32x4v b[4][NT];
 #pragma unroll
             for (int q = 0; q < 4; ++q)
 #pragma unroll
                 for (int j = 0; j < NT; ++j) {
                     const int t = 16 * j + r;
-                    b[q][j] = *reinterpret_cast<const bf16x8 *>(&sg.row[t][swz(kk * 32 + 8 * g + 4 * h + q, t) * 16]);
+                    b[q][j] = *reinterpret_cast<const u32x4v *>(&sg.row[t][swz(kk * 32 + 8 * g + 4 * h + q, t) * 16]);
                 }
             __builtin_amdgcn_sched_barrier(0);
-            bf16x8 a[4];
-            dequant(A[slot][h], h ? s23.x : s01.x, h ? s23.y : s01.y, a);
+            if constexpr (F16) {
+                f16x8 a[4];
+                dequant16(A[slot][h], h ? s23.x : s01.x, h ? s23.y : s01.y, a);
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
+                for (int q = 0; q < 4; ++q)
 #pragma unroll
-                for (int j = 0; j < NT; ++j)
-                    acc2[q & 1][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[q], b[q][j], acc2[q & 1][j], 0, 0, 0);
+                    for (int j = 0; j < NT; ++j)
+                        acc2[q & 1][j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[q], __builtin_bit_cast(f16x8, b[q][j]),
+                                                                                acc2[q & 1][j], 0, 0, 0);
+            } else {
+                bf16x8 a[4];
+                dequant(A[slot][h], h ? s23.x : s01.x, h ? s23.y : s01.y, a);
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+#pragma unroll
+                    for (int j = 0; j < NT; ++j)
+                        acc2[q & 1][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[q], __builtin_bit_cast(bf16x8, b[q][j]),
+                                                                                 acc2[q & 1][j], 0, 0, 0);
+            }
         }
     };
 #pragma unroll
@@ -237,18 +294,19 @@ __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__
 template <int NT, int W, bool PK>
 __device__ inline void w13_item(const uint8_t *__restrict__ we, const uint8_t *__restrict__ se, int H, int I, int i0,
                                 int slot0, int mc, const int32_t *__restrict__ tok_of, __amdgpu_buffer_rsrc_t xr,
-                                __bf16 *__restrict__ hb, Seg (&seg)[2], int wave, int lane, int tid)
+                                const int32_t *__restrict__ xk, __bf16 *__restrict__ hb, Seg (&seg)[2], int wave,
+                                int lane, int tid)
 {
     constexpr int HW = W / 2;
     const int r = lane & 15, g = lane >> 4;
     const bool up = wave >= HW;
     const int rr = i0 + 16 * (wave % HW) + r;  // this lane's intermediate row
     const uint8_t *arow = we + (size_t)((up ? I : 0) + rr - (PK ? r : 0)) * (H / 2);
-    const uint8_t *srow = se + 16 + (size_t)((up ? I : 0) + rr) * (H / 16);
+    const uint8_t *srow = se + 16 + (size_t)((up ? I : 0) + rr - (PK ? r : 0)) * (H / 16);
     Stager<NT, W> st;
     st.init(tok_of, slot0, mc, H, tid);
     f32x4 acc[NT];
-    stream_tile<NT, W, PK>(acc, arow, srow, H / kBlk, xr, st, seg, lane);
+    stream_tile<NT, W, PK, true>(acc, arow, srow, H / kBlk, xr, st, seg, lane);
     f32x4 *red = reinterpret_cast<f32x4 *>(&seg[1].row[0][0]);
     static_assert(sizeof(f32x4) * (W / 2) * 2 * 64 <= sizeof(Seg), "reduction buffer");
     if (up) {
@@ -257,9 +315,12 @@ __device__ inline void w13_item(const uint8_t *__restrict__ we, const uint8_t *_
     }
     sync_lds();
     if (!up) {
-        const float tg = reinterpret_cast<const float *>(se)[0], tu = reinterpret_cast<const float *>(se)[1];
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
+            // token column 16j + r: undo its 2^-k (2^k is exact: -112 <= k <= 113)
+            const int kt = 16 * j + r < mc ? xk[tok_of[slot0 + 16 * j + r]] : 0;
+            const float p2k = __uint_as_float((uint32_t)(127 + kt) << 23);
+            const float tg = reinterpret_cast<const float *>(se)[0] * p2k, tu = reinterpret_cast<const float *>(se)[1] * p2k;
             const f32x4 u = red[(wave * 2 + j) * 64 + lane];
             bf16x2 hv[2];
 #pragma unroll
@@ -282,7 +343,8 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
                                                            const uint8_t *__restrict__ es,
                                                            const int32_t *__restrict__ meta,
                                                            const int32_t *__restrict__ tok_of,
-                                                           const __bf16 *__restrict__ x, __bf16 *__restrict__ hb,
+                                                           const _Float16 *__restrict__ x16,
+                                                           const int32_t *__restrict__ xk, __bf16 *__restrict__ hb,
                                                            int T, int H, int I, int E, size_t ewb, size_t esb)
 {
     __shared__ Seg seg[2];
@@ -292,16 +354,16 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
     const int4 *recs = reinterpret_cast<const int4 *>(meta + mi.chunk_rec());
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const __amdgpu_buffer_rsrc_t xr = raw_rsrc(x, (uint32_t)T * (uint32_t)H * 2u);
+    const __amdgpu_buffer_rsrc_t xr = raw_rsrc(x16, (uint32_t)T * (uint32_t)H * 2u);
     for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
         const int4 rec = recs[item / tiles];  // {expert, first slot, tokens, -}
         const int i0 = (item % tiles) * 8 * W;
         const uint8_t *we = ew + (size_t)rec.x * ewb;
         const uint8_t *se = es + (size_t)rec.x * esb;
         if (rec.z > 16)
-            w13_item<2, W, PK>(we, se, H, I, i0, rec.y, rec.z, tok_of, xr, hb, seg, wave, lane, tid);
+            w13_item<2, W, PK>(we, se, H, I, i0, rec.y, rec.z, tok_of, xr, xk, hb, seg, wave, lane, tid);
         else
-            w13_item<1, W, PK>(we, se, H, I, i0, rec.y, rec.z, tok_of, xr, hb, seg, wave, lane, tid);
+            w13_item<1, W, PK>(we, se, H, I, i0, rec.y, rec.z, tok_of, xr, xk, hb, seg, wave, lane, tid);
     }
 }
 
@@ -314,11 +376,11 @@ __device__ inline void w2_item(const uint8_t *__restrict__ we, const uint8_t *__
     const int r = lane & 15, g = lane >> 4;
     const int row0 = n0 + 16 * wave;
     const uint8_t *arow = we + (size_t)I * H + (size_t)(row0 + (PK ? 0 : r)) * (I / 2);
-    const uint8_t *srow = se + 16 + (size_t)2 * I * (H / 16) + (size_t)(row0 + r) * (I / 16);
+    const uint8_t *srow = se + 16 + (size_t)2 * I * (H / 16) + (size_t)(row0 + (PK ? 0 : r)) * (I / 16);
     Stager<NT, W> st;
     st.init(nullptr, slot0, mc, I, tid);
     f32x4 acc[NT];
-    stream_tile<NT, W, PK>(acc, arow, srow, I / kBlk, hr, st, seg, lane);
+    stream_tile<NT, W, PK, false>(acc, arow, srow, I / kBlk, hr, st, seg, lane);
     const float td = reinterpret_cast<const float *>(se)[2];
 #pragma unroll
     for (int j = 0; j < NT; ++j)
@@ -367,17 +429,17 @@ int nvfp4_grid(const Layer &L, int T, int k, int items_per_chunk)
 
 }  // namespace
 
-hipError_t launch_w13_nvfp4(const Layer &L, const void *expert_w, const void *scales, const void *x, int T, int k,
+hipError_t launch_w13_nvfp4(const Layer &L, const void *expert_w, const void *scales, int T, int k,
                             const int32_t *meta, const int32_t *tok_of, const Workspace &ws, hipStream_t st)
 {
     dim3 grid(nvfp4_grid(L, T, k, L.I / (8 * kWaves))), block(64 * kWaves);
     if (L.wlayout)
         w13_nvfp4_kernel<kWaves, true><<<grid, block, 0, st>>>(
-            (const uint8_t *)expert_w, (const uint8_t *)scales, meta, tok_of, (const __bf16 *)x, (__bf16 *)ws.hb, T,
+            (const uint8_t *)expert_w, (const uint8_t *)scales, meta, tok_of, ws.x16, ws.xk, (__bf16 *)ws.hb, T,
             L.H, L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
     else
         w13_nvfp4_kernel<kWaves, false><<<grid, block, 0, st>>>(
-            (const uint8_t *)expert_w, (const uint8_t *)scales, meta, tok_of, (const __bf16 *)x, (__bf16 *)ws.hb, T,
+            (const uint8_t *)expert_w, (const uint8_t *)scales, meta, tok_of, ws.x16, ws.xk, (__bf16 *)ws.hb, T,
             L.H, L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
     return hipGetLastError();
 }

@@ -524,6 +524,8 @@ struct RouteArgs {
     int32_t *cnt_all;  // [1]
     int32_t *fb_acc;   // [1]
     uint8_t *xs_hi, *xs_lo, *xe_hi, *xe_lo;  // activation split (NULL: MFMA path off)
+    _Float16 *x16;                           // f16 copy of x * 2^-k (NULL: none)
+    int32_t *xk;                             // [T] the token's k
     int T, E, H, k, epw, bpt, mstar, do_group, max_chunks;
     int id_cache;  // the grouping keeps the choices in LDS (sized by the launch)
     // screened routing (large T): per K slice ks, partial sums part[ks][t][e] =
@@ -555,6 +557,49 @@ __device__ __attribute__((always_inline)) inline void write_split(const RouteArg
         A.xe_hi[(size_t)t * (H / 32) + g] = (uint8_t)ch;
         A.xe_lo[(size_t)t * (H / 32) + g] = (uint8_t)cl;
     }
+}
+
+// The token's bf16 x as f16 scaled by 2^-k, with k such that max|x| * 2^-k lies in
+// [2^14, 2^15) (k = 0 for a zero row; k >= -112): every value at least 2^-10 of the
+// row's maximum converts exactly.  Called by `nw` waves (wave index w), each of which
+// takes the row maximum on its own (no barrier among them) and converts every nw-th
+// group of eight inputs.
+__device__ inline void bf16x8_f32(const uint16_t *p, float (&v)[8])
+{
+    const uint4 u = *reinterpret_cast<const uint4 *>(p);
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        v[2 * i] = __uint_as_float(w[i] << 16);
+        v[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+}
+
+__device__ __attribute__((always_inline)) inline void write_x16(const RouteArgs &A, const uint16_t *xr, int t, int w,
+                                                                int nw, int lane)
+{
+    const int H = A.H;
+    float m = 0.f;
+    for (int h = lane * 8; h < H; h += 512) {
+        float v[8];
+        bf16x8_f32(xr + h, v);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) m = fmaxf(m, fabsf(v[i]));
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    const int ex = m > 0.f ? (int)((__float_as_uint(m) >> 23) & 0xFF) - 127 : 14;  // floor(log2 m) for normal m
+    const int kk = max(ex - 14, -112);
+    const float sc = __uint_as_float((uint32_t)(127 - kk) << 23);  // 2^-k
+    for (int h = (w * 64 + lane) * 8; h < H; h += nw * 512) {
+        float v[8];
+        bf16x8_f32(xr + h, v);
+        _Float16 q[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) q[i] = (_Float16)(v[i] * sc);
+        *reinterpret_cast<uint4 *>(A.x16 + (size_t)t * H + h) = __builtin_bit_cast(uint4, q);
+    }
+    if (w == 0 && lane == 0) A.xk[t] = kk;
 }
 
 // Last token of a step: group the T*k (token, choice) pairs by expert.  LDS holds one
@@ -705,13 +750,16 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
     if (!s_flag) return;
 
     // 2. last workgroup of token t: top-k softmax in wave 0 while waves 1-3 write the
-    // token's 2-term activation split when the MFMA path is on (groups of 32 inputs)
+    // token's 2-term activation split when the MFMA path is on (groups of 32 inputs), or
+    // its scaled f16 copy for NVFP4 weights
     if (wave == 0) {
         token_topk(A.logits + (size_t)t * E, E, A.k, A.ids + (size_t)t * A.k, A.wts + (size_t)t * A.k,
                    A.ids_user ? A.ids_user + (size_t)t * A.k : nullptr,
                    A.wts_user ? A.wts_user + (size_t)t * A.k : nullptr, lane);
     } else if (A.xs_hi) {
         write_split<XT>(A, xr, t, threadIdx.x - kWave, blockDim.x - kWave);
+    } else if constexpr (sizeof(XT) == 2) {
+        if (A.x16) write_x16(A, xr, t, wave - 1, 3, lane);
     }
     if (threadIdx.x == 0) st_dev(&A.cnt_tok[t * kCounterStride], 0);
     if (!A.do_group) return;
@@ -956,6 +1004,8 @@ __global__ __launch_bounds__(256) void route_cand_kernel(RouteArgs A)
         }
     } else if (A.xs_hi) {
         write_split<uint16_t>(A, xr, t, threadIdx.x - kWave, blockDim.x - kWave);
+    } else if (A.x16) {
+        write_x16(A, xr, t, wave - 1, 3, lane);
     }
     __syncthreads();
 
@@ -1022,6 +1072,8 @@ hipError_t launch_route(const Layer &L, const RouteParams &P, hipStream_t st)
     A.xs_lo = P.xs_lo;
     A.xe_hi = P.xe_hi;
     A.xe_lo = P.xe_lo;
+    A.x16 = P.x16;
+    A.xk = P.xk;
     A.T = P.T;
     A.E = L.E;
     A.H = L.H;

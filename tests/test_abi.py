@@ -315,13 +315,17 @@ def test_weight_layout_accepted(B):
         (dict(src=0), "NULL"),
         (dict(dst=8), "aligned"),
         (dict(dst=256 + 1024), "overlap"),
+        (dict(ssrc=1 << 31), "keep their layout"),  # FP8 scales are not converted
+        (dict(wfmt=2), "need src_scales"),
+        (dict(wfmt=2, ssrc=1 << 31, sdst=(1 << 31) + 2), "4-byte aligned"),
+        (dict(wfmt=2, ssrc=1 << 31, sdst=(1 << 31) + 64), "scales overlap"),
     ],
 )
 def test_pack_validates_before_launch(B, change, needle):
     """Every check of moe_decode_pack_weights fails before a launch (fake pointers)."""
-    args = dict(n_experts=2, src=256, dst=1 << 30, wfmt=0)
+    args = dict(n_experts=2, src=256, dst=1 << 30, wfmt=0, ssrc=None, sdst=None)
     args.update(change)
     c = cfg(B, wfmt=args["wfmt"])
     with pytest.raises(B.MoEDecodeError) as e:
-        B.moe_decode_pack_weights(c, None, args["src"], args["dst"], args["n_experts"])
+        B.moe_decode_pack_weights(c, None, args["src"], args["dst"], args["n_experts"], args["ssrc"], args["sdst"])
     assert needle in str(e.value)

@@ -49,11 +49,16 @@ class Run:
         self.bias = W.to_device(hl.bias, dev)
         self.ew = W.to_device(hl.expert_w, dev)
         self.sc = W.to_device(hl.scales, dev)
-        if weight_layout == 1:  # the library's own conversion of the row-major weights
+        if weight_layout == 1:  # the library's own conversion of the row-major weights (and NVFP4 scales)
             packed = torch.empty_like(self.ew)
-            B.moe_decode_pack_weights(bc, torch.cuda.current_stream(dev).cuda_stream, self.ew, packed, cfg.n_experts)
+            nv = cfg.wfmt == "nvfp4"
+            psc = torch.empty_like(self.sc) if nv else None
+            B.moe_decode_pack_weights(bc, torch.cuda.current_stream(dev).cuda_stream, self.ew, packed, cfg.n_experts,
+                                      self.sc if nv else None, psc)
             torch.cuda.synchronize(dev)
             self.ew = packed
+            if nv:
+                self.sc = psc
 
     def forward(self, x, topk=None):
         k = topk or self.cfg.topk
@@ -373,6 +378,21 @@ def pack_reference(expert_w, cfg):
     return out.reshape(expert_w.shape)
 
 
+def pack_scales_reference(scales, cfg):
+    """Packed NVFP4 E4M3 scales: per expert the 16 bytes of matrix scales, then per
+    matrix [rows][K/16] and per (16-row tile, 256-input block) 256 bytes, lane l's
+    scales [4g, 4g+4) of row l%16 at 4l."""
+    H, I, E = cfg.hidden, cfg.inter, cfg.n_experts
+    sc = scales.reshape(E, -1)
+    out = sc.copy()
+    off = 16
+    for rows, K in ((2 * I, H), (H, I)):
+        m = sc[:, off: off + rows * K // 16].reshape(E, rows // 16, 16, K // 256, 4, 4)
+        out[:, off: off + rows * K // 16] = m.transpose(0, 1, 3, 4, 2, 5).reshape(E, -1)
+        off += rows * K // 16
+    return out.reshape(scales.shape)
+
+
 @pytest.mark.parametrize("cfg", [SMALL_FP8, SMALL_MX, SMALL_NV], ids=["fp8", "mxfp4", "nvfp4"])
 def test_pack_matches_layout_definition(dev, cfg):
     from paper_2609_11133_amd import binding as B
@@ -381,10 +401,16 @@ def test_pack_matches_layout_definition(dev, cfg):
     bc = W.binding_config(cfg, 8, weight_layout=1)
     src = W.to_device(hl.expert_w, dev)
     dst = torch.zeros_like(src)
-    B.moe_decode_pack_weights(bc, torch.cuda.current_stream(dev).cuda_stream, src, dst, cfg.n_experts)
+    nv = cfg.wfmt == "nvfp4"
+    ssrc = W.to_device(hl.scales, dev) if nv else None
+    sdst = torch.zeros_like(ssrc) if nv else None
+    B.moe_decode_pack_weights(bc, torch.cuda.current_stream(dev).cuda_stream, src, dst, cfg.n_experts, ssrc, sdst)
     torch.cuda.synchronize(dev)
     got = dst.cpu().numpy().view(np.uint8).reshape(hl.expert_w.view(np.uint8).shape)
     assert np.array_equal(got, pack_reference(hl.expert_w.view(np.uint8), cfg))
+    if nv:
+        gs = sdst.cpu().numpy().view(np.uint8).reshape(hl.scales.view(np.uint8).shape)
+        assert np.array_equal(gs, pack_scales_reference(hl.scales.view(np.uint8), cfg))
 
 
 # every kernel variant on packed weights: FP8 staged gate/up (H/128 a multiple of 4) and
