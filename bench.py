@@ -330,7 +330,7 @@ def main():
     bcfg = W.binding_config(cfg, Tmax, args.mstar, args.screen_min_tokens, layout)
     if layout:  # weights (and NVFP4 scales) converted once, as at load time
         packed = torch.empty_like(ew0)
-        nv = cfg.wfmt == "nvfp4"
+        nv = cfg.wfmt != "fp8"  # E2M1 weights: scales packed too
         psc = torch.empty_like(sc0) if nv else None
         B.moe_decode_pack_weights(bcfg, torch.cuda.current_stream(dev).cuda_stream, ew0, packed, cfg.n_experts,
                                   sc0 if nv else None, psc)

@@ -96,8 +96,11 @@ typedef enum {
                                   32g+32) at 1024 + 16 l, and the E4M3 scales packed
                                   the same way: per tile and 256-input block one 256-byte
                                   piece, scales [4g, 4g+4) of row l%16 at 4 l; the 16
-                                  bytes of matrix scales stay first).  FP8 and MXFP4
-                                  scales are unchanged.  Written by
+                                  bytes of matrix scales stay first).  MXFP4 E8M0 scales
+                                  are packed per tile and group of four 128-input blocks:
+                                  lane l's bytes (K sub-block g of row l%16, blocks 4q..4q+3)
+                                  at 4 l of a 256-byte piece (a last group of two blocks:
+                                  2 l, 128 bytes).  FP8 scales are unchanged.  Written by
                                   moe_decode_pack_weights.  Needs MFMA tiles for every
                                   expert (mfma_min_tokens 0 or 1). */
 } moe_wlayout;
@@ -169,12 +172,12 @@ moe_status moe_decode_forward(moe_decode_t h, void *stream, const void *x, int32
                               void *y, int32_t *topk_ids, float *topk_weights);
 
 /* Enqueue on `stream` the conversion of n_experts consecutive experts' weights (and,
- * for NVFP4, their scales) from the row-major layout (src) to packed 16-row tiles (dst),
+ * for MXFP4 and NVFP4, their scales) from the row-major layout (src) to packed 16-row tiles (dst),
  * for a handle whose configuration has weight_layout = MOE_WLAYOUT_TILED16 (the other
  * fields as for that handle; weight_layout itself is not read).  src and dst are device
  * buffers of n_experts * moe_decode_expert_weight_bytes(cfg) bytes, 16-byte aligned;
  * src_scales and dst_scales of n_experts * moe_decode_expert_scale_bytes(cfg) bytes,
- * 4-byte aligned, for NVFP4 weights, NULL for FP8 and MXFP4 ones (their scales keep their
+ * 4-byte aligned, for MXFP4 and NVFP4 weights, NULL for FP8 ones (their scales keep their
  * layout).  All owned by the caller; a source and its destination must not overlap.
  * Errors as for moe_decode_init (message in moe_decode_last_error(NULL)). */
 moe_status moe_decode_pack_weights(const moe_decode_config *cfg, void *stream, const void *src, void *dst,

@@ -178,7 +178,7 @@ def moe_decode_forward(h, stream, x, n_tokens, router_w, router_bias, expert_w, 
 def moe_decode_pack_weights(cfg: moe_decode_config, stream, src, dst, n_experts: int, src_scales=None,
                             dst_scales=None):
     """Enqueue the row-major -> packed 16-row tile conversion of n_experts experts
-    (scales too for NVFP4 weights)."""
+    (scales too for MXFP4 and NVFP4 weights)."""
     _check(lib().moe_decode_pack_weights(ctypes.byref(cfg), stream, _addr(src), _addr(dst), _addr(src_scales),
                                          _addr(dst_scales), n_experts))
 

@@ -222,15 +222,15 @@ moe_status moe_decode_pack_weights(const moe_decode_config *cfg, void *stream, c
     if ((uintptr_t)src % 16 || (uintptr_t)dst % 16) FAIL(g_init_err, MOE_ERR_INVALID, "src and dst must be 16-byte aligned");
     const size_t bytes = (size_t)n_experts * moe_decode_expert_weight_bytes(cfg);
     if (overlap(src, dst, bytes)) FAIL(g_init_err, MOE_ERR_INVALID, "src and dst overlap");
-    const bool nv = cfg->wfmt == MOE_WFMT_NVFP4_E2M1_B16;
+    const bool nv = cfg->wfmt != MOE_WFMT_FP8_E4M3_B128;  // E2M1 weights: their scales are packed too
     if (nv) {
-        if (!src_scales || !dst_scales) FAIL(g_init_err, MOE_ERR_INVALID, "NVFP4 scales need src_scales and dst_scales");
+        if (!src_scales || !dst_scales) FAIL(g_init_err, MOE_ERR_INVALID, "MXFP4 and NVFP4 scales need src_scales and dst_scales");
         if ((uintptr_t)src_scales % 4 || (uintptr_t)dst_scales % 4)
             FAIL(g_init_err, MOE_ERR_INVALID, "src_scales and dst_scales must be 4-byte aligned");
         if (overlap(src_scales, dst_scales, (size_t)n_experts * moe_decode_expert_scale_bytes(cfg)))
             FAIL(g_init_err, MOE_ERR_INVALID, "src_scales and dst_scales overlap");
     } else if (src_scales || dst_scales) {
-        FAIL(g_init_err, MOE_ERR_INVALID, "FP8 and MXFP4 scales keep their layout: pass NULL scale pointers");
+        FAIL(g_init_err, MOE_ERR_INVALID, "FP8 scales keep their layout: pass NULL scale pointers");
     }
     Layer L = {};
     L.H = cfg->hidden;

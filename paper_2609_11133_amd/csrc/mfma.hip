@@ -154,7 +154,11 @@ __device__ inline ActRsrc act_rsrc(const uint8_t *hi, const uint8_t *lo, const u
 // non-temporal loads, against 6.0-6.2 TB/s for the row-major walk with either kind.
 // The tile is the same for the whole wave, so packed fragments are read through a
 // buffer resource on it (scalar registers), the lane's offset 16l and the block's
-// offset as a scalar.
+// offset as a scalar.  With packed E2M1 weights the E8M0 scales are packed too: inside
+// each 16-row tile, per group of four K blocks, lane l's four scale bytes (K sub-block
+// g of row l%16 in blocks 4q..4q+3) sit together at 4l of a 256-byte piece (a final
+// group of two blocks: 2 bytes per lane, 128 bytes).  Read row by row, one byte per
+// lane and block, the scales bound the E2M1 kernels.
 constexpr int kNonTemporal = 2;  // cache policy of a non-temporal buffer load
 
 // This lane's weight pointer for the 16-row tile starting at row `row0` (a multiple of
@@ -171,6 +175,14 @@ __device__ inline __amdgpu_buffer_rsrc_t tile_rsrc(const uint8_t *tile)
     const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
     const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
     return __builtin_amdgcn_make_buffer_rsrc((void *)(((uint64_t)hi << 32) | lo), (short)0, -1, kRawBufferWord3);
+}
+
+// E8M0 scale byte of K block kb (of KB) from a packed tile's scales `et` (byte reads:
+// the two-tile kernels; the staged ones read a word per four blocks).
+__device__ inline int e8m0_packed(const uint8_t *et, int kb, int KB, int lane)
+{
+    const int q = kb >> 2, rem = min(4, KB - 4 * q);
+    return et[256 * q + lane * rem + (kb & 3)];
 }
 
 // Weight operand fragment of K block kb from a pointer of wlane.
@@ -217,7 +229,7 @@ __device__ inline void stream_tiles(f32x4 (&acc)[2][NT], const uint8_t *const (&
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
             F.a[t] = wfrag<FMT, PK>(arow[t], kb, g);
-            F.ea[t] = FMT == 0 ? 127 : erow[t][kb * 4 + g];
+            F.ea[t] = FMT == 0 ? 127 : (PK ? e8m0_packed(erow[t], kb, KB, __lane_id()) : erow[t][kb * 4 + g]);
         }
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
@@ -271,7 +283,7 @@ __device__ inline void stream_tiles_fixed(f32x4 (&acc)[2][NT], const uint8_t *co
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
             F.a[t] = wfrag<FMT, PK>(arow[t], kb, g);
-            F.ea[t] = FMT == 0 ? 127 : erow[t][kb * 4 + g];
+            F.ea[t] = FMT == 0 ? 127 : (PK ? e8m0_packed(erow[t], kb, KBC, __lane_id()) : erow[t][kb * 4 + g]);
         }
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
@@ -339,7 +351,8 @@ __device__ inline void w13_rows(int w, const uint8_t *__restrict__ we, const uin
     const int r0 = i0 + 16 * w;  // first row of this wave in the gate and in the up matrix
     const size_t rowb = FMT == 0 ? (size_t)H : (size_t)H / 2;
     const uint8_t *arow[2] = {wlane<PK>(we, r0, rowb, lane), wlane<PK>(we, I + r0, rowb, lane)};
-    const uint8_t *erow[2] = {se + (size_t)(r0 + r) * (H / 32), se + (size_t)(I + r0 + r) * (H / 32)};
+    const int er = PK ? 0 : r;  // packed scales: the tile's
+    const uint8_t *erow[2] = {se + (size_t)(r0 + er) * (H / 32), se + (size_t)(I + r0 + er) * (H / 32)};
     const float *sblk[2] = {(const float *)se + (size_t)(r0 / 128) * (H / 128),
                             (const float *)se + (size_t)((I + r0) / 128) * (H / 128)};
     uint32_t voff[NT], eoff[NT];
@@ -441,7 +454,8 @@ __device__ inline void w2_rows(const uint8_t *__restrict__ we2, const uint8_t *_
     const size_t rowb = FMT == 0 ? (size_t)I : (size_t)I / 2;
     const uint8_t *sd8 = se + (size_t)2 * I * (H / 32);  // MXFP4 down scales
     const uint8_t *arow[2] = {wlane<PK>(we2, n0, rowb, lane), wlane<PK>(we2, n0 + 16, rowb, lane)};
-    const uint8_t *erow[2] = {sd8 + (size_t)(n0 + r) * (I / 32), sd8 + (size_t)(n0 + 16 + r) * (I / 32)};
+    const int er = PK ? 0 : r;  // packed scales: the tile's
+    const uint8_t *erow[2] = {sd8 + (size_t)(n0 + er) * (I / 32), sd8 + (size_t)(n0 + 16 + er) * (I / 32)};
     const float *sd = (const float *)se + (size_t)2 * (I / 128) * (H / 128);
     const float *sblk[2] = {sd + (size_t)(n0 / 128) * (I / 128), sd + (size_t)((n0 + 16) / 128) * (I / 128)};
     uint32_t voff[NT], eoff[NT];
@@ -589,9 +603,23 @@ __device__ inline void stream_tile_lds(f32x4 (&acc)[NT], const uint8_t *__restri
     const int nseg = KB / kSegK;
     i32x8 A[4];
     int EA[4];
-    auto loadA = [&](int slot, int kb) {
+    // packed E8M0 scales: one word per lane and segment of four blocks, a segment ahead
+    __amdgpu_buffer_rsrc_t er;
+    if constexpr (PK && FMT == 1) er = tile_rsrc(erow);
+    auto eword = [&](int sg) -> uint32_t {
+        if constexpr (PK && FMT == 1)
+            return __builtin_amdgcn_raw_buffer_load_b32(er, 4u * lane, sg * 256, 0);
+        else
+            return 0u;
+    };
+    auto loadA = [&](int slot, int kb, uint32_t word) {  // word: the E8M0 word holding block kb
         A[slot] = wfrag<FMT, PK>(arow, kb, g);
-        EA[slot] = FMT == 0 ? 127 : erow[kb * 4 + g];
+        if constexpr (FMT == 0)
+            EA[slot] = 127;
+        else if constexpr (PK)
+            EA[slot] = (int)__builtin_amdgcn_ubfe(word, 8 * (kb & 3), 8);
+        else
+            EA[slot] = erow[kb * 4 + g];
     };
     auto compute = [&](int slot, const ActSeg &S, int kk, int kb) {
         const float s = FMT == 0 ? sblk[kb] : 1.f;
@@ -609,9 +637,10 @@ __device__ inline void stream_tile_lds(f32x4 (&acc)[NT], const uint8_t *__restri
     };
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[j] = (f32x4){0.f, 0.f, 0.f, 0.f};
-    loadA(0, 0);
-    loadA(1, 1);
-    loadA(2, 2);
+    uint32_t wc = eword(0);  // word of the segment being multiplied
+    loadA(0, 0, wc);
+    loadA(1, 1, wc);
+    loadA(2, 2, wc);
     st.load(B, 0);
     st.store(seg[0], tid);
     st.load(B, nseg > 1 ? 1 : 0);
@@ -619,11 +648,14 @@ __device__ inline void stream_tile_lds(f32x4 (&acc)[NT], const uint8_t *__restri
     for (int kb = 0; kb < KB; kb += kSegK) {  // one staged segment per iteration
         const int sg = kb / kSegK;
         const ActSeg &cur = seg[sg & 1];
+        const uint32_t wn = eword(min(sg + 1, nseg - 1));  // the next segment's (the last one's past the end)
 #pragma unroll
         for (int u = 0; u < kSegK; ++u) {
-            loadA((u + 3) & 3, min(kb + u + 3, KB - 1));  // past the end: reload the last block
+            // block kb+3 is this segment's, kb+4.. the next one's; past the end: reload the last block
+            loadA((u + 3) & 3, min(kb + u + 3, KB - 1), u == 0 ? wc : wn);
             compute(u, cur, u, kb + u);
         }
+        wc = wn;
         st.store(seg[(sg + 1) & 1], tid);
         st.load(B, min(sg + 2, nseg - 1));
         sync_lds();
@@ -647,7 +679,7 @@ __device__ inline void w13_item_lds(const uint8_t *__restrict__ we, const uint8_
     const int r = lane & 15, g = lane >> 4;
     const int row0 = (wave >= HW ? I : 0) + i0 + 16 * (wave % HW);
     const uint8_t *arow = wlane<PK>(we, row0, FMT == 0 ? (size_t)H : (size_t)H / 2, lane);
-    const uint8_t *erow = se + (size_t)(row0 + r) * (H / 32);
+    const uint8_t *erow = se + (size_t)(row0 + (PK ? 0 : r)) * (H / 32);
     const float *sblk = (const float *)se + (size_t)(row0 / 128) * (H / 128);
     Stager<NT, W> st;
     st.init(tok_of, slot0, mc, H, tid);
@@ -738,7 +770,7 @@ __device__ inline void w2_item_lds(const uint8_t *__restrict__ we2, const uint8_
     const int r = lane & 15, g = lane >> 4;
     const int row0 = n0 + 16 * wave;
     const uint8_t *arow = wlane<PK>(we2, row0, FMT == 0 ? (size_t)I : (size_t)I / 2, lane);
-    const uint8_t *erow = se + (size_t)2 * I * (H / 32) + (size_t)(row0 + r) * (I / 32);
+    const uint8_t *erow = se + (size_t)2 * I * (H / 32) + (size_t)(row0 + (PK ? 0 : r)) * (I / 32);
     const float *sblk = (const float *)se + (size_t)2 * (I / 128) * (H / 128) + (size_t)(row0 / 128) * (I / 128);
     Stager<NT, W> st;
     st.init(nullptr, slot0, mc, I, tid);
@@ -881,6 +913,33 @@ __global__ void pack_kernel(const uint8_t *__restrict__ src, uint8_t *__restrict
     }
 }
 
+// MXFP4 E8M0 scales, row-major -> packed 16-row tiles (the layout above): per expert the
+// [2I][H/32] gate/up scales, then the [H][I/32] down scales.  One thread per byte of the
+// destination.
+__global__ void pack_e8m0_kernel(const uint8_t *__restrict__ src, uint8_t *__restrict__ dst, int64_t n_bytes, int H,
+                                 int I, int64_t expert_bytes)
+{
+    const int64_t w13 = (int64_t)2 * I * (H / 32);
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < n_bytes; p += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t e = p / expert_bytes, eo = p % expert_bytes;
+        const bool down = eo >= w13;
+        const int64_t mo = down ? eo - w13 : eo;
+        const int K = down ? I : H, KB = K / 128;
+        const int64_t rowb = K / 32;
+        const int64_t tile = mo / (16 * rowb);
+        const int o = (int)(mo % (16 * rowb));
+        const int nfull = KB / 4;
+        int q, rem, oo;
+        if (o < 256 * nfull) {
+            q = o / 256, rem = 4, oo = o % 256;
+        } else {
+            q = nfull, rem = KB % 4, oo = o - 256 * nfull;
+        }
+        const int l = oo / rem, kb = 4 * q + oo % rem, r = l & 15, g = l >> 4;
+        dst[p] = src[e * expert_bytes + (down ? w13 : 0) + (tile * 16 + r) * rowb + kb * 4 + g];
+    }
+}
+
 // NVFP4 E4M3 scales, row-major -> packed 16-row tiles: per matrix [rows][K/16] bytes
 // after each expert's 16 bytes of matrix scales; per (16-row tile, 256-input block) one
 // 256-byte piece, lane l's 4 bytes (scales [4g, 4g+4) of row l%16) at 4l.  One thread
@@ -936,6 +995,13 @@ hipError_t launch_w2_mfma(const Layer &L, const void *expert_w, const void *scal
 
 hipError_t launch_pack_scales(const Layer &L, const void *src, void *dst, int n_experts, hipStream_t st)
 {
+    if (L.wfmt == 1) {
+        const int64_t bytes = (int64_t)n_experts * (int64_t)L.expert_s_bytes;
+        const int64_t blocks = (bytes + 255) / 256;
+        pack_e8m0_kernel<<<(unsigned)(blocks < 16384 ? blocks : 16384), 256, 0, st>>>(
+            (const uint8_t *)src, (uint8_t *)dst, bytes, L.H, L.I, (int64_t)L.expert_s_bytes);
+        return hipGetLastError();
+    }
     const int64_t body = (int64_t)2 * L.I * (L.H / 16) + (int64_t)L.H * (L.I / 16);
     const int64_t words = (int64_t)n_experts * body / 4;
     const int64_t blocks = (words + 255) / 256;

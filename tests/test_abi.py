@@ -316,6 +316,7 @@ def test_weight_layout_accepted(B):
         (dict(dst=8), "aligned"),
         (dict(dst=256 + 1024), "overlap"),
         (dict(ssrc=1 << 31), "keep their layout"),  # FP8 scales are not converted
+        (dict(wfmt=1), "need src_scales"),
         (dict(wfmt=2), "need src_scales"),
         (dict(wfmt=2, ssrc=1 << 31, sdst=(1 << 31) + 2), "4-byte aligned"),
         (dict(wfmt=2, ssrc=1 << 31, sdst=(1 << 31) + 64), "scales overlap"),

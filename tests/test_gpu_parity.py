@@ -49,9 +49,9 @@ class Run:
         self.bias = W.to_device(hl.bias, dev)
         self.ew = W.to_device(hl.expert_w, dev)
         self.sc = W.to_device(hl.scales, dev)
-        if weight_layout == 1:  # the library's own conversion of the row-major weights (and NVFP4 scales)
+        if weight_layout == 1:  # the library's own conversion of the row-major weights (and E2M1 scales)
             packed = torch.empty_like(self.ew)
-            nv = cfg.wfmt == "nvfp4"
+            nv = cfg.wfmt != "fp8"
             psc = torch.empty_like(self.sc) if nv else None
             B.moe_decode_pack_weights(bc, torch.cuda.current_stream(dev).cuda_stream, self.ew, packed, cfg.n_experts,
                                       self.sc if nv else None, psc)
@@ -379,12 +379,26 @@ def pack_reference(expert_w, cfg):
 
 
 def pack_scales_reference(scales, cfg):
-    """Packed NVFP4 E4M3 scales: per expert the 16 bytes of matrix scales, then per
+    """Packed scales.  NVFP4 E4M3: per expert the 16 bytes of matrix scales, then per
     matrix [rows][K/16] and per (16-row tile, 256-input block) 256 bytes, lane l's
-    scales [4g, 4g+4) of row l%16 at 4l."""
+    scales [4g, 4g+4) of row l%16 at 4l.  MXFP4 E8M0: per matrix [rows][K/32] and per
+    (16-row tile, group of four 128-input blocks) lane l's bytes (sub-block g of row l%16,
+    blocks 4q..4q+3) at 4l (a last group of two blocks: 2l)."""
     H, I, E = cfg.hidden, cfg.inter, cfg.n_experts
     sc = scales.reshape(E, -1)
     out = sc.copy()
+    if cfg.wfmt == "mxfp4":
+        off = 0
+        for rows, K in ((2 * I, H), (H, I)):
+            KB = K // 128
+            m = sc[:, off: off + rows * K // 32].reshape(E, rows // 16, 16, KB, 4)  # [E][tile][r][kb][g]
+            parts = []
+            for q0 in range(0, KB, 4):
+                n = min(4, KB - q0)
+                parts.append(m[:, :, :, q0: q0 + n, :].transpose(0, 1, 4, 2, 3).reshape(E, rows // 16, -1))
+            out[:, off: off + rows * K // 32] = np.concatenate(parts, axis=2).reshape(E, -1)
+            off += rows * K // 32
+        return out.reshape(scales.shape)
     off = 16
     for rows, K in ((2 * I, H), (H, I)):
         m = sc[:, off: off + rows * K // 16].reshape(E, rows // 16, 16, K // 256, 4, 4)
@@ -393,7 +407,10 @@ def pack_scales_reference(scales, cfg):
     return out.reshape(scales.shape)
 
 
-@pytest.mark.parametrize("cfg", [SMALL_FP8, SMALL_MX, SMALL_NV], ids=["fp8", "mxfp4", "nvfp4"])
+PACK_MX_768 = LayerConfig("pk-mx-768", 768, 16, 4, 768, "bf16", "bf16", "mxfp4", None, [])
+
+
+@pytest.mark.parametrize("cfg", [SMALL_FP8, SMALL_MX, PACK_MX_768, SMALL_NV], ids=["fp8", "mxfp4", "mxfp4-768", "nvfp4"])
 def test_pack_matches_layout_definition(dev, cfg):
     from paper_2609_11133_amd import binding as B
 
@@ -401,7 +418,7 @@ def test_pack_matches_layout_definition(dev, cfg):
     bc = W.binding_config(cfg, 8, weight_layout=1)
     src = W.to_device(hl.expert_w, dev)
     dst = torch.zeros_like(src)
-    nv = cfg.wfmt == "nvfp4"
+    nv = cfg.wfmt != "fp8"
     ssrc = W.to_device(hl.scales, dev) if nv else None
     sdst = torch.zeros_like(ssrc) if nv else None
     B.moe_decode_pack_weights(bc, torch.cuda.current_stream(dev).cuda_stream, src, dst, cfg.n_experts, ssrc, sdst)
