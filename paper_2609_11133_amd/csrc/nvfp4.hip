@@ -15,7 +15,7 @@
 // two applied by the conversion, and one packed f16 multiply applies the scale's
 // mantissa 1 + j/8 (every product has at most 5 significant bits and lies in
 // [2^-13, 2688]: exact).  x enters as the routing kernel's f16 copy x * 2^-k (k per
-// token, so that every value at least 2^-10 of the token's maximum converts exactly),
+// token, so that every value at least 2^-31 of the token's maximum converts exactly),
 // and the accumulators are multiplied by 2^k.
 //
 // Operand layout of v_mfma_f32_16x16x32_bf16 (checked on the device): lane l holds

@@ -560,7 +560,7 @@ __device__ __attribute__((always_inline)) inline void write_split(const RouteArg
 }
 
 // The token's bf16 x as f16 scaled by 2^-k, with k such that max|x| * 2^-k lies in
-// [2^14, 2^15) (k = 0 for a zero row; k >= -112): every value at least 2^-10 of the
+// [2^14, 2^15) (k = 0 for a zero row; k >= -112): every value at least 2^-31 of the
 // row's maximum converts exactly.  Called by `nw` waves (wave index w), each of which
 // takes the row maximum on its own (no barrier among them) and converts every nw-th
 // group of eight inputs.
