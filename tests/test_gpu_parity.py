@@ -523,6 +523,17 @@ def test_random_nvfp4_layers(dev, i):
     check_layer(run, W.host_x(cfg, T, seed=750 + i), label=f"random nvfp4 {i}")
 
 
+@pytest.mark.parametrize("i", range(10))
+def test_random_packed_layers(dev, i):
+    """Random shapes of all three weight formats on packed 16-row tiles (and packed E2M1
+    scales), MFMA for every expert, screened routing forced on every other case."""
+    cfg, T = _random_layer(100 + i) if i % 3 else _random_nvfp4_layer(100 + i)
+    hl = W.host_layer(cfg, seed=780 + i)
+    run = Run(cfg, hl, dev, max_tokens=T, mfma_min_tokens=1, screen_min_tokens=[1, -1][i % 2], weight_layout=1)
+    say(f"[random packed] {cfg}")
+    check_layer(run, W.host_x(cfg, T, seed=780 + i), label=f"random packed {i}")
+
+
 # ---------------------------------------------------------------- full-size layers
 
 @pytest.fixture(scope="module")
