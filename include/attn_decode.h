@@ -55,12 +55,15 @@ typedef struct attn_decode_config {
     int32_t page_size;         /* P: 16 */
     int32_t max_batch;         /* largest B of any call, 1..4096 */
     int32_t max_pages_per_seq; /* block-table row length, 1..65536 */
-    int32_t fused_merge_max_splits; /* the context is split into 256-token pieces; when a
-                                  row of max_pages_per_seq pages needs at most this many,
-                                  the split kernel merges them itself (its last workgroup
-                                  per sequence and key/value head), else a second kernel
-                                  does.  0 = library default 16, negative = never, at most
-                                  16.  The result is the same bits either way. */
+    int32_t fused_merge_max_splits; /* the context is cut into 256-token pieces.  At most
+                                  this many splits per sequence: when a row of
+                                  max_pages_per_seq pages has more pieces, each workgroup
+                                  walks R consecutive pieces (the smallest R that fits,
+                                  online softmax across them), and the split kernel merges
+                                  the splits itself (its last workgroup per sequence and
+                                  key/value head).  0 = library default 16, at most 16;
+                                  negative = one piece per split, merged by a second
+                                  kernel.  Where R = 1 both merges give the same bits. */
     int32_t reserved[3];       /* must be zero */
 } attn_decode_config;
 

@@ -77,9 +77,10 @@ __device__ inline bf16x8 as_bf16x8(const u32x4v &u) { return __builtin_bit_cast(
 
 // Split kernel: partial (max, sum, O) of one 256-token split for one (sequence, key/value
 // head) and its query heads.  Grid (splits, Hkv, B), 256 threads.  Scores are kept in
-// log2 units (scale * log2 e folded in), so p = exp2(s - m).  FUSED: the merge of the
-// splits happens here (S <= kFusedSplits; `cnt` holds one zeroed counter per (b, g),
-// left at zero again), and `out` is written here.
+// log2 units (scale * log2 e folded in), so p = exp2(s - m).  A split is R consecutive
+// chunks (online softmax across them).  FUSED: the merge of the splits happens here
+// (S <= kFusedSplits; `cnt` holds one zeroed counter per (b, g), left at zero again), and
+// `out` is written here.
 template <bool FUSED>
 __global__ __launch_bounds__(256) void attn_split_kernel(const uint16_t *__restrict__ q,
                                                          const uint16_t *__restrict__ kc,
@@ -87,16 +88,16 @@ __global__ __launch_bounds__(256) void attn_split_kernel(const uint16_t *__restr
                                                          const int32_t *__restrict__ block_table, int max_pages,
                                                          const int32_t *__restrict__ ctx, int Hkv, int G,
                                                          float scale_log2, float *__restrict__ po,
-                                                         float *__restrict__ pml, int S, int32_t *__restrict__ cnt,
-                                                         uint16_t *__restrict__ out)
+                                                         float *__restrict__ pml, int S, int R,
+                                                         int32_t *__restrict__ cnt, uint16_t *__restrict__ out)
 {
-    __shared__ float s_max[kWaves][16], s_sum[kWaves][16];
+    __shared__ float s_max[2][kWaves][16], s_sum[kWaves][16];
     __shared__ f32x4 red[kWaves][kDT][64];
     __shared__ float s_w[FUSED ? kFusedSplits : 1][16], s_den[16];
     __shared__ int s_last;
     const int c = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
     const int L = min(max(ctx[b], 0), max_pages * kP);
-    const int t0 = c * kChunk;
+    const int t0 = c * R * kChunk;  // first token of this split
     const int tid = threadIdx.x, lane = tid & 63;
     uint16_t *orow = out + ((size_t)b * Hkv + g) * G * kD;  // the group's [G][D] outputs
     if (t0 >= L) {  // uniform over the workgroup
@@ -119,98 +120,124 @@ __global__ __launch_bounds__(256) void attn_split_kernel(const uint16_t *__restr
         }
     }
 
-    // This wave's four pages: keys (token r, dims [32i + 8lg, +8)) and values (dims
-    // 16j + r, tokens [4lg, 4lg + 4)).  Pages past the context or outside the cache
-    // read as zeros.
-    const int tw = t0 + kWaveTok * wave;
-    u32x4v ka[kTiles][4];
-    u32x2v vb[kTiles][kDT];
-#pragma unroll
-    for (int tt = 0; tt < kTiles; ++tt) {
-        const int ts = tw + kP * tt;  // first token of the tile (page aligned)
-        int pg = ts < L ? block_table[(size_t)b * max_pages + ts / kP] : -1;
-        pg = __builtin_amdgcn_readfirstlane(pg);
-        const bool ok = pg >= 0 && (int64_t)pg < n_pages;
-        const int64_t p = ok ? pg : 0;
-        const __amdgpu_buffer_rsrc_t kr = rsrc(kc + (p * Hkv + g) * (int64_t)(kP * kD), ok ? kP * kD * 2 : 0);
-        const __amdgpu_buffer_rsrc_t vr = rsrc(vc + (p * Hkv + g) * (int64_t)(kP * kD), ok ? kP * kD * 2 : 0);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            ka[tt][i] = __builtin_amdgcn_raw_buffer_load_b128(kr, (uint32_t)((r * kD + 32 * i + 8 * lg) * 2), 0, 0);
-#pragma unroll
-        for (int j = 0; j < kDT; ++j)
-            vb[tt][j] = __builtin_amdgcn_raw_buffer_load_b64(vr, (uint32_t)(((16 * j + r) * kP + 4 * lg) * 2), 0, 0);
-    }
-
-    // scores of this lane's 16 (token, head r) pairs, masked past the context
-    float s[kTiles][4];
-    float m = -INFINITY;
-#pragma unroll
-    for (int tt = 0; tt < kTiles; ++tt) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ka[tt][i]), qop[i], acc, 0, 0, 0);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const bool live = tw + kP * tt + 4 * lg + e < L;
-            s[tt][e] = live ? acc[e] * scale_log2 : -INFINITY;
-            m = fmaxf(m, s[tt][e]);
-        }
-    }
-    m = fmaxf(m, __shfl_xor(m, 16));
-    m = fmaxf(m, __shfl_xor(m, 32));
-    if (lg == 0) s_max[wave][r] = m;
-    __syncthreads();
-    m = fmaxf(fmaxf(s_max[0][r], s_max[1][r]), fmaxf(s_max[2][r], s_max[3][r]));  // finite: token t0 < L
-
-    // probabilities (bf16 for the P.V product; the sum uses the same rounded values)
-    float l = 0.f;
-    bf16x8 pa[kTiles / 2];
-#pragma unroll
-    for (int st = 0; st < kTiles / 2; ++st)
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-#pragma unroll
-            for (int e = 0; e < 4; e += 2) {
-                const f32x2 pv = {exp2f(s[2 * st + h][e] - m), exp2f(s[2 * st + h][e + 1] - m)};
-                const bf16x2 pb = __builtin_convertvector(pv, bf16x2);
-                pa[st][4 * h + e] = pb.x;
-                pa[st][4 * h + e + 1] = pb.y;
-                l += (float)pb.x + (float)pb.y;
-            }
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
-    if (lg == 0) s_sum[wave][r] = l;
-
-    // values past the context are zeroed: a cache slot past it may hold any bits, and
-    // 0 * NaN would not vanish
-#pragma unroll
-    for (int tt = 0; tt < kTiles; ++tt) {
-        const int nv = min(max(L - (tw + kP * tt + 4 * lg), 0), 4);
-        const uint32_t m0 = nv >= 2 ? 0xFFFFFFFFu : (nv == 1 ? 0x0000FFFFu : 0u);
-        const uint32_t m1 = nv >= 4 ? 0xFFFFFFFFu : (nv == 3 ? 0x0000FFFFu : 0u);
-#pragma unroll
-        for (int j = 0; j < kDT; ++j) {
-            vb[tt][j].x &= m0;
-            vb[tt][j].y &= m1;
-        }
-    }
+    // R consecutive 256-token chunks of the context per workgroup (online softmax across
+    // them: a running maximum per head rescales the sums and the P.V accumulators)
+    float m_run = -INFINITY, l_run = 0.f, m = -INFINITY;
     f32x4 o[kDT];
 #pragma unroll
     for (int j = 0; j < kDT; ++j) o[j] = (f32x4){0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int st = 0; st < kTiles / 2; ++st)
-#pragma unroll
-        for (int j = 0; j < kDT; ++j) {
-            const u32x4v vv = {vb[2 * st][j].x, vb[2 * st][j].y, vb[2 * st + 1][j].x, vb[2 * st + 1][j].y};
-            o[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa[st], as_bf16x8(vv), o[j], 0, 0, 0);
+    for (int rr = 0; rr < R; ++rr) {
+        const int t0 = (c * R + rr) * kChunk;
+        if (t0 >= L) break;  // uniform over the workgroup
+        // This wave's four pages: keys (token r, dims [32i + 8lg, +8)) and values (dims
+        // 16j + r, tokens [4lg, 4lg + 4)).  Pages past the context or outside the cache
+        // read as zeros.
+        const int tw = t0 + kWaveTok * wave;
+        u32x4v ka[kTiles][4];
+        u32x2v vb[kTiles][kDT];
+    #pragma unroll
+        for (int tt = 0; tt < kTiles; ++tt) {
+            const int ts = tw + kP * tt;  // first token of the tile (page aligned)
+            int pg = ts < L ? block_table[(size_t)b * max_pages + ts / kP] : -1;
+            pg = __builtin_amdgcn_readfirstlane(pg);
+            const bool ok = pg >= 0 && (int64_t)pg < n_pages;
+            const int64_t p = ok ? pg : 0;
+            const __amdgpu_buffer_rsrc_t kr = rsrc(kc + (p * Hkv + g) * (int64_t)(kP * kD), ok ? kP * kD * 2 : 0);
+            const __amdgpu_buffer_rsrc_t vr = rsrc(vc + (p * Hkv + g) * (int64_t)(kP * kD), ok ? kP * kD * 2 : 0);
+    #pragma unroll
+            for (int i = 0; i < 4; ++i)
+                ka[tt][i] = __builtin_amdgcn_raw_buffer_load_b128(kr, (uint32_t)((r * kD + 32 * i + 8 * lg) * 2), 0, 0);
+    #pragma unroll
+            for (int j = 0; j < kDT; ++j)
+                vb[tt][j] = __builtin_amdgcn_raw_buffer_load_b64(vr, (uint32_t)(((16 * j + r) * kP + 4 * lg) * 2), 0, 0);
         }
+
+        // scores of this lane's 16 (token, head r) pairs, masked past the context
+        float s[kTiles][4];
+        m = -INFINITY;
+    #pragma unroll
+        for (int tt = 0; tt < kTiles; ++tt) {
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    #pragma unroll
+            for (int i = 0; i < 4; ++i) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(ka[tt][i]), qop[i], acc, 0, 0, 0);
+    #pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const bool live = tw + kP * tt + 4 * lg + e < L;
+                s[tt][e] = live ? acc[e] * scale_log2 : -INFINITY;
+                m = fmaxf(m, s[tt][e]);
+            }
+        }
+        m = fmaxf(m, __shfl_xor(m, 16));
+        m = fmaxf(m, __shfl_xor(m, 32));
+        if (lg == 0) s_max[rr & 1][wave][r] = m;
+        __syncthreads();
+        m = fmaxf(fmaxf(s_max[rr & 1][0][r], s_max[rr & 1][1][r]), fmaxf(s_max[rr & 1][2][r], s_max[rr & 1][3][r]));
+        // running maximum (finite: token t0 < L); alpha rescales what earlier chunks added
+        // (0 on the first chunk, whose sums start at zero)
+        const float m_new = fmaxf(m_run, m);
+        const float alpha = exp2f(m_run - m_new);
+        m_run = m_new;
+        m = m_new;
+
+        // probabilities (bf16 for the P.V product; the sum uses the same rounded values)
+        float l = 0.f;
+        bf16x8 pa[kTiles / 2];
+    #pragma unroll
+        for (int st = 0; st < kTiles / 2; ++st)
+    #pragma unroll
+            for (int h = 0; h < 2; ++h)
+    #pragma unroll
+                for (int e = 0; e < 4; e += 2) {
+                    const f32x2 pv = {exp2f(s[2 * st + h][e] - m), exp2f(s[2 * st + h][e + 1] - m)};
+                    const bf16x2 pb = __builtin_convertvector(pv, bf16x2);
+                    pa[st][4 * h + e] = pb.x;
+                    pa[st][4 * h + e + 1] = pb.y;
+                    l += (float)pb.x + (float)pb.y;
+                }
+        l += __shfl_xor(l, 16);
+        l += __shfl_xor(l, 32);
+        l_run = l_run * alpha + l;
+
+        // values past the context are zeroed: a cache slot past it may hold any bits, and
+        // 0 * NaN would not vanish
+    #pragma unroll
+        for (int tt = 0; tt < kTiles; ++tt) {
+            const int nv = min(max(L - (tw + kP * tt + 4 * lg), 0), 4);
+            const uint32_t m0 = nv >= 2 ? 0xFFFFFFFFu : (nv == 1 ? 0x0000FFFFu : 0u);
+            const uint32_t m1 = nv >= 4 ? 0xFFFFFFFFu : (nv == 3 ? 0x0000FFFFu : 0u);
+    #pragma unroll
+            for (int j = 0; j < kDT; ++j) {
+                vb[tt][j].x &= m0;
+                vb[tt][j].y &= m1;
+            }
+        }
+        // o holds heads 4lg..4lg+3 of the P.V result: their rescale factors come from the
+        // lanes that hold those heads in the score layout
+        {
+            float a4[4];
+    #pragma unroll
+            for (int i = 0; i < 4; ++i) a4[i] = __shfl(alpha, 4 * lg + i);
+    #pragma unroll
+            for (int j = 0; j < kDT; ++j)
+    #pragma unroll
+                for (int i = 0; i < 4; ++i) o[j][i] *= a4[i];
+        }
+    #pragma unroll
+        for (int st = 0; st < kTiles / 2; ++st)
+    #pragma unroll
+            for (int j = 0; j < kDT; ++j) {
+                const u32x4v vv = {vb[2 * st][j].x, vb[2 * st][j].y, vb[2 * st + 1][j].x, vb[2 * st + 1][j].y};
+                o[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa[st], as_bf16x8(vv), o[j], 0, 0, 0);
+            }
+    }
+    m = m_run;
+    if (lg == 0) s_sum[wave][r] = l_run;
 
     // the workgroup's O: the four waves' partials in wave order
 #pragma unroll
     for (int j = 0; j < kDT; ++j) red[wave][j][lane] = o[j];
     __syncthreads();
-    const int ns = (L + kChunk - 1) / kChunk;  // splits of this sequence
+    const int ns = (L + R * kChunk - 1) / (R * kChunk);  // splits of this sequence
     if (FUSED && ns == 1) {
         // the only split: out = O / l (what the merge of one split gives)
 #pragma unroll
@@ -421,10 +448,14 @@ size_t partial_ml_bytes(const attn_decode_config *c)
 size_t counter_words(const attn_decode_config *c) { return (size_t)c->max_batch * c->n_kv_heads; }
 
 // The split kernel merges the splits itself when every sequence has at most this many.
-bool fused(const attn_decode_config *c)
+// Chunks of 256 tokens per workgroup: the smallest R that leaves at most `lim` splits
+// per row (the split kernel then merges them itself); 0 when the configuration asks for
+// the second kernel's merge (every chunk its own split).
+int chunks_per_split(const attn_decode_config *c)
 {
+    if (c->fused_merge_max_splits < 0) return 0;
     const int lim = c->fused_merge_max_splits == 0 ? kFusedSplits : c->fused_merge_max_splits;
-    return max_splits(c) <= lim;
+    return (max_splits(c) + lim - 1) / lim;
 }
 
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
@@ -484,22 +515,24 @@ extern "C" int attn_decode_forward(const attn_decode_config *cfg, void *workspac
         return fail(ATTN_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", workspace_bytes,
                     attn_decode_workspace_bytes(cfg));
     if (batch == 0) return ATTN_OK;
-    const int Hkv = cfg->n_kv_heads, G = cfg->n_q_heads / Hkv, S = max_splits(cfg);
+    const int Hkv = cfg->n_kv_heads, G = cfg->n_q_heads / Hkv, R = chunks_per_split(cfg);
     float *po = (float *)workspace;
     float *pml = (float *)((char *)workspace + partial_o_bytes(cfg));
     int32_t *cnt = (int32_t *)((char *)workspace + partial_o_bytes(cfg) + partial_ml_bytes(cfg));
     hipStream_t st = (hipStream_t)stream;
-    if (fused(cfg)) {
+    if (R > 0) {
+        const int S = (max_splits(cfg) + R - 1) / R;  // at most the limit
         attn_split_kernel<true><<<dim3(S, Hkv, batch), 256, 0, st>>>(
             (const uint16_t *)q, (const uint16_t *)k_cache, (const uint16_t *)v_cache, n_pages, block_table,
-            cfg->max_pages_per_seq, ctx_lens, Hkv, G, scale * kLog2e, po, pml, S, cnt, (uint16_t *)out);
+            cfg->max_pages_per_seq, ctx_lens, Hkv, G, scale * kLog2e, po, pml, S, R, cnt, (uint16_t *)out);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return fail(ATTN_ERR_HIP, "split kernel launch: %s", hipGetErrorString(e));
         return ATTN_OK;
     }
+    const int S = max_splits(cfg);
     attn_split_kernel<false><<<dim3(S, Hkv, batch), 256, 0, st>>>(
         (const uint16_t *)q, (const uint16_t *)k_cache, (const uint16_t *)v_cache, n_pages, block_table,
-        cfg->max_pages_per_seq, ctx_lens, Hkv, G, scale * kLog2e, po, pml, S, cnt, (uint16_t *)out);
+        cfg->max_pages_per_seq, ctx_lens, Hkv, G, scale * kLog2e, po, pml, S, 1, cnt, (uint16_t *)out);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(ATTN_ERR_HIP, "split kernel launch: %s", hipGetErrorString(e));
     attn_combine_kernel<<<dim3(G, Hkv, batch), 128, 0, st>>>(po, pml, ctx_lens, cfg->max_pages_per_seq, Hkv, G, S,

@@ -7,8 +7,9 @@ out over the context), with fp32 accumulation; 1e-2 leaves about a fivefold marg
 Small cases cover every split/page boundary and ragged tail, empty contexts, group
 sizes 1-16, bytes past the contexts holding NaN, and page indices outside the cache,
 with the splits merged inside the split kernel and by the second kernel (the two give
-the same bits); the full-size agentic steps of both models are compared on every row,
-the 32K-token long-context step on sampled sequences."""
+the same bits when each split is one 256-token piece), and with several pieces per split
+(online softmax inside a workgroup); the full-size agentic steps of both models are
+compared on every row, the 32K-token long-context step on sampled sequences."""
 import sys
 
 import numpy as np
@@ -87,6 +88,9 @@ def test_small_cases(dev, hq, hkv):
     check(bf16_to_f64(out), ref, label=cfg.name)
     out2, _, _ = run_gpu(cfg, h, dev, scale, fused=-1)  # merged by the second kernel
     assert torch.equal(out, out2), "the two merges differ"
+    for lim in (2, 1):  # 5 pieces: 3 per split (2 splits), or all 5 in one workgroup
+        out3, _, _ = run_gpu(cfg, h, dev, scale, fused=lim)
+        check(bf16_to_f64(out3), ref, label=f"{cfg.name} at most {lim} splits")
 
 
 @pytest.mark.parametrize("name", ["qwen3-235b-a22b-attn-agentic", "qwen3-coder-480b-a35b-tp4-attn-agentic"])
@@ -161,12 +165,14 @@ def test_full_size_step(dev, name):
 
 
 def test_long_context_sampled(dev):
-    """32K-token contexts (128 splits per sequence), checked on three sampled sequences."""
+    """32K-token contexts (128 pieces per sequence), checked on three sampled sequences:
+    16 splits of 8 pieces merged in the split kernel (the default), and 128 one-piece
+    splits merged by the second kernel."""
     cfg = A.ATTN_BY_NAME["qwen3-235b-a22b-attn-long32k"]
     h = A.host_attn(cfg, draw=2)
     scale = 1 / np.sqrt(128)
-    out, _, _ = run_gpu(cfg, h, dev, scale)
-    got = bf16_to_f64(out)
     rows = [0, 11, cfg.batch - 1]
     ref = oracle.attn_decode(h.q[rows], h.k_cache, h.v_cache, h.block_table[rows], h.ctx[rows], scale)
-    check(got, ref, rows=rows, label=cfg.name)
+    for fused in (0, -1):
+        out, _, _ = run_gpu(cfg, h, dev, scale, fused=fused)
+        check(bf16_to_f64(out), ref, rows=rows, label=f"{cfg.name} fused_merge_max_splits={fused}")
