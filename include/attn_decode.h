@@ -55,15 +55,20 @@ typedef struct attn_decode_config {
     int32_t page_size;         /* P: 16 */
     int32_t max_batch;         /* largest B of any call, 1..4096 */
     int32_t max_pages_per_seq; /* block-table row length, 1..65536 */
-    int32_t fused_merge_max_splits; /* the context is cut into 256-token pieces.  At most
-                                  this many splits per sequence: when a row of
-                                  max_pages_per_seq pages has more pieces, each workgroup
-                                  walks R consecutive pieces (the smallest R that fits,
-                                  online softmax across them), and the split kernel merges
-                                  the splits itself (its last workgroup per sequence and
-                                  key/value head).  0 = library default 16, at most 16;
-                                  negative = one piece per split, merged by a second
-                                  kernel.  Where R = 1 both merges give the same bits. */
+    int32_t fused_merge_max_splits; /* the context is cut into 256-token pieces, and each
+                                  workgroup walks R consecutive pieces of a row of
+                                  max_pages_per_seq pages (online softmax across them),
+                                  with R the smallest that leaves at most this many splits
+                                  per sequence; R grows further when one piece per
+                                  workgroup would need more than two rounds of resident
+                                  workgroups for max_batch sequences (then the grid is at
+                                  most three workgroups per compute unit).  The split
+                                  kernel merges the splits itself (its last workgroup per
+                                  sequence and key/value head).  0 = library default 16,
+                                  at most 16; negative = one piece per split, merged by a
+                                  second kernel.  Where R = 1 both merges give the same
+                                  bits; R depends only on this configuration and the
+                                  device. */
     int32_t reserved[3];       /* must be zero */
 } attn_decode_config;
 

@@ -448,14 +448,38 @@ size_t partial_ml_bytes(const attn_decode_config *c)
 size_t counter_words(const attn_decode_config *c) { return (size_t)c->max_batch * c->n_kv_heads; }
 
 // The split kernel merges the splits itself when every sequence has at most this many.
-// Chunks of 256 tokens per workgroup: the smallest R that leaves at most `lim` splits
-// per row (the split kernel then merges them itself); 0 when the configuration asks for
-// the second kernel's merge (every chunk its own split).
+// Compute units of the current device (cached per device; 0 if the query fails).
+int compute_units()
+{
+    static int cus[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    if (cus[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+        cus[dev] = n;
+    }
+    return cus[dev];
+}
+
+// 256-token chunks per workgroup; 0 when the configuration asks for the second kernel's
+// merge (every chunk its own split).  At least enough that `lim` splits cover a row.
+// When one chunk per split would need more than two rounds of resident workgroups (two
+// per compute unit), the splits grow until the grid is at most three workgroups per
+// compute unit: the walk inside a workgroup keeps as many loads in flight as more
+// workgroups would, with fewer partials to merge.  Only the configuration enters, so a
+// sequence's result does not depend on the batch it is called in.
 int chunks_per_split(const attn_decode_config *c)
 {
     if (c->fused_merge_max_splits < 0) return 0;
     const int lim = c->fused_merge_max_splits == 0 ? kFusedSplits : c->fused_merge_max_splits;
-    return (max_splits(c) + lim - 1) / lim;
+    const int sf = max_splits(c);
+    int R = (sf + lim - 1) / lim;
+    const long rows = (long)c->n_kv_heads * c->max_batch;  // workgroups per split index
+    const long slots = 2L * compute_units();
+    if (slots > 0 && (long)sf * rows > 2 * slots)
+        while (R < sf && (long)((sf + R - 1) / R) * rows > slots * 3 / 2) ++R;
+    return R;
 }
 
 bool aligned(const void *p, size_t a) { return ((uintptr_t)p & (a - 1)) == 0; }

@@ -166,8 +166,9 @@ def test_full_size_step(dev, name):
 
 def test_long_context_sampled(dev):
     """32K-token contexts (128 pieces per sequence), checked on three sampled sequences:
-    16 splits of 8 pieces merged in the split kernel (the default), and 128 one-piece
-    splits merged by the second kernel."""
+    8 splits of 16 pieces merged in the split kernel (the default on 256 compute units:
+    at most three workgroups per unit), and 128 one-piece splits merged by the second
+    kernel."""
     cfg = A.ATTN_BY_NAME["qwen3-235b-a22b-attn-long32k"]
     h = A.host_attn(cfg, draw=2)
     scale = 1 / np.sqrt(128)
