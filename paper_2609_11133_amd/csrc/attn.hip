@@ -24,6 +24,8 @@
 // row/column l%16 and K [8g, 8g+8) with g = l/16; the result gives lane l rows
 // 4g..4g+3 of column l%16.
 #include <hip/hip_runtime.h>
+
+#include <atomic>
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
@@ -448,18 +450,19 @@ size_t partial_ml_bytes(const attn_decode_config *c)
 size_t counter_words(const attn_decode_config *c) { return (size_t)c->max_batch * c->n_kv_heads; }
 
 // The split kernel merges the splits itself when every sequence has at most this many.
-// Compute units of the current device (cached per device; 0 if the query fails).
+// Compute units of the current device (cached per device, safe across host threads; 0 if
+// the query fails).
 int compute_units()
 {
-    static int cus[64];
+    static std::atomic<int> cus[64];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-    if (cus[dev] == 0) {
-        int n = 0;
+    int n = cus[dev].load(std::memory_order_relaxed);
+    if (n == 0) {
         if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-        cus[dev] = n;
+        cus[dev].store(n, std::memory_order_relaxed);
     }
-    return cus[dev];
+    return n;
 }
 
 // 256-token chunks per workgroup; 0 when the configuration asks for the second kernel's
