@@ -86,8 +86,9 @@ def parse():
                     help="decode attention over a paged KV cache instead of the MoE layer: one JSON line per "
                          "workload of attn_workload.ATTN_CONFIGS")
     ap.add_argument("--attn-merge-max-splits", type=int, default=0,
-                    help="with --attn: contexts of at most this many 256-token splits are merged inside the split "
-                         "kernel (0: library default, -1: always by a second kernel)")
+                    help="with --attn: at most this many splits per sequence, each walking one or more 256-token "
+                         "pieces and merged inside the split kernel (0: library default 16, -1: one piece per split, "
+                         "merged by a second kernel)")
     ap.add_argument("--stack", action="store_true",
                     help="also time the stack of 12 distinct 480B-shaped layers decoded back to back, T = 1..256")
     ap.add_argument("--stack-steps", type=int, default=20)
