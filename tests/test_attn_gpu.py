@@ -168,12 +168,20 @@ def test_long_context_sampled(dev):
     """32K-token contexts (128 pieces per sequence), checked on three sampled sequences:
     8 splits of 16 pieces merged in the split kernel (the default on 256 compute units:
     at most three workgroups per unit), and 128 one-piece splits merged by the second
-    kernel."""
+    kernel; a call with fewer sequences on the same workspace repeats their rows bitwise."""
     cfg = A.ATTN_BY_NAME["qwen3-235b-a22b-attn-long32k"]
     h = A.host_attn(cfg, draw=2)
     scale = 1 / np.sqrt(128)
     rows = [0, 11, cfg.batch - 1]
     ref = oracle.attn_decode(h.q[rows], h.k_cache, h.v_cache, h.block_table[rows], h.ctx[rows], scale)
     for fused in (0, -1):
-        out, _, _ = run_gpu(cfg, h, dev, scale, fused=fused)
+        out, m, d = run_gpu(cfg, h, dev, scale, fused=fused)
         check(bf16_to_f64(out), ref, rows=rows, label=f"{cfg.name} fused_merge_max_splits={fused}")
+        if fused == 0:
+            # the split count follows the configuration, not the call: a call with the first
+            # 12 sequences on the same workspace gives their rows bit for bit
+            nb = 12
+            out2 = torch.full_like(out, 0x7FC1)
+            m.forward(d["q"], d["k_cache"], d["v_cache"], h.n_pages, d["block_table"], d["ctx"], nb, scale, out2)
+            torch.cuda.synchronize(dev)
+            assert torch.equal(out2[:nb], out[:nb]) and torch.all(out2[nb:] == 0x7FC1)
