@@ -2,9 +2,11 @@
 
 A step is one decode step of one MoE layer (router, top-k, grouping, grouped
 experts, combine) over one batch of T synthetic tokens, with all inputs resident in
-HBM.  The default workload is the Qwen3-235B-A22B-shaped layer (hidden 4096, 128
-experts, top-8, SwiGLU intermediate 1536, FP8-E4M3 weights with 128x128 fp32 block
-scales, bf16 activations) at T = 64, the largest decode batch of its sweep.
+HBM.  The headline workload is the Qwen3-Coder-480B-A35B-shaped layer (hidden 6144,
+160 experts, top-8, SwiGLU intermediate 2560, FP8-E4M3 weights with 128x128 fp32
+block scales, bf16 activations, router bias N(0, 0.5)) at T = 64, the largest batch
+of its sweep at or below 64 tokens; the Qwen3-235B-A22B-shaped layer (hidden 4096,
+128 experts, top-8, I 1536) is swept in the same run and reported beside it.
 
 Cold-cache protocol: steps cycle over L copies of the layer's expert weights at
 distinct HBM addresses and over a pool of 16 token batches, so consecutive steps
@@ -22,6 +24,7 @@ bounded sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import glob
 import hashlib
 import json
 import math
@@ -75,7 +78,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", default="qwen3-235b-a22b")
+    ap.add_argument("--config", default="qwen3-coder-480b-a35b", help="layer of the headline line")
+    ap.add_argument("--also", default="qwen3-235b-a22b",
+                    help="comma-separated further layer configurations swept in the same run and reported under "
+                         "other_layers ('' for none)")
     ap.add_argument("--tokens", type=int, default=None, help="T of the headline line (default: largest T <= 64)")
     ap.add_argument("--copies", type=int, default=0, help="weight copies cycled (0: enough for 8 GB)")
     ap.add_argument("--no-sweep", action="store_true")
@@ -97,6 +103,8 @@ def parse():
                          "moe_decode_pack_weights) or row-major")
     ap.add_argument("--screen-min-tokens", type=int, default=0,
                     help="tokens per step from which routing screens the logits (0: library default, -1: never)")
+    ap.add_argument("--power-cap-probe", action="store_true",
+                    help="read the board power cap, its range, the clocks and who may write the cap, then exit")
     ap.add_argument("--mstar", type=int, default=0,
                     help="tokens per expert from which MFMA tiles are used (0: library default, -1: GEMV only)")
     return ap.parse_args()
@@ -134,6 +142,51 @@ class PowerSampler:
             except Exception:  # noqa: BLE001
                 pass
             stop.wait(0.1)
+
+
+def power_cap_probe():
+    """The board power cap as this process sees it, read only: amdsmi's cap and
+    range, the GPU and memory clocks, and the driver's sysfs cap files with their
+    owner, mode and whether this user may write them.  A cap sweep needs a writable
+    cap; the job pool these runs use allows no power-cap or clock setting at all."""
+    rec = dict(euid=os.geteuid())
+    try:
+        import amdsmi
+
+        amdsmi.amdsmi_init()
+        h = amdsmi.amdsmi_get_processor_handles()[0]
+    except Exception as e:  # noqa: BLE001
+        rec["error"] = "amdsmi unavailable: " + repr(e)
+        return rec
+
+    def clocks():
+        out = {}
+        for name in ("GFX", "MEM"):
+            try:
+                out[name.lower()] = amdsmi.amdsmi_get_clock_info(h, getattr(amdsmi.AmdSmiClkType, name))
+            except Exception as e:  # noqa: BLE001
+                out[name.lower()] = repr(e)
+        return out
+
+    try:
+        rec["cap_uW"] = amdsmi.amdsmi_get_power_cap_info(h, 0)
+    except Exception as e:  # noqa: BLE001
+        rec["cap_uW"] = repr(e)
+    rec["clocks"] = clocks()
+    files = []
+    for p in sorted(glob.glob("/sys/class/drm/card*/device/hwmon/hwmon*/power1_cap")):
+        try:
+            st = os.stat(p)
+            files.append(dict(path=p, mode=oct(st.st_mode & 0o777), uid=st.st_uid,
+                              writable_by_this_user=os.access(p, os.W_OK)))
+        except OSError as e:
+            files.append(dict(path=p, error=repr(e)))
+    rec["sysfs_power_cap_files"] = files
+    try:
+        amdsmi.amdsmi_shut_down()
+    except Exception:  # noqa: BLE001
+        pass
+    return rec
 
 
 def settle_hbm(dev, reserve_bytes=int(32e9), wait_s=3.0):
@@ -289,49 +342,48 @@ def run_attn(args, dev):
         torch.cuda.empty_cache()
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU; multi-GPU sharding is a design note only",
-                          "n_gpus": args.gpus}))
-        sys.exit(2)
+def cpu_info():
+    """Host cores the oracle may use: the affinity mask, the CPU share of this host's
+    GPU jobs (OMP_NUM_THREADS where the job scheduler sets it) and the CPU model."""
+    affinity = len(os.sched_getaffinity(0))
+    share = os.environ.get("OMP_NUM_THREADS")
+    share = int(share) if share and share.isdigit() and int(share) > 0 else None
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return affinity, share, model
 
-    import numpy as np
+
+def bench_layer(args, dev, cfg, sweep_T, T_main, pool=16):
+    """Time one layer configuration over its T sweep: tokens/s from an event-free
+    region of K steps (plus five repetitions), per-kernel durations from a second
+    region with the library's stage events, and board power over a steady loop at
+    every T.  Returns (results by T, layout, copies, setup seconds, host layer)."""
     import torch
 
     from paper_2609_11133_amd import binding as B
-    from paper_2609_11133_amd import configs as C
     from paper_2609_11133_amd import workload as W
 
-    if not os.path.exists(B.LIB_PATH):
-        import __graft_entry__
-
-        __graft_entry__.build()
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    dev = torch.device("cuda:0")
-    settle_hbm(dev)
-    if args.attn:
-        run_attn(args, dev)
-        return
-    cfg = C.BY_NAME[args.config]
-    small = [t for t in cfg.tokens if t <= 64]
-    T_main = args.tokens or (max(small) if small else min(cfg.tokens))
-    sweep_T = sorted(set(cfg.tokens) | {T_main}) if not args.no_sweep else [T_main]
     Tmax = max(sweep_T)
     layer_bytes = cfg.n_experts * (cfg.expert_weight_bytes() + cfg.expert_scale_bytes())
     copies = args.copies or max(2, math.ceil(8e9 / layer_bytes))
 
     t0 = time.time()
     hl = W.host_layer(cfg)
-    pool = 16
     xs = {T: [W.to_device(W.host_x(cfg, T, batch=b), dev) for b in range(pool)] for T in sweep_T}
     rw, bias = W.to_device(hl.router_w, dev), W.to_device(hl.bias, dev)
     ew0, sc0 = W.to_device(hl.expert_w, dev), W.to_device(hl.scales, dev)
     layout = 0 if args.layout == "row-major" else 1
     bcfg = W.binding_config(cfg, Tmax, args.mstar, args.screen_min_tokens, layout)
-    if layout:  # weights (and NVFP4 scales) converted once, as at load time
+    if layout:  # weights (and E2M1 scales) converted once, as at load time
         packed = torch.empty_like(ew0)
-        nv = cfg.wfmt != "fp8"  # E2M1 weights: scales packed too
+        nv = cfg.wfmt != "fp8"
         psc = torch.empty_like(sc0) if nv else None
         B.moe_decode_pack_weights(bcfg, torch.cuda.current_stream(dev).cuda_stream, ew0, packed, cfg.n_experts,
                                   sc0 if nv else None, psc)
@@ -414,14 +466,13 @@ def main():
             experts_frac=exp_gbs / PEAK_HBM_GBS,
             w13_bytes_per_launch=w13_bytes,
         )
-        print(f"[bench] T={T}: {results[T]['tokens_per_s']:.0f} tok/s, {ms * 1e3:.1f} us/step "
+        print(f"[bench] {cfg.name} T={T}: {results[T]['tokens_per_s']:.0f} tok/s, {ms * 1e3:.1f} us/step "
               f"(5 reps: median {statistics.median(reps) * 1e3:.1f} +- {statistics.stdev(reps) * 1e3:.1f}), layer "
               f"{results[T]['layer_GBs']:.0f} GB/s, experts {exp_gbs:.0f} GB/s, stages(us) "
               + " ".join(f"{n}={v * 1e3:.1f}" for n, v in zip(B.STAGE_NAMES, st_ms)), file=sys.stderr, flush=True)
 
     # board power over a steady loop at each batch size (4 s at the headline one), and
     # over 2 s of an idle device (after 3 s of rest) for context
-    power = None
     if not args.no_power:
         ps = PowerSampler()
         if ps.ok:
@@ -457,31 +508,88 @@ def main():
 
             torch.cuda.synchronize(dev)
             time.sleep(3.0)  # the board sensor averages over about a second
-            idle_W, idle_n, _, _ = sample(2.0, lambda: (time.sleep(0.05), 0)[1])
+            idle_W, _, _, _ = sample(2.0, lambda: (time.sleep(0.05), 0)[1])
             for T in sweep_T:
                 pw, ns, n, dt = sample(4.0 if T == T_main else 3.0, loop_at(T))
                 if pw:
-                    results[T]["power"] = dict(board_W=pw, samples=ns, tokens_per_J=(n * T / dt) / pw)
-                    print(f"[power] T={T}: {pw:.0f} W board (idle {idle_W or 0:.0f} W), "
+                    results[T]["power"] = dict(board_W=pw, samples=ns, tokens_per_J=(n * T / dt) / pw,
+                                               idle_board_W=idle_W)
+                    print(f"[power] {cfg.name} T={T}: {pw:.0f} W board (idle {idle_W or 0:.0f} W), "
                           f"{results[T]['power']['tokens_per_J']:.1f} tokens/J", file=sys.stderr, flush=True)
-            if results[T_main].get("power"):
-                power = dict(results[T_main]["power"], idle_board_W=idle_W)
-        if power is None:
-            power = dict(board_W=None, note="amdsmi power unreadable: " + getattr(ps, "err", "no samples"))
+        else:
+            for T in sweep_T:
+                results[T]["power"] = dict(board_W=None, note="amdsmi power unreadable: " + getattr(ps, "err", "?"))
+    m.close()
+    del ews, scs, xs, ew0, sc0
+    torch.cuda.empty_cache()
+    return results, layout, copies, setup_s, hl
+
+
+def sweep_json(results):
+    return {str(T): {k: (v if not isinstance(v, float) else round(v, 4)) for k, v in r.items()}
+            for T, r in results.items()}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU: the layer is measured at one GPU's share "
+                                   "(the TP4 shard configuration), and sharding across GPUs is a design note only",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_11133_amd import binding as B
+    from paper_2609_11133_amd import configs as C
+    from paper_2609_11133_amd import workload as W
+
+    if not os.path.exists(B.LIB_PATH):
+        import __graft_entry__
+
+        __graft_entry__.build()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    settle_hbm(dev)
+    if args.attn:
+        run_attn(args, dev)
+        return
+    if args.power_cap_probe:
+        print(json.dumps(power_cap_probe()), flush=True)
+        return
+    cfg = C.BY_NAME[args.config]
+    small = [t for t in cfg.tokens if t <= 64]
+    T_main = args.tokens or (max(small) if small else min(cfg.tokens))
+    sweep_T = sorted(set(cfg.tokens) | {T_main}) if not args.no_sweep else [T_main]
+    results, layout, copies, setup_s, hl = bench_layer(args, dev, cfg, sweep_T, T_main)
+
+    # further layer configurations, timed the same way and reported beside the headline
+    others = {}
+    for name in [n for n in (args.also or "").split(",") if n and n != cfg.name]:
+        ocfg = C.BY_NAME[name]
+        ores, _, ocopies, osetup, _ = bench_layer(args, dev, ocfg, sorted(ocfg.tokens), max(ocfg.tokens))
+        others[name] = dict(
+            workload=f"{ocfg.name} MoE decode layer: hidden {ocfg.hidden}, {ocfg.n_experts} experts, "
+                     f"top-{ocfg.topk}, SwiGLU intermediate {ocfg.inter}, {ocfg.wfmt} weights, {ocfg.act} activations",
+            cold_cache=f"{ocopies} weight copies x 16 token batches cycled", setup_s=round(osetup, 1),
+            sweep=sweep_json(ores))
 
     # the fp64 oracle on this host's cores, on a bounded sample of the headline batch
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
 
-        threads = len(os.sched_getaffinity(0))
-        threads = max(1, min(threads, 16))
+        affinity, share, model = cpu_info()
+        threads = min(affinity, share) if share else affinity
         x_host = W.host_x(cfg, T_main, batch=0)
         tp = time.perf_counter()
         oracle.forward(x_host, hl.router_w, hl.bias, hl.expert_w, hl.scales, cfg.topk, cfg.inter, cfg.wfmt_id,
                        tokens=[0], threads=threads)
         t1 = time.perf_counter() - tp
-        n_tok = max(1, min(T_main, int(args.cpu_seconds / max(t1, 1e-3))))
+        # one token keeps at most k threads busy: with more threads and tokens a token
+        # costs about t1 * min(threads, k) / threads of wall time
+        per_tok = max(t1 * min(threads, cfg.topk) / threads, 1e-3)
+        n_tok = max(1, min(T_main, int(args.cpu_seconds / per_tok)))
         tokens = list(range(n_tok))
         tp = time.perf_counter()
         oracle.forward(x_host, hl.router_w, hl.bias, hl.expert_w, hl.scales, cfg.topk, cfg.inter, cfg.wfmt_id,
@@ -490,16 +598,19 @@ def main():
         cpu = dict(value=n_tok / dt, unit="tokens/s", cores=threads, kind="oracle",
                    sample=f"first {n_tok} of the {T_main} tokens of batch 0: full layer in fp64 (exact router "
                           f"logits, top-{cfg.topk}, {cfg.topk} dequantised experts per token, combine); "
-                          f"{dt:.1f} s wall")
+                          f"{dt:.1f} s wall",
+                   affinity_cpus=affinity, cpu_share=share, cpu_model=model,
+                   threads_rule="the affinity mask's CPUs, capped at this host's per-GPU CPU share "
+                                "(OMP_NUM_THREADS) where it is set")
+        print(f"[cpu] oracle {n_tok} tokens in {dt:.1f} s on {threads} threads (affinity {affinity}, share {share}, "
+              f"{model})", file=sys.stderr, flush=True)
 
     R = results[T_main]
     traffic, traffic_src = w13_traffic(cfg, T_main)
     stack = None
     if args.stack:
-        m.close()
-        del ews, scs, xs
-        torch.cuda.empty_cache()
         stack = run_stack(args, dev)
+    power = R.get("power")
     line = {
         "metric": METRIC,
         "value": R["tokens_per_s"],
@@ -515,8 +626,8 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": f"{cfg.name} MoE decode layer: hidden {cfg.hidden}, {cfg.n_experts} experts, top-{cfg.topk}, "
-                        f"SwiGLU intermediate {cfg.inter}, {cfg.wfmt} weights, {cfg.act} activations, "
-                        f"T={T_main} tokens per step",
+                        f"SwiGLU intermediate {cfg.inter}, {cfg.wfmt} weights, {cfg.act} activations"
+                        + (f", router bias {cfg.bias}" if cfg.bias else "") + f", T={T_main} tokens per step",
             "tokens_per_step": T_main,
             "weights": {"fp8": "fp8-e4m3, fp32 scale per 128x128 block", "mxfp4": "mxfp4 (e2m1 + e8m0/32)",
                         "nvfp4": "nvfp4 (e2m1 + e4m3/16 + fp32/matrix)"}[cfg.wfmt]
@@ -547,8 +658,8 @@ def main():
             "avg_launch_us": R["stage_ms"]["w13"] * 1e3,
             "bytes_per_launch": R["w13_bytes_per_launch"],
         },
-        "sweep": {str(T): {k: (v if not isinstance(v, float) else round(v, 4)) for k, v in r.items()}
-                  for T, r in results.items()},
+        "sweep": sweep_json(results),
+        "other_layers": others or None,
         "power": power,
         "cpu_baseline": cpu,
         "stack": stack,

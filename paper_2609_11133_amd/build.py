@@ -48,12 +48,14 @@ def build(force: bool = True) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
     os.replace(tmp, LIB)
-    build_probe()
     return LIB
 
 
 def build_probe() -> str:
-    """The HBM streaming reference executable (roofline ceiling and PMC scaling)."""
+    """The HBM streaming reference executable: measurement tooling, not part of the
+    library.  Its runs give the streaming ceilings and the copy-kernel scale of the
+    FETCH_SIZE / WRITE_SIZE counters that the traffic profiles are normalised by;
+    built on request only (``python -m paper_2609_11133_amd.build --probe``)."""
     tmp = PROBE + ".tmp"
     r = subprocess.run([HIPCC, *FLAGS, os.path.join(CSRC, "stream_probe.hip"), "-o", tmp], capture_output=True,
                        text=True)
@@ -64,4 +66,6 @@ def build_probe() -> str:
 
 
 if __name__ == "__main__":
-    print(build())
+    import sys
+
+    print(build_probe() if "--probe" in sys.argv[1:] else build())

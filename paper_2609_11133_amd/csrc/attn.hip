@@ -60,7 +60,9 @@ template <typename T>
 __device__ inline void st_dev(T *p, T v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
 template <typename T>
 __device__ inline T ld_dev(const T *p) { return __hip_atomic_load(const_cast<T *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
-__device__ inline void wait_stores() { __builtin_amdgcn_s_waitcnt(0); }
+// The memory clobber keeps the compiler from moving memory accesses across the wait,
+// so every store issued before it has completed when the counter is bumped.
+__device__ inline void wait_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 __device__ inline uint16_t to_bf16(float y)
 {
