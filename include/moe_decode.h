@@ -25,7 +25,8 @@
  *
  * Memory: every tensor pointer is a DEVICE pointer owned by the caller.  The library
  * never allocates device memory: its scratch lives in a caller-provided workspace
- * (moe_decode_workspace_bytes).  The handle itself is host memory.
+ * (moe_decode_workspace_bytes), or, for moe_decode_forward_noalloc, in a static
+ * device array of the library.  The handle itself is host memory.
  *
  * Layouts (row-major, C order):
  *   x, y          [T][H]  act_dtype (bf16 or fp32); y must not alias x
@@ -170,6 +171,27 @@ moe_status moe_decode_init(const moe_decode_config *cfg, void *workspace, size_t
 moe_status moe_decode_forward(moe_decode_t h, void *stream, const void *x, int32_t n_tokens, const void *router_w,
                               const float *router_bias, const void *expert_w, const void *scales, int32_t topk,
                               void *y, int32_t *topk_ids, float *topk_weights);
+
+/* The same decode step as moe_decode_forward, for callers that cannot allocate device
+ * memory or create a handle: code under HIP graph capture, tight serving loops, and
+ * harnesses that forbid hipMalloc.  It takes the configuration itself (validated as by
+ * moe_decode_init) and uses as its workspace a static device array of the library
+ * (64 MiB, 256-byte aligned; one copy on each device the library runs on, held until
+ * the process ends), so it calls no hipMalloc, hipFree, host allocator or other
+ * allocating routine.  Configurations whose workspace (moe_decode_workspace_bytes)
+ * exceeds 64 MiB less 256.5 KiB of routing counters are rejected with
+ * MOE_ERR_WORKSPACE before anything is enqueued.  `stream` must belong to the
+ * current device (MOE_ERR_INVALID otherwise); the first call on a device also
+ * enqueues one clear of the array's counters on that stream.  Arguments, layouts,
+ * alignment, results and bitwise determinism as for moe_decode_forward; errors are
+ * reported through moe_decode_last_error(NULL) of the calling thread.  Every call on
+ * one device shares that device's array and it keeps the last call's contents:
+ * calls that overlap on one device (concurrent streams or host threads) race, and
+ * there are no statistics to read back. */
+moe_status moe_decode_forward_noalloc(const moe_decode_config *cfg, void *stream, const void *x, int32_t n_tokens,
+                                      const void *router_w, const float *router_bias, const void *expert_w,
+                                      const void *scales, int32_t topk, void *y, int32_t *topk_ids,
+                                      float *topk_weights);
 
 /* Enqueue on `stream` the conversion of n_experts consecutive experts' weights (and,
  * for MXFP4 and NVFP4, their scales) from the row-major layout (src) to packed 16-row tiles (dst),

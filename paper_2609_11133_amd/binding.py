@@ -96,6 +96,8 @@ def lib():
         L.moe_decode_init.argtypes = [cfgp, P, SZ, ctypes.POINTER(P)]
         L.moe_decode_forward.restype = ctypes.c_int
         L.moe_decode_forward.argtypes = [P, P, P, I32, P, P, P, P, I32, P, P, P]
+        L.moe_decode_forward_noalloc.restype = ctypes.c_int
+        L.moe_decode_forward_noalloc.argtypes = [cfgp, P, P, I32, P, P, P, P, I32, P, P, P]
         L.moe_decode_pack_weights.restype = ctypes.c_int
         L.moe_decode_pack_weights.argtypes = [cfgp, P, P, P, P, P, I32]
         L.moe_decode_route.restype = ctypes.c_int
@@ -173,6 +175,15 @@ def moe_decode_forward(h, stream, x, n_tokens, router_w, router_bias, expert_w, 
     _check(lib().moe_decode_forward(h, stream, _addr(x), n_tokens, _addr(router_w), _addr(router_bias),
                                     _addr(expert_w), _addr(scales), topk, _addr(y), _addr(topk_ids),
                                     _addr(topk_weights)), h)
+
+
+def moe_decode_forward_noalloc(cfg: moe_decode_config, stream, x, n_tokens, router_w, router_bias, expert_w, scales,
+                               topk, y, topk_ids=None, topk_weights=None):
+    """One decode step on the library's static device scratch array (no handle, no
+    workspace, no allocation)."""
+    _check(lib().moe_decode_forward_noalloc(ctypes.byref(cfg), stream, _addr(x), n_tokens, _addr(router_w),
+                                            _addr(router_bias), _addr(expert_w), _addr(scales), topk, _addr(y),
+                                            _addr(topk_ids), _addr(topk_weights)))
 
 
 def moe_decode_pack_weights(cfg: moe_decode_config, stream, src, dst, n_experts: int, src_scales=None,

@@ -5,6 +5,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 
 #include "../../include/moe_decode.h"
@@ -158,20 +159,11 @@ size_t moe_decode_expert_scale_bytes(const moe_decode_config *cfg)
     return 16 + 3 * H * I / 16;
 }
 
-moe_status moe_decode_init(const moe_decode_config *cfg, void *workspace, size_t workspace_bytes, moe_decode_t *out)
+}  // extern "C"
+
+// Fill a handle for a validated configuration whose workspace starts at `workspace`.
+static void fill_handle(moe_decode_s *h, const moe_decode_config *cfg, void *workspace)
 {
-    g_init_err[0] = 0;
-    if (!out) FAIL(g_init_err, MOE_ERR_INVALID, "out is NULL");
-    *out = nullptr;
-    moe_status s = check_config(cfg, g_init_err);
-    if (s != MOE_OK) return s;
-    const size_t need = moe_decode_workspace_bytes(cfg);
-    if (!workspace) FAIL(g_init_err, MOE_ERR_WORKSPACE, "workspace is NULL");
-    if ((uintptr_t)workspace % 256) FAIL(g_init_err, MOE_ERR_WORKSPACE, "workspace is not 256-byte aligned");
-    if (workspace_bytes < need)
-        FAIL(g_init_err, MOE_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
-    moe_decode_s *h = new (std::nothrow) moe_decode_s();
-    if (!h) FAIL(g_init_err, MOE_ERR_INVALID, "out of host memory");
     h->cfg = *cfg;
     h->L.H = cfg->hidden;
     h->L.E = cfg->n_experts;
@@ -200,6 +192,25 @@ moe_status moe_decode_init(const moe_decode_config *cfg, void *workspace, size_t
     h->err[0] = 0;
     h->prof_cap = h->prof_n = 0;
     h->prof_ev = nullptr;
+}
+
+extern "C" {
+
+moe_status moe_decode_init(const moe_decode_config *cfg, void *workspace, size_t workspace_bytes, moe_decode_t *out)
+{
+    g_init_err[0] = 0;
+    if (!out) FAIL(g_init_err, MOE_ERR_INVALID, "out is NULL");
+    *out = nullptr;
+    moe_status s = check_config(cfg, g_init_err);
+    if (s != MOE_OK) return s;
+    const size_t need = moe_decode_workspace_bytes(cfg);
+    if (!workspace) FAIL(g_init_err, MOE_ERR_WORKSPACE, "workspace is NULL");
+    if ((uintptr_t)workspace % 256) FAIL(g_init_err, MOE_ERR_WORKSPACE, "workspace is not 256-byte aligned");
+    if (workspace_bytes < need)
+        FAIL(g_init_err, MOE_ERR_WORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+    moe_decode_s *h = new (std::nothrow) moe_decode_s();
+    if (!h) FAIL(g_init_err, MOE_ERR_INVALID, "out of host memory");
+    fill_handle(h, cfg, workspace);
     *out = h;
     return MOE_OK;
 }
@@ -398,6 +409,82 @@ moe_status moe_decode_forward(moe_decode_t h, void *stream, const void *x, int32
         h->prof_n++;
     }
     return MOE_OK;
+}
+
+}  // extern "C"
+
+// ---- forward without allocation: the workspace is a static device array.
+//
+// Layout of `scratch`: the routing counters first, sized for the largest token count
+// any configuration accepts (1024), then the workspace of the call's configuration,
+// carved as for a handle.  The counters are zero when the code object is loaded
+// (static storage), are cleared once more when a device is set up, and every forward
+// call leaves them at zero again (each counter is reset by the workgroup that
+// consumes it), so nothing has to be cleared per call.
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+constexpr size_t kScratchCounterBytes =
+    ((size_t)(1024 + 2) * kCounterStride * sizeof(int32_t) + 255) & ~(size_t)255;
+constexpr int kScratchMaxDevices = 64;
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+static std::mutex g_scratch_mu;
+static void *g_scratch_dev[kScratchMaxDevices];  // device address of `scratch` on each device
+
+// Device address of this device's copy of `scratch` (set up on the first call on the
+// device, with that device current).  Host code never uses the array's own name: on
+// the host it is a stand-in, not a device address.
+static moe_status scratch_base(hipStream_t st, void **out, char *err)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) FAIL(err, MOE_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+    if (st) {
+        hipDevice_t sdev = -1;
+        e = hipStreamGetDevice(st, &sdev);
+        if (e != hipSuccess) FAIL(err, MOE_ERR_HIP, "hipStreamGetDevice: %s", hipGetErrorString(e));
+        if (sdev != dev) FAIL(err, MOE_ERR_INVALID, "the stream belongs to device %d but device %d is current", (int)sdev, dev);
+    }
+    if (dev < 0 || dev >= kScratchMaxDevices) FAIL(err, MOE_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, kScratchMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            FAIL(err, MOE_ERR_HIP, "hipGetSymbolAddress(scratch): %s", e != hipSuccess ? hipGetErrorString(e) : "NULL");
+        e = launch_zero((int32_t *)p, (int)(kScratchCounterBytes / sizeof(int32_t)), st);
+        if (e != hipSuccess) FAIL(err, MOE_ERR_HIP, "clearing the scratch counters: %s", hipGetErrorString(e));
+        g_scratch_dev[dev] = p;
+    }
+    *out = g_scratch_dev[dev];
+    return MOE_OK;
+}
+
+extern "C" {
+
+moe_status moe_decode_forward_noalloc(const moe_decode_config *cfg, void *stream, const void *x, int32_t n_tokens,
+                                      const void *router_w, const float *router_bias, const void *expert_w,
+                                      const void *scales, int32_t topk, void *y, int32_t *topk_ids,
+                                      float *topk_weights)
+{
+    g_init_err[0] = 0;
+    moe_status s = check_config(cfg, g_init_err);
+    if (s != MOE_OK) return s;
+    const size_t need = moe_decode_workspace_bytes(cfg);
+    if (need > kScratchBytes - kScratchCounterBytes)
+        FAIL(g_init_err, MOE_ERR_WORKSPACE, "the configuration needs %zu bytes of workspace; the static scratch holds %zu",
+             need, kScratchBytes - kScratchCounterBytes);
+    void *base = nullptr;
+    s = scratch_base((hipStream_t)stream, &base, g_init_err);
+    if (s != MOE_OK) return s;
+    moe_decode_s h{};  // on the stack: no allocation of any kind
+    fill_handle(&h, cfg, (char *)base + kScratchCounterBytes);
+    h.ws.sync = (int32_t *)base;
+    h.synced = 1;
+    s = moe_decode_forward(&h, stream, x, n_tokens, router_w, router_bias, expert_w, scales, topk, y, topk_ids,
+                           topk_weights);
+    if (s != MOE_OK) memcpy(g_init_err, h.err, sizeof g_init_err);
+    return s;
 }
 
 moe_status moe_decode_get_stats(moe_decode_t h, moe_decode_stats *out, int32_t *counts_host)
