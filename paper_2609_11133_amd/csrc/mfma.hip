@@ -197,7 +197,11 @@ __device__ inline i32x8 wfrag(const uint8_t *a, int kb, int g)
             const u32x4v y = __builtin_amdgcn_raw_buffer_load_b128(r, v + 1024, kb * 2048, kNonTemporal);
             return (i32x8){(int)x.x, (int)x.y, (int)x.z, (int)x.w, (int)y.x, (int)y.y, (int)y.z, (int)y.w};
         } else {
-            const u32x4v x = __builtin_amdgcn_raw_buffer_load_b128(r, v, kb * 1024, kNonTemporal);
+            // ordinary loads for E2M1 tiles: an expert with several token chunks re-reads
+            // its tiles, and the non-temporal policy made those re-reads miss the caches
+            // (4-bit MXFP4 layer at 256 tokens per step: 1.31x its algorithmic bytes
+            // fetched, 997k against 1,036k tokens/s with ordinary loads)
+            const u32x4v x = __builtin_amdgcn_raw_buffer_load_b128(r, v, kb * 1024, 0);
             return (i32x8){(int)x.x, (int)x.y, (int)x.z, (int)x.w, 0, 0, 0, 0};
         }
     } else {
@@ -529,10 +533,12 @@ struct alignas(16) ActSeg {
     uint8_t sink[kSegK * 4];                // target of the threads that stage no exponents
 };
 
-// Piece c (16 bytes) of token t's row is stored at piece swz(c, t): the piece index
-// within a 128-byte K block is XORed with the token, spreading a fragment read of 16
-// tokens over the LDS banks.
-__device__ inline int swz(int c, int t) { return (c & ~7) | ((c ^ t) & 7); }
+// Piece c (16 bytes) of token t's 512-byte segment row is stored at piece swz(c, t):
+// the low four bits of the piece index are XORed with the token, so the 16 tokens of a
+// fragment read (one 16-lane group) fall on 16 distinct 16-byte bank groups of the
+// 64-bank LDS.  A three-bit XOR left pairs of tokens on one bank group: the counters
+// showed bank-conflict stalls in about 40 % of the LDS's active cycles.
+__device__ inline int swz(int c, int t) { return (c & ~15) | ((c ^ t) & 15); }
 
 __device__ inline void sync_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
@@ -590,39 +596,51 @@ struct Stager {
     }
 };
 
-// Streams this wave's weight tile (this lane's row `arow`) over KB K blocks (KB a
-// multiple of 4) against NT staged token tiles; acc[j] as in stream_tiles.  All W
-// waves of the workgroup call it together: it synchronises them once per staged
-// segment (four K blocks).  On return no wave reads `seg` any more.
-template <int FMT, int NT, int W, bool PK>
-__device__ inline void stream_tile_lds(f32x4 (&acc)[NT], const uint8_t *__restrict__ arow,
-                                       const uint8_t *__restrict__ erow, const float *__restrict__ sblk, int KB,
+// Streams this wave's NA weight tiles (this lane's rows arow[a]) over KB K blocks (KB a
+// multiple of 4) against NT staged token tiles; acc[a][j] as in stream_tiles.  Each
+// activation fragment read from LDS feeds the NA tiles' MFMAs.  All W waves of the
+// workgroup call it together: it synchronises them once per staged segment (four K
+// blocks).  On return no wave reads `seg` any more.
+template <int FMT, int NT, int W, int NA, bool PK>
+__device__ inline void stream_tile_lds(f32x4 (&acc)[NA][NT], const uint8_t *const (&arow)[NA],
+                                       const uint8_t *const (&erow)[NA], const float *const (&sblk)[NA], int KB,
                                        const ActRsrc &B, Stager<NT, W> &st, ActSeg (&seg)[2], int lane, int tid)
 {
     const int r = lane & 15, g = lane >> 4;
     const int nseg = KB / kSegK;
-    i32x8 A[4];
-    int EA[4];
-    // packed E8M0 scales: one word per lane and segment of four blocks, a segment ahead
-    __amdgpu_buffer_rsrc_t er;
-    if constexpr (PK && FMT == 1) er = tile_rsrc(erow);
-    auto eword = [&](int sg) -> uint32_t {
-        if constexpr (PK && FMT == 1)
-            return __builtin_amdgcn_raw_buffer_load_b32(er, 4u * lane, sg * 256, 0);
-        else
-            return 0u;
+    i32x8 A[4][NA];
+    int EA[4][NA];
+    // packed E8M0 scales: one word per lane, tile and segment of four blocks, a segment ahead
+    __amdgpu_buffer_rsrc_t er[NA];
+    if constexpr (PK && FMT == 1) {
+#pragma unroll
+        for (int a = 0; a < NA; ++a) er[a] = tile_rsrc(erow[a]);
+    }
+    auto eword = [&](uint32_t (&w)[NA], int sg) {
+#pragma unroll
+        for (int a = 0; a < NA; ++a) {
+            if constexpr (PK && FMT == 1)
+                w[a] = __builtin_amdgcn_raw_buffer_load_b32(er[a], 4u * lane, sg * 256, 0);
+            else
+                w[a] = 0u;
+        }
     };
-    auto loadA = [&](int slot, int kb, uint32_t word) {  // word: the E8M0 word holding block kb
-        A[slot] = wfrag<FMT, PK>(arow, kb, g);
-        if constexpr (FMT == 0)
-            EA[slot] = 127;
-        else if constexpr (PK)
-            EA[slot] = (int)__builtin_amdgcn_ubfe(word, 8 * (kb & 3), 8);
-        else
-            EA[slot] = erow[kb * 4 + g];
+    auto loadA = [&](int slot, int kb, const uint32_t (&word)[NA]) {  // word: the E8M0 words holding block kb
+#pragma unroll
+        for (int a = 0; a < NA; ++a) {
+            A[slot][a] = wfrag<FMT, PK>(arow[a], kb, g);
+            if constexpr (FMT == 0)
+                EA[slot][a] = 127;
+            else if constexpr (PK)
+                EA[slot][a] = (int)__builtin_amdgcn_ubfe(word[a], 8 * (kb & 3), 8);
+            else
+                EA[slot][a] = erow[a][kb * 4 + g];
+        }
     };
     auto compute = [&](int slot, const ActSeg &S, int kk, int kb) {
-        const float s = FMT == 0 ? sblk[kb] : 1.f;
+        float sc[NA];
+#pragma unroll
+        for (int a = 0; a < NA; ++a) sc[a] = FMT == 0 ? sblk[a][kb] : 1.f;
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
             const int t = 16 * j + r;
@@ -632,12 +650,17 @@ __device__ inline void stream_tile_lds(f32x4 (&acc)[NT], const uint8_t *__restri
             const u32x4v l1 = *reinterpret_cast<const u32x4v *>(&S.code[1][t][swz(kk * 8 + 4 + g, t) * 16]);
             const i32x8 bh = {(int)h0.x, (int)h0.y, (int)h0.z, (int)h0.w, (int)h1.x, (int)h1.y, (int)h1.z, (int)h1.w};
             const i32x8 bl = {(int)l0.x, (int)l0.y, (int)l0.z, (int)l0.w, (int)l1.x, (int)l1.y, (int)l1.z, (int)l1.w};
-            mma2<FMT>(acc[j], A[slot], EA[slot], s, bh, S.ex[0][t][kk * 4 + g], bl, S.ex[1][t][kk * 4 + g]);
+            const int eh = S.ex[0][t][kk * 4 + g], el = S.ex[1][t][kk * 4 + g];
+#pragma unroll
+            for (int a = 0; a < NA; ++a) mma2<FMT>(acc[a][j], A[slot][a], EA[slot][a], sc[a], bh, eh, bl, el);
         }
     };
 #pragma unroll
-    for (int j = 0; j < NT; ++j) acc[j] = (f32x4){0.f, 0.f, 0.f, 0.f};
-    uint32_t wc = eword(0);  // word of the segment being multiplied
+    for (int a = 0; a < NA; ++a)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[a][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
+    uint32_t wc[NA], wn[NA];  // words of the segment being multiplied and of the next one
+    eword(wc, 0);
     loadA(0, 0, wc);
     loadA(1, 1, wc);
     loadA(2, 2, wc);
@@ -648,55 +671,71 @@ __device__ inline void stream_tile_lds(f32x4 (&acc)[NT], const uint8_t *__restri
     for (int kb = 0; kb < KB; kb += kSegK) {  // one staged segment per iteration
         const int sg = kb / kSegK;
         const ActSeg &cur = seg[sg & 1];
-        const uint32_t wn = eword(min(sg + 1, nseg - 1));  // the next segment's (the last one's past the end)
+        eword(wn, min(sg + 1, nseg - 1));  // the last segment's past the end
 #pragma unroll
         for (int u = 0; u < kSegK; ++u) {
-            // block kb+3 is this segment's, kb+4.. the next one's; past the end: reload the last block
+            // block kb+3 is this segment's, kb+4.. the next one's; past the end: reload the last block.
+            // The scheduling barrier keeps each block's loads here: left to itself the
+            // scheduler sinks the next segment's loads to the end of the segment, and every
+            // segment then starts with a full memory latency.
             loadA((u + 3) & 3, min(kb + u + 3, KB - 1), u == 0 ? wc : wn);
+            __builtin_amdgcn_sched_barrier(0);
             compute(u, cur, u, kb + u);
         }
-        wc = wn;
+#pragma unroll
+        for (int a = 0; a < NA; ++a) wc[a] = wn[a];
         st.store(seg[(sg + 1) & 1], tid);
         st.load(B, min(sg + 2, nseg - 1));
         sync_lds();
     }
 }
 
-// gate/up: item = (chunk, rows [i0, i0+8W)) for W waves; wave w streams gate
-// (w < W/2) or up (w >= W/2) rows i0 + 16*(w % (W/2)).  The accumulators meet in
-// LDS (over the staging buffer the last segment no longer needs) and wave e < NT*W/4
-// forms h and its 2-term split for token tile e % NT of 32-row group e / NT (32 rows
-// are one E8M0 group per token).
-template <int FMT, int NT, int W, bool PK>
+// gate/up: item = (chunk, NA*8W rows of the intermediate dimension) for W waves; wave w
+// streams NA gate (w < W/2) or up (w >= W/2) tiles, rows i0 + 16*q for tiles
+// q = NA*(w % (W/2)) + a.  The accumulators meet in LDS (over the staging buffer the
+// last segment no longer needs) and wave e < NT*NA*W/4 forms h and its 2-term split for
+// token tile e % NT of 32-row group e / NT (32 rows are one E8M0 group per token).
+template <int FMT, int NT, int W, int NA, bool PK>
 __device__ inline void w13_item_lds(const uint8_t *__restrict__ we, const uint8_t *__restrict__ se, int H, int I,
                                     int i0, int slot0, int mc, const int32_t *__restrict__ tok_of, const ActRsrc &X,
                                     uint8_t *__restrict__ hs_hi, uint8_t *__restrict__ hs_lo,
                                     uint8_t *__restrict__ he_hi, uint8_t *__restrict__ he_lo, ActSeg (&seg)[2],
                                     int wave, int lane, int tid)
 {
-    constexpr int HW = W / 2;  // waves per projection
-    constexpr int NG = W / 4;  // 32-row groups per item
+    constexpr int HW = W / 2;       // waves per projection
+    constexpr int NQ = HW * NA;     // tiles per projection
+    constexpr int NG = NQ / 2;      // 32-row groups per item
+    static_assert(NG * NT <= W, "one epilogue wave per (group, token tile)");
     const int r = lane & 15, g = lane >> 4;
-    const int row0 = (wave >= HW ? I : 0) + i0 + 16 * (wave % HW);
-    const uint8_t *arow = wlane<PK>(we, row0, FMT == 0 ? (size_t)H : (size_t)H / 2, lane);
-    const uint8_t *erow = se + (size_t)(row0 + (PK ? 0 : r)) * (H / 32);
-    const float *sblk = (const float *)se + (size_t)(row0 / 128) * (H / 128);
+    const size_t rowb = FMT == 0 ? (size_t)H : (size_t)H / 2;
+    const uint8_t *arow[NA];
+    const uint8_t *erow[NA];
+    const float *sblk[NA];
+#pragma unroll
+    for (int a = 0; a < NA; ++a) {
+        const int row0 = (wave >= HW ? I : 0) + i0 + 16 * (NA * (wave % HW) + a);
+        arow[a] = wlane<PK>(we, row0, rowb, lane);
+        erow[a] = se + (size_t)(row0 + (PK ? 0 : r)) * (H / 32);
+        sblk[a] = (const float *)se + (size_t)(row0 / 128) * (H / 128);
+    }
     Stager<NT, W> st;
     st.init(tok_of, slot0, mc, H, tid);
-    f32x4 acc[NT];
-    stream_tile_lds<FMT, NT, W, PK>(acc, arow, erow, sblk, H / 128, X, st, seg, lane, tid);
-    // red[w][j][lane]: W*2*64 f32x4 fit in seg[1].code, which the next item first
-    // writes after its first barrier, so no wave still reads red by then.
-    static_assert(sizeof(f32x4) * W * 2 * 64 <= sizeof(seg[1].code), "reduction buffer");
+    f32x4 acc[NA][NT];
+    stream_tile_lds<FMT, NT, W, NA, PK>(acc, arow, erow, sblk, H / 128, X, st, seg, lane, tid);
+    // red[(proj*NQ + q)*NT + j][lane]: 2*NQ*NT*64 f32x4 fit in seg[1].code, which the
+    // next item first writes after its first barrier, so no wave still reads red by then.
+    static_assert(sizeof(f32x4) * 2 * NQ * NT * 64 <= sizeof(seg[1].code), "reduction buffer");
     f32x4 *red = reinterpret_cast<f32x4 *>(&seg[1].code[0][0][0]);
+    auto ridx = [&](int proj, int q, int j) { return ((proj * NQ + q) * NT + j) * 64 + lane; };
 #pragma unroll
-    for (int j = 0; j < NT; ++j) red[(wave * 2 + j) * 64 + lane] = acc[j];
+    for (int a = 0; a < NA; ++a)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) red[ridx(wave / HW, NA * (wave % HW) + a, j)] = acc[a][j];
     sync_lds();
     if (wave < NG * NT) {
         const int j = wave % NT, grp = wave / NT;
-        const f32x4 g0 = red[((2 * grp) * 2 + j) * 64 + lane], g1 = red[((2 * grp + 1) * 2 + j) * 64 + lane];
-        const f32x4 u0 = red[((HW + 2 * grp) * 2 + j) * 64 + lane];
-        const f32x4 u1 = red[((HW + 2 * grp + 1) * 2 + j) * 64 + lane];
+        const f32x4 g0 = red[ridx(0, 2 * grp, j)], g1 = red[ridx(0, 2 * grp + 1, j)];
+        const f32x4 u0 = red[ridx(1, 2 * grp, j)], u1 = red[ridx(1, 2 * grp + 1, j)];
         float h[8], res[8];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -731,7 +770,7 @@ __device__ inline void w13_item_lds(const uint8_t *__restrict__ we, const uint8_
     }
 }
 
-template <int FMT, int W, bool PK>
+template <int FMT, int W, int NA, bool PK>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W == 8 ? 4 : 1))) void w13_mfma_lds_kernel(
     const uint8_t *__restrict__ ew, const uint8_t *__restrict__ es, const int32_t *__restrict__ meta,
     const int32_t *__restrict__ tok_of, const uint8_t *__restrict__ xs_hi, const uint8_t *__restrict__ xs_lo,
@@ -741,7 +780,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W == 8 ?
 {
     __shared__ ActSeg seg[2];
     const MetaIdx mi{E};
-    const int tiles = I / (8 * W);
+    const int tiles = I / (8 * W * NA);
     const int n_items = meta[mi.n_mfma_chunks()] * tiles;
     const int4 *recs = reinterpret_cast<const int4 *>(meta + mi.chunk_rec());
     const int tid = threadIdx.x, lane = tid & 63;
@@ -749,53 +788,60 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W == 8 ?
     const ActRsrc X = act_rsrc(xs_hi, xs_lo, xe_hi, xe_lo, (uint32_t)T, (uint32_t)H);
     for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
         const int4 rec = recs[item / tiles];  // {expert, first slot, tokens, -}
-        const int i0 = (item % tiles) * 8 * W;
+        const int i0 = (item % tiles) * 8 * W * NA;
         const uint8_t *we = ew + (size_t)rec.x * ewb;
         const uint8_t *se = es + (size_t)rec.x * esb;
         if (rec.z > 16)
-            w13_item_lds<FMT, 2, W, PK>(we, se, H, I, i0, rec.y, rec.z, tok_of, X, hs_hi, hs_lo, he_hi, he_lo, seg,
-                                    wave, lane, tid);
+            w13_item_lds<FMT, 2, W, NA, PK>(we, se, H, I, i0, rec.y, rec.z, tok_of, X, hs_hi, hs_lo, he_hi, he_lo,
+                                            seg, wave, lane, tid);
         else
-            w13_item_lds<FMT, 1, W, PK>(we, se, H, I, i0, rec.y, rec.z, tok_of, X, hs_hi, hs_lo, he_hi, he_lo, seg,
-                                    wave, lane, tid);
+            w13_item_lds<FMT, 1, W, NA, PK>(we, se, H, I, i0, rec.y, rec.z, tok_of, X, hs_hi, hs_lo, he_hi, he_lo,
+                                            seg, wave, lane, tid);
     }
 }
 
-// down: item = (chunk, rows [n0, n0+16W)) for W waves; wave w streams rows n0 + 16w.
-template <int FMT, int NT, int W, bool PK>
+// down: item = (chunk, rows [n0, n0+16*NA*W)) for W waves; wave w streams rows
+// n0 + 16*(NA*w + a), a < NA.
+template <int FMT, int NT, int W, int NA, bool PK>
 __device__ inline void w2_item_lds(const uint8_t *__restrict__ we2, const uint8_t *__restrict__ se, int H, int I,
                                    int n0, int slot0, int mc, const ActRsrc &Hs, float *__restrict__ obuf,
                                    ActSeg (&seg)[2], int wave, int lane, int tid)
 {
     const int r = lane & 15, g = lane >> 4;
-    const int row0 = n0 + 16 * wave;
-    const uint8_t *arow = wlane<PK>(we2, row0, FMT == 0 ? (size_t)I : (size_t)I / 2, lane);
-    const uint8_t *erow = se + (size_t)2 * I * (H / 32) + (size_t)(row0 + (PK ? 0 : r)) * (I / 32);
-    const float *sblk = (const float *)se + (size_t)2 * (I / 128) * (H / 128) + (size_t)(row0 / 128) * (I / 128);
+    const size_t rowb = FMT == 0 ? (size_t)I : (size_t)I / 2;
+    const uint8_t *arow[NA];
+    const uint8_t *erow[NA];
+    const float *sblk[NA];
+#pragma unroll
+    for (int a = 0; a < NA; ++a) {
+        const int row0 = n0 + 16 * (NA * wave + a);
+        arow[a] = wlane<PK>(we2, row0, rowb, lane);
+        erow[a] = se + (size_t)2 * I * (H / 32) + (size_t)(row0 + (PK ? 0 : r)) * (I / 32);
+        sblk[a] = (const float *)se + (size_t)2 * (I / 128) * (H / 128) + (size_t)(row0 / 128) * (I / 128);
+    }
     Stager<NT, W> st;
     st.init(nullptr, slot0, mc, I, tid);
-    f32x4 acc[NT];
-    stream_tile_lds<FMT, NT, W, PK>(acc, arow, erow, sblk, I / 128, Hs, st, seg, lane, tid);
+    f32x4 acc[NA][NT];
+    stream_tile_lds<FMT, NT, W, NA, PK>(acc, arow, erow, sblk, I / 128, Hs, st, seg, lane, tid);
 #pragma unroll
     for (int j = 0; j < NT; ++j)
-        if (16 * j + r < mc)
-            *reinterpret_cast<f32x4 *>(obuf + ((size_t)slot0 + 16 * j + r) * H + row0 + 4 * g) = acc[j];
+        if (16 * j + r < mc) {
+            const size_t slot = (size_t)slot0 + 16 * j + r;
+#pragma unroll
+            for (int a = 0; a < NA; ++a)
+                *reinterpret_cast<f32x4 *>(obuf + slot * H + n0 + 16 * (NA * wave + a) + 4 * g) = acc[a][j];
+        }
 }
 
-template <int FMT, int W, bool PK>
-__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W == 8 ? 4 : 1))) void w2_mfma_lds_kernel(const uint8_t *__restrict__ ew,
-                                                             const uint8_t *__restrict__ es,
-                                                             const int32_t *__restrict__ meta,
-                                                             const uint8_t *__restrict__ hs_hi,
-                                                             const uint8_t *__restrict__ hs_lo,
-                                                             const uint8_t *__restrict__ he_hi,
-                                                             const uint8_t *__restrict__ he_lo,
-                                                             float *__restrict__ obuf, int P, int H, int I, int E,
-                                                             size_t ewb, size_t esb)
+template <int FMT, int W, int NA, bool PK>
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W == 8 ? 4 : 1))) void w2_mfma_lds_kernel(
+    const uint8_t *__restrict__ ew, const uint8_t *__restrict__ es, const int32_t *__restrict__ meta,
+    const uint8_t *__restrict__ hs_hi, const uint8_t *__restrict__ hs_lo, const uint8_t *__restrict__ he_hi,
+    const uint8_t *__restrict__ he_lo, float *__restrict__ obuf, int P, int H, int I, int E, size_t ewb, size_t esb)
 {
     __shared__ ActSeg seg[2];
     const MetaIdx mi{E};
-    const int tiles = H / (16 * W);
+    const int tiles = H / (16 * W * NA);
     const int n_items = meta[mi.n_mfma_chunks()] * tiles;
     const int4 *recs = reinterpret_cast<const int4 *>(meta + mi.chunk_rec());
     const int tid = threadIdx.x, lane = tid & 63;
@@ -804,13 +850,13 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W == 8 ?
     const ActRsrc Hs = act_rsrc(hs_hi, hs_lo, he_hi, he_lo, (uint32_t)P, (uint32_t)I);
     for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
         const int4 rec = recs[item / tiles];
-        const int n0 = (item % tiles) * 16 * W;
+        const int n0 = (item % tiles) * 16 * W * NA;
         const uint8_t *we2 = ew + (size_t)rec.x * ewb + w2off;
         const uint8_t *se = es + (size_t)rec.x * esb;
         if (rec.z > 16)
-            w2_item_lds<FMT, 2, W, PK>(we2, se, H, I, n0, rec.y, rec.z, Hs, obuf, seg, wave, lane, tid);
+            w2_item_lds<FMT, 2, W, NA, PK>(we2, se, H, I, n0, rec.y, rec.z, Hs, obuf, seg, wave, lane, tid);
         else
-            w2_item_lds<FMT, 1, W, PK>(we2, se, H, I, n0, rec.y, rec.z, Hs, obuf, seg, wave, lane, tid);
+            w2_item_lds<FMT, 1, W, NA, PK>(we2, se, H, I, n0, rec.y, rec.z, Hs, obuf, seg, wave, lane, tid);
     }
 }
 
@@ -822,7 +868,10 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W == 8 ?
 // weight byte and, held to 128 VGPRs, run two per CU (the MXFP4 layer at T=256:
 // 570k against 604k tokens/s).
 template <int FMT>
-constexpr int kStagedWaves = FMT == 0 ? 4 : 8;
+constexpr int kStagedWaves = FMT == 0 ? 4 : 4;
+// Weight tiles per wave of the staged kernels (NA).
+template <int FMT>
+constexpr int kStagedTiles = FMT == 0 ? 1 : 2;
 
 // Workgroups for `items_per_chunk` items per chunk record, `per_block` items per workgroup.
 int mfma_grid(const Layer &L, int T, int k, int items_per_chunk, int per_block)
@@ -838,9 +887,9 @@ template <int FMT, bool PK>
 hipError_t launch_w13_lds(const Layer &L, const uint8_t *ew, const uint8_t *es, int T, int k, const int32_t *meta,
                           const int32_t *tok_of, const Workspace &ws, hipStream_t st)
 {
-    constexpr int W = kStagedWaves<FMT>;
-    dim3 grid(mfma_grid(L, T, k, L.I / (8 * W), 1)), block(64 * W);
-    w13_mfma_lds_kernel<FMT, W, PK><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.xs_hi, ws.xs_lo, ws.xe_hi, ws.xe_lo,
+    constexpr int W = kStagedWaves<FMT>, NA = kStagedTiles<FMT>;
+    dim3 grid(mfma_grid(L, T, k, L.I / (8 * W * NA), 1)), block(64 * W);
+    w13_mfma_lds_kernel<FMT, W, NA, PK><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.xs_hi, ws.xs_lo, ws.xe_hi, ws.xe_lo,
                                                         ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, T, L.H, L.I, L.E,
                                                         L.expert_w_bytes, L.expert_s_bytes);
     return hipGetLastError();
@@ -850,9 +899,9 @@ template <int FMT, bool PK>
 hipError_t launch_w2_lds(const Layer &L, const uint8_t *ew, const uint8_t *es, int T, int k, const int32_t *meta,
                          const Workspace &ws, hipStream_t st)
 {
-    constexpr int W = kStagedWaves<FMT>;
-    dim3 grid(mfma_grid(L, T, k, L.H / (16 * W), 1)), block(64 * W);
-    w2_mfma_lds_kernel<FMT, W, PK><<<grid, block, 0, st>>>(ew, es, meta, ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, ws.o,
+    constexpr int W = kStagedWaves<FMT>, NA = kStagedTiles<FMT>;
+    dim3 grid(mfma_grid(L, T, k, L.H / (16 * W * NA), 1)), block(64 * W);
+    w2_mfma_lds_kernel<FMT, W, NA, PK><<<grid, block, 0, st>>>(ew, es, meta, ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, ws.o,
                                                        T * k, L.H, L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
     return hipGetLastError();
 }
