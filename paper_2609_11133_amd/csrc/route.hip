@@ -1050,13 +1050,12 @@ hipError_t launch_zero(int32_t *p, int n, hipStream_t st)
 
 hipError_t launch_route(const Layer &L, const RouteParams &P, hipStream_t st)
 {
-    // Experts per wave: enough waves to cover the GPU, few experts per wave at small T:
-    // one up to 4096 (token, expert) pairs (480B-shaped layer at T=16: 20.8 -> 18.5 us
-    // against two), then about 2048 waves (at 8192 pairs two experts per wave beat one,
-    // 22.9 against 24.7 us).
-    const int target_waves = 2048;
-    int epw = P.T * L.E <= 4096 ? 1 : (P.T * L.E + target_waves - 1) / target_waves;
-    epw = epw < 1 ? 1 : (epw > kEPW ? kEPW : epw);
+    // Experts per wave: one up to 6400 (token, expert) pairs, four above.  Timed on the
+    // 235B- and 480B-shaped routers with one to four experts per wave at 2048-12288
+    // pairs: one is best or within 1.3 us up to 6400 pairs (480B-shaped, 32 tokens:
+    // 16.5 us against 17.3 / 17.9 / 18.9 with two / three / four), four from 7168 pairs on
+    // or within 0.8 us (235B-shaped, 64 tokens: 15.6 against 18.5 with one).
+    const int epw = P.T * L.E <= 6400 ? 1 : kEPW;
     const int bpt = (L.E + 4 * epw - 1) / (4 * epw);
     RouteArgs A;
     A.x = P.x;
