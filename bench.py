@@ -330,7 +330,8 @@ def run_attn(args, dev):
             "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "dtype": "bf16", "data": "synthetic",
             "config": {"workload": f"{cfg.name}: {cfg.batch} sequences, {cfg.n_q_heads} query / {cfg.n_kv_heads} "
                                    f"key-value heads, head dim 128, 16-token pages, {cfg.mix} context lengths "
-                                   f"(mean {ctx_mean:.0f} tokens)", "cold_cache": f"{copies} KV-cache copies x 4 draws"},
+                                   f"(mean {ctx_mean:.0f} tokens), block-table rows of {mp} pages",
+                       "cold_cache": f"{copies} KV-cache copies x 4 draws"},
             "roofline": {"kernel": "attn_split_kernel + attn_combine_kernel (one step)", "bound": "hbm",
                          "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS,
                          "bytes_per_step": kv},

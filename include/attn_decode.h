@@ -55,20 +55,23 @@ typedef struct attn_decode_config {
     int32_t page_size;         /* P: 16 */
     int32_t max_batch;         /* largest B of any call, 1..4096 */
     int32_t max_pages_per_seq; /* block-table row length, 1..65536 */
-    int32_t fused_merge_max_splits; /* the context is cut into 256-token pieces, and each
-                                  workgroup walks R consecutive pieces of a row of
-                                  max_pages_per_seq pages (online softmax across them),
-                                  with R the smallest that leaves at most this many splits
-                                  per sequence; R grows further when one piece per
-                                  workgroup would need more than two rounds of resident
-                                  workgroups for max_batch sequences (then the grid is at
-                                  most three workgroups per compute unit).  The split
-                                  kernel merges the splits itself (its last workgroup per
+    int32_t fused_merge_max_splits; /* the context is cut into 256-token pieces.  The grid
+                                  has S splits per sequence: the fewest that cover a row
+                                  of max_pages_per_seq pages with at most this many, and
+                                  fewer when one piece per workgroup would need more than
+                                  two rounds of resident workgroups for max_batch
+                                  sequences (then the grid is at most three workgroups per
+                                  compute unit).  Each sequence walks R = ceil(its own
+                                  pieces / S) consecutive pieces per workgroup (online
+                                  softmax across them), so a short context uses one piece
+                                  per split whatever the capacity.  The split kernel
+                                  merges the splits itself (its last workgroup per
                                   sequence and key/value head).  0 = library default 16,
                                   at most 16; negative = one piece per split, merged by a
                                   second kernel.  Where R = 1 both merges give the same
-                                  bits; R depends only on this configuration and the
-                                  device. */
+                                  bits; a sequence's result depends only on its own
+                                  context, this configuration and the device, never on
+                                  the rest of the batch. */
     int32_t reserved[3];       /* must be zero */
 } attn_decode_config;
 

@@ -45,6 +45,7 @@ class AttnConfig:
     mix: str  # "standard", "agentic" or "long:N"
     head_dim: int = 128
     page: int = 16
+    capacity: Optional[int] = None  # tokens a block-table row holds (None: the longest context)
 
 
 ATTN_CONFIGS = [
@@ -52,6 +53,9 @@ ATTN_CONFIGS = [
     AttnConfig("qwen3-235b-a22b-attn-standard", 64, 4, 24, "standard"),
     AttnConfig("qwen3-coder-480b-a35b-tp4-attn-agentic", 24, 2, 48, "agentic"),
     AttnConfig("qwen3-235b-a22b-attn-long32k", 64, 4, 24, "long:32768"),
+    # the agentic step on a configuration sized for 32K-token contexts (block-table rows
+    # of 2048 pages), as a server that also admits long contexts would size it
+    AttnConfig("qwen3-235b-a22b-attn-agentic-cap32k", 64, 4, 24, "agentic", capacity=32768),
 ]
 ATTN_BY_NAME = {c.name: c for c in ATTN_CONFIGS}
 
@@ -96,6 +100,8 @@ def host_attn(cfg: AttnConfig, seed: int = SEED, draw: int = 0, ctx: Optional[np
     B, Hq, Hkv, D, P = cfg.batch, cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim, cfg.page
     L = context_lengths(cfg.mix, B, seed, draw) if ctx is None else np.asarray(ctx, np.int32)
     pages = (L.astype(np.int64) + P - 1) // P
+    if max_pages is None and cfg.capacity:
+        max_pages = (cfg.capacity + P - 1) // P
     mp = int(max(1, pages.max())) if max_pages is None else max_pages
     used = int(pages.sum())
     n_pages = max(1, used + used // 10)

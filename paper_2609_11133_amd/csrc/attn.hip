@@ -82,7 +82,7 @@ __device__ inline bf16x8 as_bf16x8(const u32x4v &u) { return __builtin_bit_cast(
 // Split kernel: partial (max, sum, O) of one 256-token split for one (sequence, key/value
 // head) and its query heads.  Grid (splits, Hkv, B), 256 threads.  Scores are kept in
 // log2 units (scale * log2 e folded in), so p = exp2(s - m).  A split is R consecutive
-// chunks (online softmax across them).  FUSED: the merge of the splits happens here
+// chunks (online softmax across them); with FUSED each sequence sets its own R.  FUSED: the merge of the splits happens here
 // (S <= kFusedSplits; `cnt` holds one zeroed counter per (b, g), left at zero again), and
 // `out` is written here.
 template <bool FUSED>
@@ -101,6 +101,11 @@ __global__ __launch_bounds__(256) void attn_split_kernel(const uint16_t *__restr
     __shared__ int s_last;
     const int c = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
     const int L = min(max(ctx[b], 0), max_pages * kP);
+    // FUSED: each sequence spreads its own chunks over the S splits of the grid, at least
+    // one chunk per split (R = ceil(chunks / S), at most the configuration's R): a short
+    // context in a configuration sized for long ones still gets one workgroup per chunk,
+    // and a sequence's result depends on its own length only, never on its batch.
+    if (FUSED) R = max(1, ((L + kChunk - 1) / kChunk + S - 1) / S);
     const int t0 = c * R * kChunk;  // first token of this split
     const int tid = threadIdx.x, lane = tid & 63;
     uint16_t *orow = out + ((size_t)b * Hkv + g) * G * kD;  // the group's [G][D] outputs
@@ -439,14 +444,26 @@ int check_config(const attn_decode_config *c)
 
 int max_splits(const attn_decode_config *c) { return (c->max_pages_per_seq * kP + kChunk - 1) / kChunk; }
 
+// Partials per (sequence, key/value head) the workspace holds: every 256-token chunk's
+// when the second kernel merges; with the merge in the split kernel at most the split
+// limit (the grid's S never exceeds it, whatever the device), so the workspace does not
+// grow with the context capacity.
+int partial_slots(const attn_decode_config *c)
+{
+    const int sf = max_splits(c);
+    if (c->fused_merge_max_splits < 0) return sf;
+    const int lim = c->fused_merge_max_splits == 0 ? kFusedSplits : c->fused_merge_max_splits;
+    return sf < lim ? sf : lim;
+}
+
 size_t partial_o_bytes(const attn_decode_config *c)
 {
-    return ((size_t)c->max_batch * c->n_kv_heads * max_splits(c) * 16 * kD * 4 + 255) & ~(size_t)255;
+    return ((size_t)c->max_batch * c->n_kv_heads * partial_slots(c) * 16 * kD * 4 + 255) & ~(size_t)255;
 }
 
 size_t partial_ml_bytes(const attn_decode_config *c)
 {
-    return ((size_t)c->max_batch * c->n_kv_heads * max_splits(c) * 16 * 8 + 255) & ~(size_t)255;
+    return ((size_t)c->max_batch * c->n_kv_heads * partial_slots(c) * 16 * 8 + 255) & ~(size_t)255;
 }
 
 size_t counter_words(const attn_decode_config *c) { return (size_t)c->max_batch * c->n_kv_heads; }
@@ -467,13 +484,14 @@ int compute_units()
     return n;
 }
 
-// 256-token chunks per workgroup; 0 when the configuration asks for the second kernel's
-// merge (every chunk its own split).  At least enough that `lim` splits cover a row.
-// When one chunk per split would need more than two rounds of resident workgroups (two
-// per compute unit), the splits grow until the grid is at most three workgroups per
-// compute unit: the walk inside a workgroup keeps as many loads in flight as more
-// workgroups would, with fewer partials to merge.  Only the configuration enters, so a
-// sequence's result does not depend on the batch it is called in.
+// 256-token chunks per workgroup for a full row of the block table, which sets the
+// grid's split count S = ceil(row chunks / R); 0 when the configuration asks for the
+// second kernel's merge (every chunk its own split).  At least enough that `lim` splits
+// cover a row.  When one chunk per split would need more than two rounds of resident
+// workgroups (two per compute unit), the splits grow until the grid is at most three
+// workgroups per compute unit: the walk inside a workgroup keeps as many loads in flight
+// as more workgroups would, with fewer partials to merge.  Only the configuration enters;
+// the kernel spreads each sequence's own chunks over the S splits.
 int chunks_per_split(const attn_decode_config *c)
 {
     if (c->fused_merge_max_splits < 0) return 0;
@@ -550,7 +568,8 @@ extern "C" int attn_decode_forward(const attn_decode_config *cfg, void *workspac
     int32_t *cnt = (int32_t *)((char *)workspace + partial_o_bytes(cfg) + partial_ml_bytes(cfg));
     hipStream_t st = (hipStream_t)stream;
     if (R > 0) {
-        const int S = (max_splits(cfg) + R - 1) / R;  // at most the limit
+        const int S = (max_splits(cfg) + R - 1) / R;  // at most the limit, and at most partial_slots
+        if (S > partial_slots(cfg)) return fail(ATTN_ERR_INVALID, "internal: %d splits exceed the workspace", S);
         attn_split_kernel<true><<<dim3(S, Hkv, batch), 256, 0, st>>>(
             (const uint16_t *)q, (const uint16_t *)k_cache, (const uint16_t *)v_cache, n_pages, block_table,
             cfg->max_pages_per_seq, ctx_lens, Hkv, G, scale * kLog2e, po, pml, S, R, cnt, (uint16_t *)out);

@@ -185,3 +185,23 @@ def test_long_context_sampled(dev):
             m.forward(d["q"], d["k_cache"], d["v_cache"], h.n_pages, d["block_table"], d["ctx"], nb, scale, out2)
             torch.cuda.synchronize(dev)
             assert torch.equal(out2[:nb], out[:nb]) and torch.all(out2[nb:] == 0x7FC1)
+
+
+def test_capacity_sized_config_short_contexts(dev):
+    """The agentic step on a configuration sized for 32K-token contexts (2048-page rows,
+    so the grid has 8 splits of up to 16 pieces): every sequence spreads its own 3-8
+    pieces one per split, matches the oracle per row, and a call with fewer sequences on
+    the same workspace repeats their rows bit for bit."""
+    cfg = A.ATTN_BY_NAME["qwen3-235b-a22b-attn-agentic-cap32k"]
+    h = A.host_attn(cfg, draw=5)
+    assert h.block_table.shape[1] == 2048
+    scale = 1 / np.sqrt(128)
+    out, m, d = run_gpu(cfg, h, dev, scale)
+    ref = oracle.attn_decode(h.q, h.k_cache, h.v_cache, h.block_table, h.ctx, scale)
+    check(bf16_to_f64(out), ref, label=cfg.name)
+    nb = 7
+    out2 = torch.full_like(out, 0x7FC1)
+    m.forward(d["q"], d["k_cache"], d["v_cache"], h.n_pages, d["block_table"], d["ctx"], nb, scale, out2)
+    torch.cuda.synchronize(dev)
+    assert torch.equal(out2[:nb], out[:nb]) and torch.all(out2[nb:] == 0x7FC1)
+
