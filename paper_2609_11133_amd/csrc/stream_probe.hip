@@ -14,6 +14,16 @@
 //                    layout): each lane 16 bytes at 16l and 1024 + 16l of a block, eight
 //                    blocks in flight, non-temporal
 //          copy      contiguous 16-byte copy (reads and writes MiB each)
+//          tilestream <MiB> <iters> <tile KiB> <depth>
+//                    one launch streams MiB as packed tiles of <tile KiB> per wave (2 KB
+//                    blocks, <depth> of them in flight per wave, 4 or 8), non-temporal;
+//                    successive launches read different regions of a 4 GiB arena, so no
+//                    launch finds its bytes in the MALL: the time of one cold launch of that
+//                    shape, ramp and tail included
+//          chain <iters>
+//                    the launch floor of one decode step: four empty kernels back to back
+//                    in the grid shapes of the 235B-shaped layer's step at one token
+//                    (routing 32, gate/up 432, down 288, combine 4 workgroups of 256)
 // Prints one line: mode, bytes moved per launch, mean ms, GB/s.
 #include <hip/hip_runtime.h>
 #include <stdio.h>
@@ -104,6 +114,40 @@ __global__ __launch_bounds__(256) void packed_kernel(const uint8_t *__restrict__
     if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9E3779B9u) sink[0] = 1;
 }
 
+// Wave w streams tile w (tile_blocks 2 KB blocks at 2048 * tile_blocks * w), lane l
+// reading 16 bytes at 16l and 1024 + 16l of each block, D blocks in flight.
+template <int D>
+__global__ __launch_bounds__(256) void tilestream_kernel(const uint8_t *__restrict__ a, int tile_blocks,
+                                                         uint32_t *__restrict__ sink)
+{
+    const int lane = threadIdx.x & 63;
+    const size_t wave = (size_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const uint8_t *tile = a + wave * (size_t)tile_blocks * 2048 + 16 * lane;
+    u32x4 acc = {0, 0, 0, 0};
+    u32x4 v[D][2];
+#pragma unroll
+    for (int u = 0; u < D - 1; ++u) {
+        v[u][0] = ld<true>(reinterpret_cast<const u32x4 *>(tile + u * 2048));
+        v[u][1] = ld<true>(reinterpret_cast<const u32x4 *>(tile + u * 2048 + 1024));
+    }
+    for (int kb = 0; kb < tile_blocks; kb += D) {  // tile_blocks is a multiple of D
+#pragma unroll
+        for (int u = 0; u < D; ++u) {
+            const int nb = kb + u + D - 1;  // block loaded now; past the tile: reload the last one
+            const int b = nb < tile_blocks ? nb : tile_blocks - 1;
+            v[(u + D - 1) % D][0] = ld<true>(reinterpret_cast<const u32x4 *>(tile + (size_t)b * 2048));
+            v[(u + D - 1) % D][1] = ld<true>(reinterpret_cast<const u32x4 *>(tile + (size_t)b * 2048 + 1024));
+            acc ^= v[u][0] ^ v[u][1];
+        }
+    }
+    if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9E3779B9u) sink[0] = 1;
+}
+
+__global__ void empty_kernel(uint32_t *__restrict__ sink, int never)
+{
+    if (never == 1) sink[0] = 1;
+}
+
 __global__ __launch_bounds__(256) void copy_kernel(const u32x4 *__restrict__ a, u32x4 *__restrict__ b, size_t n)
 {
     const size_t stride = (size_t)gridDim.x * blockDim.x;
@@ -119,8 +163,89 @@ __global__ __launch_bounds__(256) void copy_kernel(const u32x4 *__restrict__ a, 
         }                                                                                    \
     } while (0)
 
+static int run_tilestream(size_t bytes, int iters, int tile_kib, int depth)
+{
+    if (tile_kib < 2 || tile_kib % 2 || (depth != 4 && depth != 8) || (tile_kib / 2) % depth ||
+        bytes % ((size_t)tile_kib * 1024 * 4)) {
+        fprintf(stderr, "tilestream: tile KiB even, (tile KiB / 2) a multiple of depth (4 or 8), MiB a "
+                        "multiple of 4 tiles\n");
+        return 2;
+    }
+    const size_t arena = (size_t)4 << 30;
+    if (bytes > arena / 4) {
+        fprintf(stderr, "tilestream: at most 1 GiB per launch\n");
+        return 2;
+    }
+    const int regions = (int)(arena / bytes);
+    uint8_t *a = nullptr;
+    uint32_t *sink = nullptr;
+    CHECK(hipMalloc(&a, arena));
+    CHECK(hipMalloc(&sink, 4));
+    CHECK(hipMemset(a, 1, arena));
+    const int tile_blocks = tile_kib / 2;
+    const int grid = (int)(bytes / ((size_t)tile_kib * 1024) / 4);
+    auto launch = [&](int i) {
+        const uint8_t *p = a + (size_t)(i % regions) * bytes;
+        if (depth == 4)
+            tilestream_kernel<4><<<grid, 256>>>(p, tile_blocks, sink);
+        else
+            tilestream_kernel<8><<<grid, 256>>>(p, tile_blocks, sink);
+        CHECK(hipGetLastError());
+    };
+    for (int i = 0; i < regions; ++i) launch(i);
+    CHECK(hipDeviceSynchronize());
+    hipEvent_t e0, e1;
+    CHECK(hipEventCreate(&e0));
+    CHECK(hipEventCreate(&e1));
+    float total = 0.f;
+    for (int i = 0; i < iters; ++i) {  // one launch between two events, each launch cold
+        CHECK(hipEventRecord(e0, 0));
+        launch(i);
+        CHECK(hipEventRecord(e1, 0));
+        CHECK(hipEventSynchronize(e1));
+        float ms = 0.f;
+        CHECK(hipEventElapsedTime(&ms, e0, e1));
+        total += ms;
+    }
+    const float ms = total / iters;
+    printf("tilestream bytes=%zu tile_kib=%d depth=%d waves=%zu ms=%.4f GBps=%.1f\n", bytes, tile_kib, depth,
+           bytes / ((size_t)tile_kib * 1024), ms, bytes / (ms * 1e-3) / 1e9);
+    CHECK(hipFree(a));
+    CHECK(hipFree(sink));
+    return 0;
+}
+
+static int run_chain(int iters)
+{
+    uint32_t *sink = nullptr;
+    CHECK(hipMalloc(&sink, 4));
+    const int grids[4] = {32, 432, 288, 4};
+    auto step = [&]() {
+        for (int g : grids) empty_kernel<<<g, 256>>>(sink, 0);
+        CHECK(hipGetLastError());
+    };
+    for (int i = 0; i < 10; ++i) step();
+    CHECK(hipDeviceSynchronize());
+    hipEvent_t e0, e1;
+    CHECK(hipEventCreate(&e0));
+    CHECK(hipEventCreate(&e1));
+    CHECK(hipEventRecord(e0, 0));
+    for (int i = 0; i < iters; ++i) step();
+    CHECK(hipEventRecord(e1, 0));
+    CHECK(hipEventSynchronize(e1));
+    float ms = 0.f;
+    CHECK(hipEventElapsedTime(&ms, e0, e1));
+    printf("chain kernels=4 us_per_step=%.2f us_per_launch=%.2f\n", ms * 1e3 / iters, ms * 1e3 / iters / 4);
+    CHECK(hipFree(sink));
+    return 0;
+}
+
 int main(int argc, char **argv)
 {
+    if (argc >= 3 && !strcmp(argv[1], "chain")) return run_chain(atoi(argv[2]) > 0 ? atoi(argv[2]) : 1000);
+    if (argc >= 6 && !strcmp(argv[1], "tilestream"))
+        return run_tilestream((size_t)atol(argv[2]) << 20, atoi(argv[3]) > 0 ? atoi(argv[3]) : 1, atoi(argv[4]),
+                              atoi(argv[5]));
     if (argc < 4) {
         fprintf(stderr, "usage: %s read|read_nt|tiles|tiles_nt|deep_nt|packed_nt|copy MiB iters\n", argv[0]);
         return 2;
