@@ -96,8 +96,11 @@ typedef enum {
                                   row l%16's bytes [32g, 32g+16) at 16 l and [32g+16,
                                   32g+32) at 1024 + 16 l, and the E4M3 scales packed
                                   the same way: per tile and 256-input block one 256-byte
-                                  piece, scales [4g, 4g+4) of row l%16 at 4 l; the 16
-                                  bytes of matrix scales stay first).  MXFP4 E8M0 scales
+                                  piece, scales [4g, 4g+4) of row l%16 at 4 l, or, for a
+                                  matrix whose K/256 is a multiple of four, per tile and
+                                  group of four blocks one 1 KB piece, lane l's 4 scales
+                                  of each block of the group (block by block) at 16 l;
+                                  the 16 bytes of matrix scales stay first).  MXFP4 E8M0 scales
                                   are packed per tile and group of four 128-input blocks:
                                   lane l's bytes (K sub-block g of row l%16, blocks 4q..4q+3)
                                   at 4 l of a 256-byte piece (a last group of two blocks:

@@ -693,8 +693,9 @@ __device__ inline void stream_tile_lds(f32x4 (&acc)[NA][NT], const uint8_t *cons
 // gate/up: item = (chunk, NA*8W rows of the intermediate dimension) for W waves; wave w
 // streams NA gate (w < W/2) or up (w >= W/2) tiles, rows i0 + 16*q for tiles
 // q = NA*(w % (W/2)) + a.  The accumulators meet in LDS (over the staging buffer the
-// last segment no longer needs) and wave e < NT*NA*W/4 forms h and its 2-term split for
-// token tile e % NT of 32-row group e / NT (32 rows are one E8M0 group per token).
+// last segment no longer needs) and wave w forms h and its 2-term split for the pairs
+// e = w, w + W, ... < NT*NA*W/4 of token tile e % NT and 32-row group e / NT (32 rows are
+// one E8M0 group per token).
 template <int FMT, int NT, int W, int NA, bool PK>
 __device__ inline void w13_item_lds(const uint8_t *__restrict__ we, const uint8_t *__restrict__ se, int H, int I,
                                     int i0, int slot0, int mc, const int32_t *__restrict__ tok_of, const ActRsrc &X,
@@ -705,7 +706,6 @@ __device__ inline void w13_item_lds(const uint8_t *__restrict__ we, const uint8_
     constexpr int HW = W / 2;       // waves per projection
     constexpr int NQ = HW * NA;     // tiles per projection
     constexpr int NG = NQ / 2;      // 32-row groups per item
-    static_assert(NG * NT <= W, "one epilogue wave per (group, token tile)");
     const int r = lane & 15, g = lane >> 4;
     const size_t rowb = FMT == 0 ? (size_t)H : (size_t)H / 2;
     const uint8_t *arow[NA];
@@ -732,8 +732,8 @@ __device__ inline void w13_item_lds(const uint8_t *__restrict__ we, const uint8_
 #pragma unroll
         for (int j = 0; j < NT; ++j) red[ridx(wave / HW, NA * (wave % HW) + a, j)] = acc[a][j];
     sync_lds();
-    if (wave < NG * NT) {
-        const int j = wave % NT, grp = wave / NT;
+    for (int e = wave; e < NG * NT; e += W) {  // one (group, token tile) per wave and pass
+        const int j = e % NT, grp = e / NT;
         const f32x4 g0 = red[ridx(0, 2 * grp, j)], g1 = red[ridx(0, 2 * grp + 1, j)];
         const f32x4 u0 = red[ridx(1, 2 * grp, j)], u1 = red[ridx(1, 2 * grp + 1, j)];
         float h[8], res[8];
@@ -869,9 +869,12 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W == 8 ?
 // 570k against 604k tokens/s).
 template <int FMT>
 constexpr int kStagedWaves = FMT == 0 ? 4 : 4;
-// Weight tiles per wave of the staged kernels (NA).
-template <int FMT>
-constexpr int kStagedTiles = FMT == 0 ? 1 : 2;
+// Weight tiles per wave of the staged kernels (NA).  E2M1 tiles: four on packed weights
+// (each staged activation fragment then feeds four tiles; MXFP4 Zipf layer at T=256
+// 1,035k -> 1,094k tokens/s), two on row-major ones (four need more than the 256
+// registers two waves per SIMD allow there).
+template <int FMT, bool PK>
+constexpr int kStagedTiles = FMT == 0 ? 1 : (PK ? 4 : 2);
 
 // Workgroups for `items_per_chunk` items per chunk record, `per_block` items per workgroup.
 int mfma_grid(const Layer &L, int T, int k, int items_per_chunk, int per_block)
@@ -887,7 +890,7 @@ template <int FMT, bool PK>
 hipError_t launch_w13_lds(const Layer &L, const uint8_t *ew, const uint8_t *es, int T, int k, const int32_t *meta,
                           const int32_t *tok_of, const Workspace &ws, hipStream_t st)
 {
-    constexpr int W = kStagedWaves<FMT>, NA = kStagedTiles<FMT>;
+    constexpr int W = kStagedWaves<FMT>, NA = kStagedTiles<FMT, PK>;
     dim3 grid(mfma_grid(L, T, k, L.I / (8 * W * NA), 1)), block(64 * W);
     w13_mfma_lds_kernel<FMT, W, NA, PK><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.xs_hi, ws.xs_lo, ws.xe_hi, ws.xe_lo,
                                                         ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, T, L.H, L.I, L.E,
@@ -899,7 +902,7 @@ template <int FMT, bool PK>
 hipError_t launch_w2_lds(const Layer &L, const uint8_t *ew, const uint8_t *es, int T, int k, const int32_t *meta,
                          const Workspace &ws, hipStream_t st)
 {
-    constexpr int W = kStagedWaves<FMT>, NA = kStagedTiles<FMT>;
+    constexpr int W = kStagedWaves<FMT>, NA = kStagedTiles<FMT, PK>;
     dim3 grid(mfma_grid(L, T, k, L.H / (16 * W * NA), 1)), block(64 * W);
     w2_mfma_lds_kernel<FMT, W, NA, PK><<<grid, block, 0, st>>>(ew, es, meta, ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, ws.o,
                                                        T * k, L.H, L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
@@ -990,9 +993,11 @@ __global__ void pack_e8m0_kernel(const uint8_t *__restrict__ src, uint8_t *__res
 }
 
 // NVFP4 E4M3 scales, row-major -> packed 16-row tiles: per matrix [rows][K/16] bytes
-// after each expert's 16 bytes of matrix scales; per (16-row tile, 256-input block) one
-// 256-byte piece, lane l's 4 bytes (scales [4g, 4g+4) of row l%16) at 4l.  One thread
-// per 4-byte word of the destination.
+// after each expert's 16 bytes of matrix scales.  Per (16-row tile, 256-input block) one
+// 256-byte piece, lane l's 4 bytes (scales [4g, 4g+4) of row l%16) at 4l; where the
+// matrix's block count K/256 is a multiple of four, per (16-row tile, group of four
+// blocks) one 1 KB piece instead, lane l's 16 bytes (its 4 bytes of each block of the
+// group, block by block) at 16l.  One thread per 4-byte word of the destination.
 __global__ void pack_scales_kernel(const uint8_t *__restrict__ src, uint8_t *__restrict__ dst, int64_t n_words, int H,
                                    int I, int64_t expert_bytes)
 {
@@ -1003,10 +1008,17 @@ __global__ void pack_scales_kernel(const uint8_t *__restrict__ src, uint8_t *__r
         const int64_t e = off / body, eo = off % body;
         const bool down = eo >= w13;
         const int64_t mo = down ? eo - w13 : eo;
-        const int64_t rowb = (down ? I : H) / 16;        // scale bytes per row
-        const int64_t tile = mo / (16 * rowb), to = mo % (16 * rowb);
-        const int64_t kb = to / 256;
-        const int l = (int)(to % 256) / 4, r = l & 15, g = l >> 4;
+        const int K = down ? I : H;
+        const int64_t rowb = K / 16;                     // scale bytes per row
+        const int64_t tile = mo / (16 * rowb);
+        const int w = (int)(mo % (16 * rowb)) / 4;       // word within the tile's scales
+        int l, kb;
+        if ((K / 256) % 4 == 0) {
+            l = (w % 256) / 4, kb = 4 * (w / 256) + w % 4;
+        } else {
+            l = w % 64, kb = w / 64;
+        }
+        const int r = l & 15, g = l >> 4;
         const int64_t base = e * expert_bytes + 16 + (down ? w13 : 0);
         *reinterpret_cast<uint32_t *>(dst + base + mo) =
             *reinterpret_cast<const uint32_t *>(src + base + (tile * 16 + r) * rowb + kb * 16 + 4 * g);

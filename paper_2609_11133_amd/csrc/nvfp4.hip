@@ -31,8 +31,12 @@
 // [32g+16, 32g+32) at 1024 + 16l, read with non-temporal buffer loads off the tile (a
 // wave-uniform resource), so each load instruction of a wave reads 1 KB of contiguous
 // bytes.  The E4M3 scales are packed the same way: a block's 16 rows x 16 scales are one
-// 256-byte piece, lane l's four (scales [4g, 4g+4) of row l%16) at 4l.  Read row by row,
-// the scales were the packed kernels' bound (16 segments of 16 bytes per load).
+// 256-byte piece, lane l's four (scales [4g, 4g+4) of row l%16) at 4l; where a matrix's
+// block count is a multiple of four, per group of four blocks one 1 KB piece instead,
+// lane l's 16 bytes (its four scales of each block of the group, block by block) at 16l,
+// so one 16-byte load per lane brings four blocks' scales (GS below).  Read row by row,
+// the scales were the packed kernels' bound (16 segments of 16 bytes per load), and one
+// 32-bit load per lane and block still cost about a tenth of the gate/up kernel's time.
 //
 // Work items follow the FP8 staged kernels (mfma.hip): one workgroup of W waves per
 // (chunk of <= 32 tokens of one expert, rows), one 16-row weight tile per wave through
@@ -181,11 +185,15 @@ __device__ inline void dequant16(const u32x4v &w, float s0, float s1, f16x8 (&a)
 //   arow  row-major: this lane's weight row; packed: the wave's 16-row tile
 //   srow  row-major: this lane's scale row; packed: the tile's scales
 //   F16   f16 operands (the staged activations are f16), else bf16
-template <int NT, int W, bool PK, bool F16>
+//   GS    packed scales in groups of four blocks (PK, KB a multiple of 4): one 16-byte
+//         load per lane and group, issued a group ahead, at a fixed place in the loop
+//         (a conditional load in the steady state would make every wait conservative)
+template <int NT, int W, bool PK, bool F16, bool GS>
 __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__ arow,
                                    const uint8_t *__restrict__ srow, int KB, __amdgpu_buffer_rsrc_t rs,
                                    Stager<NT, W> &st, Seg (&seg)[2], int lane)
 {
+    static_assert(!GS || PK, "grouped scales are a packed layout");
     const int r = lane & 15, g = lane >> 4;
     const int nseg = (KB + kSegBlk - 1) / kSegBlk;
     u32x4v A[4][2];
@@ -199,7 +207,7 @@ __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__
         if constexpr (PK) {
             A[slot][0] = __builtin_amdgcn_raw_buffer_load_b128(tr, 16u * lane, kb * 2048, kNonTemporal);
             A[slot][1] = __builtin_amdgcn_raw_buffer_load_b128(tr, 16u * lane + 1024u, kb * 2048, kNonTemporal);
-            S[slot] = __builtin_amdgcn_raw_buffer_load_b32(sr, 4u * lane, kb * 256, 0);
+            if constexpr (!GS) S[slot] = __builtin_amdgcn_raw_buffer_load_b32(sr, 4u * lane, kb * 256, 0);
         } else {
             const uint8_t *p = arow + (size_t)kb * (kBlk / 2) + 32 * g;
             A[slot][0] = *reinterpret_cast<const u32x4v *>(p);
@@ -211,9 +219,11 @@ __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__
     // dequantised, so the LDS latency hides behind that VALU work; instructions q
     // accumulate into acc2[q % 2], so consecutive MFMAs do not wait on each other.
     f32x4 acc2[2][NT];
-    auto compute = [&](int slot, const Seg &sg, int kk) {
-        const f32x2 s01 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(S[slot], 1.0f, false);
-        const f32x2 s23 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(S[slot], 1.0f, true);
+    // the four scales of group q of a grouped layout
+    auto load_group = [&](int q) { return __builtin_amdgcn_raw_buffer_load_b128(sr, 16u * lane, q * 1024, 0); };
+    auto compute = [&](int slot, const Seg &sg, int kk, uint32_t sw) {
+        const f32x2 s01 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(sw, 1.0f, false);
+        const f32x2 s23 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(sw, 1.0f, true);
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             u32x4v b[4][NT];
@@ -251,35 +261,53 @@ __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__
     loadA(0, 0);
     loadA(1, min(1, KB - 1));
     loadA(2, min(2, KB - 1));
+    u32x4v SG0 = {0u, 0u, 0u, 0u}, SG1 = {0u, 0u, 0u, 0u};
+    if constexpr (GS) SG0 = load_group(0);
     st.load(rs, 0);
     st.store(seg[0]);
     st.load(rs, min(1, nseg - 1));
     sync_lds();
     int sg = 0, kb = 0;
-    for (; kb + 4 <= KB; sg += 2, kb += 4) {  // two segments (four blocks) per iteration
+    // Four blocks (two segments) per step: blocks kb..kb+3 are multiplied while kb+3..kb+6
+    // load; with grouped scales the next group's load leads the step and `cur` holds
+    // this group's.
+    auto step = [&](const u32x4v &cur, u32x4v &nxt) {
+        if constexpr (GS) nxt = load_group(min((kb >> 2) + 1, KB / 4 - 1));
         loadA(3, min(kb + 3, KB - 1));  // past the end: reload the last block
-        compute(0, seg[0], 0);
+        compute(0, seg[0], 0, GS ? cur[0] : S[0]);
         loadA(0, min(kb + 4, KB - 1));
-        compute(1, seg[0], 1);
+        compute(1, seg[0], 1, GS ? cur[1] : S[1]);
         st.store(seg[1]);
         st.load(rs, min(sg + 2, nseg - 1));
         sync_lds();
         loadA(1, min(kb + 5, KB - 1));
-        compute(2, seg[1], 0);
+        compute(2, seg[1], 0, GS ? cur[2] : S[2]);
         loadA(2, min(kb + 6, KB - 1));
-        compute(3, seg[1], 1);
+        compute(3, seg[1], 1, GS ? cur[3] : S[3]);
         st.store(seg[0]);
         st.load(rs, min(sg + 3, nseg - 1));
         sync_lds();
-    }
-    // Fewer than four blocks remain, in ring slots 0..2: segment sg sits in seg[0] and
-    // segment sg + 1 in the stager's registers.
-    if (kb < KB) compute(0, seg[0], 0);
-    if (kb + 1 < KB) compute(1, seg[0], 1);
-    if (kb + 2 < KB) {
-        st.store(seg[1]);
-        sync_lds();
-        compute(2, seg[1], 0);
+        sg += 2;
+        kb += 4;
+    };
+    if constexpr (GS) {
+        // two steps per iteration, so the current and next groups trade registers by name
+        for (; kb + 8 <= KB;) {
+            step(SG0, SG1);
+            step(SG1, SG0);
+        }
+        if (kb + 4 <= KB) step(SG0, SG1);  // KB is a multiple of 4: nothing remains after
+    } else {
+        while (kb + 4 <= KB) step(SG0, SG1);
+        // Fewer than four blocks remain, in ring slots 0..2: segment sg sits in seg[0] and
+        // segment sg + 1 in the stager's registers.
+        if (kb < KB) compute(0, seg[0], 0, S[0]);
+        if (kb + 1 < KB) compute(1, seg[0], 1, S[1]);
+        if (kb + 2 < KB) {
+            st.store(seg[1]);
+            sync_lds();
+            compute(2, seg[1], 0, S[2]);
+        }
     }
     if (kb < KB) sync_lds();
 #pragma unroll
@@ -291,7 +319,7 @@ __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__
 // gate waves through LDS (seg[1], free once stream_tile returns; the next item first
 // writes it after its first barrier), and the gate waves form h = silu(g) * u, round
 // it to bf16 and store it.
-template <int NT, int W, bool PK>
+template <int NT, int W, bool PK, bool GS>
 __device__ inline void w13_item(const uint8_t *__restrict__ we, const uint8_t *__restrict__ se, int H, int I, int i0,
                                 int slot0, int mc, const int32_t *__restrict__ tok_of, __amdgpu_buffer_rsrc_t xr,
                                 const int32_t *__restrict__ xk, __bf16 *__restrict__ hb, Seg (&seg)[2], int wave,
@@ -306,7 +334,7 @@ __device__ inline void w13_item(const uint8_t *__restrict__ we, const uint8_t *_
     Stager<NT, W> st;
     st.init(tok_of, slot0, mc, H, tid);
     f32x4 acc[NT];
-    stream_tile<NT, W, PK, true>(acc, arow, srow, H / kBlk, xr, st, seg, lane);
+    stream_tile<NT, W, PK, true, GS>(acc, arow, srow, H / kBlk, xr, st, seg, lane);
     f32x4 *red = reinterpret_cast<f32x4 *>(&seg[1].row[0][0]);
     static_assert(sizeof(f32x4) * (W / 2) * 2 * 64 <= sizeof(Seg), "reduction buffer");
     if (up) {
@@ -338,7 +366,7 @@ __device__ inline void w13_item(const uint8_t *__restrict__ we, const uint8_t *_
     }
 }
 
-template <int W, bool PK>
+template <int W, bool PK, bool GS>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) void w13_nvfp4_kernel(const uint8_t *__restrict__ ew,
                                                            const uint8_t *__restrict__ es,
                                                            const int32_t *__restrict__ meta,
@@ -361,14 +389,14 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
         const uint8_t *we = ew + (size_t)rec.x * ewb;
         const uint8_t *se = es + (size_t)rec.x * esb;
         if (rec.z > 16)
-            w13_item<2, W, PK>(we, se, H, I, i0, rec.y, rec.z, tok_of, xr, xk, hb, seg, wave, lane, tid);
+            w13_item<2, W, PK, GS>(we, se, H, I, i0, rec.y, rec.z, tok_of, xr, xk, hb, seg, wave, lane, tid);
         else
-            w13_item<1, W, PK>(we, se, H, I, i0, rec.y, rec.z, tok_of, xr, xk, hb, seg, wave, lane, tid);
+            w13_item<1, W, PK, GS>(we, se, H, I, i0, rec.y, rec.z, tok_of, xr, xk, hb, seg, wave, lane, tid);
     }
 }
 
 // down: item = (chunk, rows [n0, n0 + 16W)); wave w streams rows n0 + 16w.
-template <int NT, int W, bool PK>
+template <int NT, int W, bool PK, bool GS>
 __device__ inline void w2_item(const uint8_t *__restrict__ we, const uint8_t *__restrict__ se, int H, int I, int n0,
                                int slot0, int mc, __amdgpu_buffer_rsrc_t hr, float *__restrict__ obuf, Seg (&seg)[2],
                                int wave, int lane, int tid)
@@ -380,7 +408,7 @@ __device__ inline void w2_item(const uint8_t *__restrict__ we, const uint8_t *__
     Stager<NT, W> st;
     st.init(nullptr, slot0, mc, I, tid);
     f32x4 acc[NT];
-    stream_tile<NT, W, PK, false>(acc, arow, srow, I / kBlk, hr, st, seg, lane);
+    stream_tile<NT, W, PK, false, GS>(acc, arow, srow, I / kBlk, hr, st, seg, lane);
     const float td = reinterpret_cast<const float *>(se)[2];
 #pragma unroll
     for (int j = 0; j < NT; ++j)
@@ -388,7 +416,7 @@ __device__ inline void w2_item(const uint8_t *__restrict__ we, const uint8_t *__
             *reinterpret_cast<f32x4 *>(obuf + ((size_t)slot0 + 16 * j + r) * H + row0 + 4 * g) = td * acc[j];
 }
 
-template <int W, bool PK>
+template <int W, bool PK, bool GS>
 __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) void w2_nvfp4_kernel(const uint8_t *__restrict__ ew,
                                                           const uint8_t *__restrict__ es,
                                                           const int32_t *__restrict__ meta,
@@ -409,9 +437,9 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
         const uint8_t *we = ew + (size_t)rec.x * ewb;
         const uint8_t *se = es + (size_t)rec.x * esb;
         if (rec.z > 16)
-            w2_item<2, W, PK>(we, se, H, I, n0, rec.y, rec.z, hr, obuf, seg, wave, lane, tid);
+            w2_item<2, W, PK, GS>(we, se, H, I, n0, rec.y, rec.z, hr, obuf, seg, wave, lane, tid);
         else
-            w2_item<1, W, PK>(we, se, H, I, n0, rec.y, rec.z, hr, obuf, seg, wave, lane, tid);
+            w2_item<1, W, PK, GS>(we, se, H, I, n0, rec.y, rec.z, hr, obuf, seg, wave, lane, tid);
     }
 }
 
@@ -429,18 +457,26 @@ int nvfp4_grid(const Layer &L, int T, int k, int items_per_chunk)
 
 }  // namespace
 
+// Grouped packed scales (four blocks per 16-byte load) where the matrix's 256-input block
+// count is a multiple of four; moe_decode_pack_weights writes that layout for such
+// matrices.
+bool grouped_scales(const Layer &L, int K) { return L.wlayout && (K / kBlk) % 4 == 0; }
+
 hipError_t launch_w13_nvfp4(const Layer &L, const void *expert_w, const void *scales, int T, int k,
                             const int32_t *meta, const int32_t *tok_of, const Workspace &ws, hipStream_t st)
 {
     dim3 grid(nvfp4_grid(L, T, k, L.I / (8 * kWaves))), block(64 * kWaves);
-    if (L.wlayout)
-        w13_nvfp4_kernel<kWaves, true><<<grid, block, 0, st>>>(
-            (const uint8_t *)expert_w, (const uint8_t *)scales, meta, tok_of, ws.x16, ws.xk, (__bf16 *)ws.hb, T,
-            L.H, L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
+    const uint8_t *ew = (const uint8_t *)expert_w, *es = (const uint8_t *)scales;
+    __bf16 *hb = (__bf16 *)ws.hb;
+    if (grouped_scales(L, L.H))
+        w13_nvfp4_kernel<kWaves, true, true><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.x16, ws.xk, hb, T, L.H,
+                                                                     L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
+    else if (L.wlayout)
+        w13_nvfp4_kernel<kWaves, true, false><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.x16, ws.xk, hb, T, L.H,
+                                                                      L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
     else
-        w13_nvfp4_kernel<kWaves, false><<<grid, block, 0, st>>>(
-            (const uint8_t *)expert_w, (const uint8_t *)scales, meta, tok_of, ws.x16, ws.xk, (__bf16 *)ws.hb, T,
-            L.H, L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
+        w13_nvfp4_kernel<kWaves, false, false><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.x16, ws.xk, hb, T, L.H,
+                                                                       L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
     return hipGetLastError();
 }
 
@@ -448,14 +484,17 @@ hipError_t launch_w2_nvfp4(const Layer &L, const void *expert_w, const void *sca
                            const int32_t *meta, const Workspace &ws, hipStream_t st)
 {
     dim3 grid(nvfp4_grid(L, T, k, L.H / (16 * kWaves))), block(64 * kWaves);
-    if (L.wlayout)
-        w2_nvfp4_kernel<kWaves, true><<<grid, block, 0, st>>>((const uint8_t *)expert_w, (const uint8_t *)scales,
-                                                              meta, (const __bf16 *)ws.hb, ws.o, T * k, L.H, L.I, L.E,
-                                                              L.expert_w_bytes, L.expert_s_bytes);
+    const uint8_t *ew = (const uint8_t *)expert_w, *es = (const uint8_t *)scales;
+    const __bf16 *hb = (const __bf16 *)ws.hb;
+    if (grouped_scales(L, L.I))
+        w2_nvfp4_kernel<kWaves, true, true><<<grid, block, 0, st>>>(ew, es, meta, hb, ws.o, T * k, L.H, L.I, L.E,
+                                                                    L.expert_w_bytes, L.expert_s_bytes);
+    else if (L.wlayout)
+        w2_nvfp4_kernel<kWaves, true, false><<<grid, block, 0, st>>>(ew, es, meta, hb, ws.o, T * k, L.H, L.I, L.E,
+                                                                     L.expert_w_bytes, L.expert_s_bytes);
     else
-        w2_nvfp4_kernel<kWaves, false><<<grid, block, 0, st>>>((const uint8_t *)expert_w, (const uint8_t *)scales,
-                                                               meta, (const __bf16 *)ws.hb, ws.o, T * k, L.H, L.I,
-                                                               L.E, L.expert_w_bytes, L.expert_s_bytes);
+        w2_nvfp4_kernel<kWaves, false, false><<<grid, block, 0, st>>>(ew, es, meta, hb, ws.o, T * k, L.H, L.I, L.E,
+                                                                      L.expert_w_bytes, L.expert_s_bytes);
     return hipGetLastError();
 }
 

@@ -380,7 +380,9 @@ def pack_reference(expert_w, cfg):
 def pack_scales_reference(scales, cfg):
     """Packed scales.  NVFP4 E4M3: per expert the 16 bytes of matrix scales, then per
     matrix [rows][K/16] and per (16-row tile, 256-input block) 256 bytes, lane l's
-    scales [4g, 4g+4) of row l%16 at 4l.  MXFP4 E8M0: per matrix [rows][K/32] and per
+    scales [4g, 4g+4) of row l%16 at 4l; where K/256 is a multiple of four, per (16-row
+    tile, group of four blocks) 1 KB, lane l's scales of each block of the group at 16l.
+    MXFP4 E8M0: per matrix [rows][K/32] and per
     (16-row tile, group of four 128-input blocks) lane l's bytes (sub-block g of row l%16,
     blocks 4q..4q+3) at 4l (a last group of two blocks: 2l)."""
     H, I, E = cfg.hidden, cfg.inter, cfg.n_experts
@@ -400,8 +402,13 @@ def pack_scales_reference(scales, cfg):
         return out.reshape(scales.shape)
     off = 16
     for rows, K in ((2 * I, H), (H, I)):
-        m = sc[:, off: off + rows * K // 16].reshape(E, rows // 16, 16, K // 256, 4, 4)
-        out[:, off: off + rows * K // 16] = m.transpose(0, 1, 3, 4, 2, 5).reshape(E, -1)
+        KB = K // 256
+        m = sc[:, off: off + rows * K // 16].reshape(E, rows // 16, 16, KB, 4, 4)  # [E][tile][r][kb][g][4]
+        if KB % 4 == 0:  # [E][tile][group][g][r][block of the group][4]
+            v = m.reshape(E, rows // 16, 16, KB // 4, 4, 4, 4).transpose(0, 1, 3, 5, 2, 4, 6)
+        else:  # [E][tile][kb][g][r][4]
+            v = m.transpose(0, 1, 3, 4, 2, 5)
+        out[:, off: off + rows * K // 16] = v.reshape(E, -1)
         off += rows * K // 16
     return out.reshape(scales.shape)
 
@@ -409,7 +416,11 @@ def pack_scales_reference(scales, cfg):
 PACK_MX_768 = LayerConfig("pk-mx-768", 768, 16, 4, 768, "bf16", "bf16", "mxfp4", None, [])
 
 
-@pytest.mark.parametrize("cfg", [SMALL_FP8, SMALL_MX, PACK_MX_768, SMALL_NV], ids=["fp8", "mxfp4", "mxfp4-768", "nvfp4"])
+PACK_NV_G = LayerConfig("pk-nv-g", 2048, 8, 2, 1024, "bf16", "bf16", "nvfp4", None, [])
+
+
+@pytest.mark.parametrize("cfg", [SMALL_FP8, SMALL_MX, PACK_MX_768, SMALL_NV, PACK_NV_G],
+                         ids=["fp8", "mxfp4", "mxfp4-768", "nvfp4", "nvfp4-grouped"])
 def test_pack_matches_layout_definition(dev, cfg):
     from paper_2609_11133_amd import binding as B
 
@@ -440,6 +451,10 @@ PACKED_CFGS = [
     LayerConfig("pk-f32-mx", 256, 8, 2, 256, "f32", "f32", "mxfp4", None, []),
     LayerConfig("pk-nv", 512, 16, 4, 256, "bf16", "bf16", "nvfp4", "normal:0.5", []),
     LayerConfig("pk-nv-odd", 1280, 16, 4, 768, "bf16", "bf16", "nvfp4", "zipf:1.1", []),
+    # grouped NVFP4 scales (K/256 a multiple of four): one group in both projections, and
+    # three groups (gate/up) with two (down)
+    LayerConfig("pk-nv-g4", 1024, 16, 4, 1024, "bf16", "bf16", "nvfp4", None, []),
+    LayerConfig("pk-nv-g12", 3072, 8, 2, 2048, "bf16", "bf16", "nvfp4", "normal:0.5", []),
 ]
 
 
@@ -449,6 +464,25 @@ def test_packed_layout_layers(dev, cfg, T):
     hl = W.host_layer(cfg, seed=561)
     run = Run(cfg, hl, dev, max_tokens=40, weight_layout=1)
     check_layer(run, W.host_x(cfg, T, seed=561), label=f"{cfg.name} packed T={T}")
+
+
+PK_MX_SKEW = LayerConfig("pk-mx-skew", 1024, 8, 2, 512, "bf16", "bf16", "mxfp4", "zipf:1.1", [])
+
+
+@pytest.mark.parametrize("T", [20, 70, 150])
+def test_packed_mxfp4_skewed_chunks(dev, T):
+    """Packed MXFP4 weights on the staged kernels (four tiles per wave) with a
+    Zipf-skewed small layer: the hot expert holds 17 tokens at T=20 (one chunk of two
+    token tiles), 56 at T=70 (two chunks) and 115 at T=150 (four chunks)."""
+    hl = W.host_layer(PK_MX_SKEW, seed=571)
+    run = Run(PK_MX_SKEW, hl, dev, max_tokens=150, weight_layout=1)
+    check_layer(run, W.host_x(PK_MX_SKEW, T, seed=571 + T), label=f"{PK_MX_SKEW.name} T={T}")
+    st, counts = run.m.stats()
+    say(f"[skew] T={T}: tokens per expert {sorted(counts, reverse=True)}")
+    if T >= 70:
+        assert max(counts) > 32
+    if T == 150:
+        assert max(counts) > 64
 
 
 @pytest.mark.parametrize("T", [1, 64])
