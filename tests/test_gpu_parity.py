@@ -442,12 +442,15 @@ def test_pack_matches_layout_definition(dev, cfg):
 
 # every kernel variant on packed weights: FP8 staged gate/up (H/128 a multiple of 4) and
 # two-tile gate/up (H = 384), two-tile down (I/128 < 16) and staged down (I = 2048);
-# E2M1 staged (H, I multiples of 512) and two-tile (H = I = 768) kernels
+# E2M1 staged (H, I multiples of 512; three gate/up tiles per wave at I = 768) and
+# two-tile (H = I = 768) kernels
 PACKED_CFGS = [
     LayerConfig("pk-fp8", 512, 16, 4, 256, "bf16", "bf16", "fp8", "normal:0.5", []),
     LayerConfig("pk-fp8-h384", 384, 16, 4, 2048, "bf16", "bf16", "fp8", None, []),
     LayerConfig("pk-mx", 512, 16, 4, 512, "bf16", "bf16", "mxfp4", "zipf:1.1", []),
     LayerConfig("pk-mx-768", 768, 16, 4, 768, "bf16", "bf16", "mxfp4", None, []),
+    # E2M1 staged gate/up with three tiles per wave (I a multiple of 768)
+    LayerConfig("pk-mx-i768", 1024, 16, 4, 768, "bf16", "bf16", "mxfp4", "zipf:1.1", []),
     LayerConfig("pk-f32-mx", 256, 8, 2, 256, "f32", "f32", "mxfp4", None, []),
     LayerConfig("pk-nv", 512, 16, 4, 256, "bf16", "bf16", "nvfp4", "normal:0.5", []),
     LayerConfig("pk-nv-odd", 1280, 16, 4, 768, "bf16", "bf16", "nvfp4", "zipf:1.1", []),
