@@ -625,15 +625,19 @@ __device__ inline void stream_tile_lds(f32x4 (&acc)[NA][NT], const uint8_t *cons
                 w[a] = 0u;
         }
     };
-    auto loadA = [&](int slot, int kb, const uint32_t (&word)[NA]) {  // word: the E8M0 words holding block kb
+    // Packed E8M0 scales are taken from the segment's words when the block is multiplied,
+    // not when its weights are loaded: the next segment's words arrive during this one,
+    // and reading them at the load of the next segment's first block made every wave
+    // wait there for all but its five newest loads (MXFP4 Zipf layer at T=256: gate/up
+    // 120.0 -> 118.8 us in four-wave workgroups, 116.0 -> 115.5 us in eight-wave ones).
+    uint32_t wc[NA], wn[NA];  // words of the segment being multiplied and of the next one
+    auto loadA = [&](int slot, int kb) {
 #pragma unroll
         for (int a = 0; a < NA; ++a) {
             A[slot][a] = wfrag<FMT, PK>(arow[a], kb, g);
             if constexpr (FMT == 0)
                 EA[slot][a] = 127;
-            else if constexpr (PK)
-                EA[slot][a] = (int)__builtin_amdgcn_ubfe(word[a], 8 * (kb & 3), 8);
-            else
+            else if constexpr (!PK)
                 EA[slot][a] = erow[a][kb * 4 + g];
         }
     };
@@ -641,6 +645,10 @@ __device__ inline void stream_tile_lds(f32x4 (&acc)[NA][NT], const uint8_t *cons
         float sc[NA];
 #pragma unroll
         for (int a = 0; a < NA; ++a) sc[a] = FMT == 0 ? sblk[a][kb] : 1.f;
+        if constexpr (FMT == 1 && PK) {
+#pragma unroll
+            for (int a = 0; a < NA; ++a) EA[slot][a] = (int)__builtin_amdgcn_ubfe(wc[a], 8 * kk, 8);
+        }
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
             const int t = 16 * j + r;
@@ -659,11 +667,10 @@ __device__ inline void stream_tile_lds(f32x4 (&acc)[NA][NT], const uint8_t *cons
     for (int a = 0; a < NA; ++a)
 #pragma unroll
         for (int j = 0; j < NT; ++j) acc[a][j] = (f32x4){0.f, 0.f, 0.f, 0.f};
-    uint32_t wc[NA], wn[NA];  // words of the segment being multiplied and of the next one
     eword(wc, 0);
-    loadA(0, 0, wc);
-    loadA(1, 1, wc);
-    loadA(2, 2, wc);
+    loadA(0, 0);
+    loadA(1, 1);
+    loadA(2, 2);
     st.load(B, 0);
     st.store(seg[0], tid);
     st.load(B, nseg > 1 ? 1 : 0);
@@ -678,7 +685,7 @@ __device__ inline void stream_tile_lds(f32x4 (&acc)[NA][NT], const uint8_t *cons
             // The scheduling barrier keeps each block's loads here: left to itself the
             // scheduler sinks the next segment's loads to the end of the segment, and every
             // segment then starts with a full memory latency.
-            loadA((u + 3) & 3, min(kb + u + 3, KB - 1), u == 0 ? wc : wn);
+            loadA((u + 3) & 3, min(kb + u + 3, KB - 1));
             __builtin_amdgcn_sched_barrier(0);
             compute(u, cur, u, kb + u);
         }
@@ -722,10 +729,12 @@ __device__ inline void w13_item_lds(const uint8_t *__restrict__ we, const uint8_
     st.init(tok_of, slot0, mc, H, tid);
     f32x4 acc[NA][NT];
     stream_tile_lds<FMT, NT, W, NA, PK>(acc, arow, erow, sblk, H / 128, X, st, seg, lane, tid);
-    // red[(proj*NQ + q)*NT + j][lane]: 2*NQ*NT*64 f32x4 fit in seg[1].code, which the
-    // next item first writes after its first barrier, so no wave still reads red by then.
-    static_assert(sizeof(f32x4) * 2 * NQ * NT * 64 <= sizeof(seg[1].code), "reduction buffer");
-    f32x4 *red = reinterpret_cast<f32x4 *>(&seg[1].code[0][0][0]);
+    // red[(proj*NQ + q)*NT + j][lane]: 2*NQ*NT*64 f32x4.  Where they fit in seg[1].code,
+    // which the next item first writes after its first barrier, no wave still reads red
+    // by then; otherwise red starts at seg[0] and a barrier follows its last read.
+    constexpr bool kRedAll = sizeof(f32x4) * 2 * NQ * NT * 64 > sizeof(seg[1].code);
+    static_assert(sizeof(f32x4) * 2 * NQ * NT * 64 <= sizeof(seg), "reduction buffer");
+    f32x4 *red = kRedAll ? reinterpret_cast<f32x4 *>(&seg[0]) : reinterpret_cast<f32x4 *>(&seg[1].code[0][0][0]);
     auto ridx = [&](int proj, int q, int j) { return ((proj * NQ + q) * NT + j) * 64 + lane; };
 #pragma unroll
     for (int a = 0; a < NA; ++a)
@@ -768,10 +777,11 @@ __device__ inline void w13_item_lds(const uint8_t *__restrict__ we, const uint8_
             }
         }
     }
+    if constexpr (kRedAll) sync_lds();
 }
 
 template <int FMT, int W, int NA, bool PK>
-__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W == 8 ? 4 : 1))) void w13_mfma_lds_kernel(
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W == 8 ? (FMT == 1 ? 2 : 4) : 1))) void w13_mfma_lds_kernel(
     const uint8_t *__restrict__ ew, const uint8_t *__restrict__ es, const int32_t *__restrict__ meta,
     const int32_t *__restrict__ tok_of, const uint8_t *__restrict__ xs_hi, const uint8_t *__restrict__ xs_lo,
     const uint8_t *__restrict__ xe_hi, const uint8_t *__restrict__ xe_lo, uint8_t *__restrict__ hs_hi,
@@ -863,29 +873,35 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W == 8 ?
 // Waves per workgroup of the staged kernels.  FP8 weights stream at 4 waves and two
 // workgroups per CU: eight waves per CU hold the HBM stream at its best, and more
 // waves per CU slowed it (the 235B- and 480B-shaped layers lost 9-18%).  E2M1
-// weights carry half the bytes per activation fragment, so staging and fragment
-// reads, not HBM, bound them; 8-wave workgroups halve the staged activation bytes per
-// weight byte and, held to 128 VGPRs, run two per CU (the MXFP4 layer at T=256:
-// 570k against 604k tokens/s).
+// weights carry half the bytes per activation fragment, so the activation staging, not
+// HBM, bounds them: 4 waves with several tiles each (kStagedTiles), and 8 waves for the
+// three-tile gate/up (kThreeTileWaves), which stage each segment once for more rows.
+// Eight-wave workgroups held to 128 VGPRs to run two per CU lost (the MXFP4 layer at
+// T=256, one tile per wave: 570k against 604k tokens/s).
 template <int FMT>
-constexpr int kStagedWaves = FMT == 0 ? 4 : 4;
+constexpr int kStagedWaves = 4;
 // Weight tiles per wave of the staged kernels (NA).  E2M1 tiles: four on packed weights
 // (each staged activation fragment then feeds four tiles; MXFP4 Zipf layer at T=256
 // 1,035k -> 1,094k tokens/s), two on row-major ones (four need more than the 256
 // registers two waves per SIMD allow there).
 template <int FMT, bool PK>
 constexpr int kStagedTiles = FMT == 0 ? 1 : (PK ? 4 : 2);
-// Packed E2M1 gate/up takes three tiles per wave where I is a multiple of 768: an item
-// then covers 96 rows, a chunk 16 items (I = 1536), and since consecutive workgroups go
-// round-robin over the 8 XCDs, tile q of every chunk of one expert runs on one XCD and
+// Packed E2M1 gate/up takes three tiles per wave in eight-wave workgroups (one per CU,
+// up to 256 VGPRs) where I is a multiple of 1536: an item then covers 192 rows, a chunk
+// a multiple of 8 items, and since consecutive workgroups go round-robin over the 8
+// XCDs, tile q of every chunk of one expert runs on one XCD, at about the same time, and
 // its later chunks find the weights in that XCD's L2.  At four tiles (12 items per
-// chunk) consecutive chunks land 4 XCDs apart.  MXFP4 Zipf layer at T=256: gate/up
-// fetch 760 -> 629 MB, 126.0 -> 120.0 us, 1,095k -> 1,124k tokens/s.  Padding 12 items
-// to a stride of 16 instead put twice the work on half the XCDs (126 -> 138 us).
+// chunk at I = 1536) consecutive chunks land 4 XCDs apart.  MXFP4 Zipf layer at T=256:
+// three tiles in four-wave workgroups (96 rows, 16 items per chunk) took gate/up fetch
+// 760 -> 629 MB and 126.0 -> 120.0 us; eight waves, which stage each activation
+// segment once for twice the rows, 120.0 -> 116.0 us (1,124k -> 1,140k tokens/s).
+// Padding 12 items to a stride of 16 instead put twice the work on half the XCDs (126 ->
+// 138 us).  The down projection stays at four waves (eight: 69.5 -> 72.4 us).
+constexpr int kThreeTileWaves = 8;  // waves per workgroup of the three-tile gate/up
 template <int FMT, bool PK>
 constexpr bool w13_three_tiles(const Layer &L)
 {
-    return FMT == 1 && PK && L.I % (8 * kStagedWaves<FMT> * 3 * 8) == 0;
+    return FMT == 1 && PK && L.I % (8 * kThreeTileWaves * 3 * 8) == 0;
 }
 
 // Workgroups for `items_per_chunk` items per chunk record, `per_block` items per workgroup.
@@ -898,11 +914,10 @@ int mfma_grid(const Layer &L, int T, int k, int items_per_chunk, int per_block)
     return blocks < 1 ? 1 : (blocks > 65535 ? 65535 : (int)blocks);
 }
 
-template <int FMT, bool PK, int NA>
+template <int FMT, bool PK, int NA, int W = kStagedWaves<FMT>>
 hipError_t launch_w13_lds(const Layer &L, const uint8_t *ew, const uint8_t *es, int T, int k, const int32_t *meta,
                           const int32_t *tok_of, const Workspace &ws, hipStream_t st)
 {
-    constexpr int W = kStagedWaves<FMT>;
     dim3 grid(mfma_grid(L, T, k, L.I / (8 * W * NA), 1)), block(64 * W);
     w13_mfma_lds_kernel<FMT, W, NA, PK><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.xs_hi, ws.xs_lo, ws.xe_hi, ws.xe_lo,
                                                         ws.hs_hi, ws.hs_lo, ws.he_hi, ws.he_lo, T, L.H, L.I, L.E,
@@ -927,7 +942,8 @@ hipError_t w13_launch(const Layer &L, const uint8_t *ew, const uint8_t *es, int 
 {
     if ((L.H / 128) % 4 == 0) {
         if constexpr (FMT == 1 && PK)
-            if (w13_three_tiles<FMT, PK>(L)) return launch_w13_lds<FMT, PK, 3>(L, ew, es, T, k, meta, tok_of, ws, st);
+            if (w13_three_tiles<FMT, PK>(L))
+                return launch_w13_lds<FMT, PK, 3, kThreeTileWaves>(L, ew, es, T, k, meta, tok_of, ws, st);
         return launch_w13_lds<FMT, PK, kStagedTiles<FMT, PK>>(L, ew, es, T, k, meta, tok_of, ws, st);
     }
     dim3 grid(mfma_grid(L, T, k, L.I / 64, 1)), block(256);

@@ -442,15 +442,15 @@ def test_pack_matches_layout_definition(dev, cfg):
 
 # every kernel variant on packed weights: FP8 staged gate/up (H/128 a multiple of 4) and
 # two-tile gate/up (H = 384), two-tile down (I/128 < 16) and staged down (I = 2048);
-# E2M1 staged (H, I multiples of 512; three gate/up tiles per wave at I = 768) and
-# two-tile (H = I = 768) kernels
+# E2M1 staged (H, I multiples of 512; three gate/up tiles per wave in eight-wave
+# workgroups at I = 1536) and two-tile (H = I = 768) kernels
 PACKED_CFGS = [
     LayerConfig("pk-fp8", 512, 16, 4, 256, "bf16", "bf16", "fp8", "normal:0.5", []),
     LayerConfig("pk-fp8-h384", 384, 16, 4, 2048, "bf16", "bf16", "fp8", None, []),
     LayerConfig("pk-mx", 512, 16, 4, 512, "bf16", "bf16", "mxfp4", "zipf:1.1", []),
     LayerConfig("pk-mx-768", 768, 16, 4, 768, "bf16", "bf16", "mxfp4", None, []),
-    # E2M1 staged gate/up with three tiles per wave (I a multiple of 768)
-    LayerConfig("pk-mx-i768", 1024, 16, 4, 768, "bf16", "bf16", "mxfp4", "zipf:1.1", []),
+    # E2M1 staged gate/up with three tiles per wave (I a multiple of 1536)
+    LayerConfig("pk-mx-i1536", 1024, 16, 4, 1536, "bf16", "bf16", "mxfp4", "zipf:1.1", []),
     LayerConfig("pk-f32-mx", 256, 8, 2, 256, "f32", "f32", "mxfp4", None, []),
     LayerConfig("pk-nv", 512, 16, 4, 256, "bf16", "bf16", "nvfp4", "normal:0.5", []),
     LayerConfig("pk-nv-odd", 1280, 16, 4, 768, "bf16", "bf16", "nvfp4", "zipf:1.1", []),
@@ -470,18 +470,22 @@ def test_packed_layout_layers(dev, cfg, T):
 
 
 PK_MX_SKEW = LayerConfig("pk-mx-skew", 1024, 8, 2, 512, "bf16", "bf16", "mxfp4", "zipf:1.1", [])
+# three gate/up tiles per wave (I a multiple of 1536)
+PK_MX_SKEW_I1536 = LayerConfig("pk-mx-skew-i1536", 512, 8, 2, 1536, "bf16", "bf16", "mxfp4", "zipf:1.1", [])
 
 
+@pytest.mark.parametrize("cfg", [PK_MX_SKEW, PK_MX_SKEW_I1536], ids=lambda c: c.name)
 @pytest.mark.parametrize("T", [20, 70, 150])
-def test_packed_mxfp4_skewed_chunks(dev, T):
-    """Packed MXFP4 weights on the staged kernels (four tiles per wave) with a
-    Zipf-skewed small layer: the hot expert holds 17 tokens at T=20 (one chunk of two
-    token tiles), 56 at T=70 (two chunks) and 115 at T=150 (four chunks)."""
-    hl = W.host_layer(PK_MX_SKEW, seed=571)
-    run = Run(PK_MX_SKEW, hl, dev, max_tokens=150, weight_layout=1)
-    check_layer(run, W.host_x(PK_MX_SKEW, T, seed=571 + T), label=f"{PK_MX_SKEW.name} T={T}")
+def test_packed_mxfp4_skewed_chunks(dev, cfg, T):
+    """Packed MXFP4 weights on the staged kernels (four and three tiles per wave) with a
+    Zipf-skewed small layer: the hot expert fits one chunk of two token tiles at T=20
+    (17 and 13 tokens), takes two chunks at T=70 (more than 32) and three or four at
+    T=150 (more than 64)."""
+    hl = W.host_layer(cfg, seed=571)
+    run = Run(cfg, hl, dev, max_tokens=150, weight_layout=1)
+    check_layer(run, W.host_x(cfg, T, seed=571 + T), label=f"{cfg.name} T={T}")
     st, counts = run.m.stats()
-    say(f"[skew] T={T}: tokens per expert {sorted(counts, reverse=True)}")
+    say(f"[skew] {cfg.name} T={T}: tokens per expert {sorted(counts, reverse=True)}")
     if T >= 70:
         assert max(counts) > 32
     if T == 150:
