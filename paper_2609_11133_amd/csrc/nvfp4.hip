@@ -464,24 +464,40 @@ int nvfp4_grid(const Layer &L, int T, int k, int items_per_chunk)
 // matrices.
 bool grouped_scales(const Layer &L, int K) { return L.wlayout && (K / kBlk) % 4 == 0; }
 
-hipError_t launch_w13_nvfp4(const Layer &L, const void *expert_w, const void *scales, int T, int k,
-                            const int32_t *meta, const int32_t *tok_of, const Workspace &ws, hipStream_t st)
+// Gate/up workgroups of eight waves from 1024 (token, expert) pairs per step: with full
+// chunks each staged activation segment then serves twice the rows.  235B-shaped NVFP4
+// layer (four waves -> eight): Zipf T=256 gate/up 180.4 -> 169.6 us; T=64 152.0 -> 151.2
+// (equal within the spread); T=8 67.4 -> 70.0 and T=32 134.5 -> 137.3 us, so smaller
+// batches keep four.  Both give the same bits: a wave's rows and its K order do not
+// change.  The down projection keeps four (eight: 108.5 -> 121.0 us at Zipf T=256).
+constexpr int kWideBatchPairs = 1024;
+
+template <int W>
+hipError_t w13_nvfp4_launch(const Layer &L, const uint8_t *ew, const uint8_t *es, int T, int k, const int32_t *meta,
+                            const int32_t *tok_of, const Workspace &ws, hipStream_t st)
 {
-    dim3 grid(nvfp4_grid(L, T, k, L.I / (8 * kWaves))), block(64 * kWaves);
-    const uint8_t *ew = (const uint8_t *)expert_w, *es = (const uint8_t *)scales;
+    dim3 grid(nvfp4_grid(L, T, k, L.I / (8 * W))), block(64 * W);
     __bf16 *hb = (__bf16 *)ws.hb;
     if (grouped_scales(L, L.H))
-        w13_nvfp4_kernel<kWaves, true, true><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.x16, ws.xk, hb, T, L.H,
-                                                                     L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
+        w13_nvfp4_kernel<W, true, true><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.x16, ws.xk, hb, T, L.H, L.I,
+                                                                L.E, L.expert_w_bytes, L.expert_s_bytes);
     else if (L.wlayout)
-        w13_nvfp4_kernel<kWaves, true, false><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.x16, ws.xk, hb, T, L.H,
-                                                                      L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
+        w13_nvfp4_kernel<W, true, false><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.x16, ws.xk, hb, T, L.H, L.I,
+                                                                 L.E, L.expert_w_bytes, L.expert_s_bytes);
     else
-        w13_nvfp4_kernel<kWaves, false, false><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.x16, ws.xk, hb, T, L.H,
-                                                                       L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
+        w13_nvfp4_kernel<W, false, false><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.x16, ws.xk, hb, T, L.H, L.I,
+                                                                  L.E, L.expert_w_bytes, L.expert_s_bytes);
     return hipGetLastError();
 }
 
+hipError_t launch_w13_nvfp4(const Layer &L, const void *expert_w, const void *scales, int T, int k,
+                            const int32_t *meta, const int32_t *tok_of, const Workspace &ws, hipStream_t st)
+{
+    const uint8_t *ew = (const uint8_t *)expert_w, *es = (const uint8_t *)scales;
+    if ((long)T * k >= kWideBatchPairs && L.I % (8 * 8) == 0)
+        return w13_nvfp4_launch<8>(L, ew, es, T, k, meta, tok_of, ws, st);
+    return w13_nvfp4_launch<kWaves>(L, ew, es, T, k, meta, tok_of, ws, st);
+}
 hipError_t launch_w2_nvfp4(const Layer &L, const void *expert_w, const void *scales, int T, int k,
                            const int32_t *meta, const Workspace &ws, hipStream_t st)
 {

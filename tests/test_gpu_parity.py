@@ -492,6 +492,18 @@ def test_packed_mxfp4_skewed_chunks(dev, cfg, T):
         assert max(counts) > 64
 
 
+PK_NV_WIDE = LayerConfig("pk-nv-wide", 1024, 16, 8, 1024, "bf16", "bf16", "nvfp4", "zipf:1.1", [])
+
+
+@pytest.mark.parametrize("T", [127, 128, 140])
+def test_nvfp4_eight_wave_gate_up(dev, T):
+    """NVFP4 gate/up on either side of the eight-wave choice (from 1024 (token, expert)
+    pairs per step: T=128 at top-8), with skewed routing so that chunks are full."""
+    hl = W.host_layer(PK_NV_WIDE, seed=591)
+    run = Run(PK_NV_WIDE, hl, dev, max_tokens=140, weight_layout=1)
+    check_layer(run, W.host_x(PK_NV_WIDE, T, seed=591 + T), label=f"{PK_NV_WIDE.name} T={T}")
+
+
 @pytest.mark.parametrize("T", [1, 64])
 def test_full_235b_packed(dev, full_235b, T):
     """The 235B-shaped layer on packed weights (staged gate/up, the 12-block down)."""
