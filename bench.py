@@ -5,8 +5,13 @@ experts, combine) over one batch of T synthetic tokens, with all inputs resident
 HBM.  The headline workload is the Qwen3-Coder-480B-A35B-shaped layer (hidden 6144,
 160 experts, top-8, SwiGLU intermediate 2560, FP8-E4M3 weights with 128x128 fp32
 block scales, bf16 activations, router bias N(0, 0.5)) at T = 64, the largest batch
-of its sweep at or below 64 tokens; the Qwen3-235B-A22B-shaped layer (hidden 4096,
-128 experts, top-8, I 1536) is swept in the same run and reported beside it.
+of its sweep at or below 64 tokens.  The same run times, and reports beside it, the
+other workloads: the Qwen3-235B-A22B-shaped layer (hidden 4096, 128 experts, top-8,
+I 1536) swept over T = 1/8/32/64, one GPU's TP4 share of the 480B-shaped layer, the
+235B-shaped layer with MXFP4 and with NVFP4 weights (the Zipf-skewed batch of 256
+tokens for both, and the NVFP4 sweep), the stack of 12 distinct 480B-shaped layers
+decoded back to back over T = 1..256, and the decode-attention steps over a paged KV
+cache (--no-stack, --no-attn and --also '' leave them out).
 
 Cold-cache protocol: steps cycle over L copies of the layer's expert weights at
 distinct HBM addresses and over a pool of 16 token batches, so consecutive steps
@@ -79,12 +84,16 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--config", default="qwen3-coder-480b-a35b", help="layer of the headline line")
-    ap.add_argument("--also", default="qwen3-235b-a22b",
+    ap.add_argument("--also", default="qwen3-235b-a22b,qwen3-coder-480b-a35b-tp4,qwen3-235b-a22b-mxfp4-zipf,"
+                                      "qwen3-235b-a22b-nvfp4,qwen3-235b-a22b-nvfp4-zipf",
                     help="comma-separated further layer configurations swept in the same run and reported under "
                          "other_layers ('' for none)")
+    ap.add_argument("--no-attn", action="store_true", help="leave the decode-attention steps out of the default run")
+    ap.add_argument("--no-stack", action="store_true", help="leave the 12-layer stack out of the default run")
     ap.add_argument("--tokens", type=int, default=None, help="T of the headline line (default: largest T <= 64)")
     ap.add_argument("--copies", type=int, default=0, help="weight copies cycled (0: enough for 8 GB)")
-    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="the headline T only (no sweep, no stack, no attention steps)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-power", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU work of the oracle sample")
@@ -96,7 +105,8 @@ def parse():
                          "pieces and merged inside the split kernel (0: library default 16, -1: one piece per split, "
                          "merged by a second kernel)")
     ap.add_argument("--stack", action="store_true",
-                    help="also time the stack of 12 distinct 480B-shaped layers decoded back to back, T = 1..256")
+                    help="time the stack of 12 distinct 480B-shaped layers decoded back to back, T = 1..256, also "
+                         "with --no-sweep (the default run times it unless --no-stack)")
     ap.add_argument("--stack-steps", type=int, default=20)
     ap.add_argument("--layout", choices=["packed", "row-major"], default=None,
                     help="expert weight layout: packed 16-row tiles (default; converted once at setup by "
@@ -278,16 +288,18 @@ def run_stack(args, dev):
                 steps=args.stack_steps, by_tokens=out)
 
 
-def run_attn(args, dev):
+def run_attn(args, dev, emit=True):
     """Decode attention: per workload, B sequences' step time between HIP events over K
     steps that cycle KV-cache copies (>= 1 GB, so no step finds its cache in the MALL)
-    and 4 length draws; GB/s = the context's K and V bytes per step / step time."""
+    and 4 length draws; GB/s = the context's K and V bytes per step / step time.
+    Returns one record per workload; with `emit`, also prints each as a JSON line."""
     import numpy as np
     import torch
 
     from paper_2609_11133_amd import attn_workload as A
     from paper_2609_11133_amd import binding as B
 
+    lines = []
     for cfg in A.ATTN_CONFIGS:
         draws = [A.host_attn(cfg, draw=d, garbage=False) for d in range(4)]
         mp = max(h.block_table.shape[1] for h in draws)
@@ -338,9 +350,12 @@ def run_attn(args, dev):
         }
         print(f"[attn] {cfg.name}: {ms * 1e3:.1f} us/step, {gbs:.0f} GB/s ({gbs / PEAK_HBM_GBS:.3f} of peak), "
               f"mean context {ctx_mean:.0f}", file=sys.stderr, flush=True)
-        print(json.dumps(line), flush=True)
+        if emit:
+            print(json.dumps(line), flush=True)
+        lines.append(line)
         del dd, m
         torch.cuda.empty_cache()
+    return lines
 
 
 def cpu_info():
@@ -608,9 +623,17 @@ def main():
 
     R = results[T_main]
     traffic, traffic_src = w13_traffic(cfg, T_main)
+    # the 12-layer stack and the decode-attention steps: in the default run, or on request
     stack = None
-    if args.stack:
+    if args.stack or not (args.no_stack or args.no_sweep):
         stack = run_stack(args, dev)
+    attention = None
+    if not (args.no_attn or args.no_sweep):
+        attention = [dict(workload=a["config"]["workload"], us_per_step=round(a["ms_per_step"] * 1e3, 2),
+                          sequences_per_s=round(a["value"], 1), GBs=round(a["roofline"]["achieved"], 1),
+                          frac_of_peak=round(a["roofline"]["frac"], 4), bytes_per_step=a["roofline"]["bytes_per_step"],
+                          cold_cache=a["config"]["cold_cache"])
+                     for a in run_attn(args, dev, emit=False)]
     power = R.get("power")
     line = {
         "metric": METRIC,
@@ -664,6 +687,7 @@ def main():
         "power": power,
         "cpu_baseline": cpu,
         "stack": stack,
+        "attention": attention,
         "setup_s": round(setup_s, 1),
     }
     print(json.dumps(line))
