@@ -767,9 +767,13 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs A)
     if (!A.do_group) return;
     wait_stores();
     __syncthreads();
-    if (threadIdx.x == 0) s_flag = atomicAdd(A.cnt_all, 1) == A.T - 1;
-    __syncthreads();
-    if (!s_flag) return;
+    // One token: its last workgroup is the step's last, without the second counter's
+    // round trip (group_pairs leaves that counter at zero, where it already is).
+    if (A.T > 1) {
+        if (threadIdx.x == 0) s_flag = atomicAdd(A.cnt_all, 1) == A.T - 1;
+        __syncthreads();
+        if (!s_flag) return;
+    }
 
     group_pairs(A, lds, s_scan);
 }
