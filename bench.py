@@ -271,21 +271,18 @@ def run_stack(args, dev):
         torch.cuda.synchronize(dev)
         ms = start.elapsed_time(end) / args.stack_steps
         bytes_step = sum(n_act) * Be
-        out[str(T)] = dict(tokens_per_s=round(T / (ms * 1e-3), 1), ms_per_stack_step=round(ms, 4),
-                           us_per_layer=round(ms * 1e3 / cfg.layers, 1), n_active_mean=statistics.mean(n_act),
-                           GBs=round(bytes_step / (ms * 1e-3) / 1e9, 1),
-                           frac_of_peak=round(bytes_step / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4))
-        print(f"[stack] T={T}: {out[str(T)]['tokens_per_s']:.0f} tok/s, {ms * 1e3:.0f} us per 12-layer step, "
-              f"{out[str(T)]['GBs']:.0f} GB/s", file=sys.stderr, flush=True)
+        out[str(T)] = [round(T / (ms * 1e-3), 1), round(ms * 1e3, 1),
+                       round(bytes_step / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)]
+        print(f"[stack] T={T}: {T / (ms * 1e-3):.0f} tok/s, {ms * 1e3:.0f} us per 12-layer step "
+              f"({ms * 1e3 / cfg.layers:.1f} us per layer), {bytes_step / (ms * 1e-3) / 1e9:.0f} GB/s, "
+              f"n_active {statistics.mean(n_act):.1f}", file=sys.stderr, flush=True)
         del xs, ys
     m.close()
     del layers
     torch.cuda.empty_cache()
-    return dict(workload=f"{cfg.layers} distinct {cfg.name[:-4]}-shaped layers (H {cfg.hidden}, {cfg.n_experts} "
-                         f"experts, top-{cfg.topk}, I {cfg.inter}, fp8, "
-                         f"{'packed 16-row tiles' if layout else 'row-major'}), back to back, "
+    return dict(workload=f"{cfg.layers} distinct {cfg.name[:-4]}-shaped fp8 layers back to back, "
                          f"{cfg.layers * cfg.n_experts * Be / 1e9:.1f} GB of expert weights",
-                steps=args.stack_steps, by_tokens=out)
+                steps=args.stack_steps, fields=["tokens_per_s", "us_per_stack_step", "frac_of_peak"], **out)
 
 
 def run_attn(args, dev, emit=True):
@@ -541,9 +538,29 @@ def bench_layer(args, dev, cfg, sweep_T, T_main, pool=16):
     return results, layout, copies, setup_s, hl
 
 
-def sweep_json(results):
-    return {str(T): {k: (v if not isinstance(v, float) else round(v, 4)) for k, v in r.items()}
-            for T, r in results.items()}
+SWEEP_FIELDS = ["tokens_per_s", "us_per_step", "n_active_mean", "layer_frac", "w13_frac", "experts_frac",
+                "route_us", "w13_us", "w2_us", "combine_us", "board_W", "tokens_per_J"]
+OTHER_FIELDS = ["tokens_per_s", "us_per_step", "w13_frac", "experts_frac", "tokens_per_J"]
+
+
+def sweep_row(r, fields):
+    """One T of a layer as a list in the order of `fields`: the JSON line carries every
+    workload of the run, so each T is a short row and the full per-T records go to stderr."""
+    pw = r.get("power") or {}
+    v = dict(tokens_per_s=round(r["tokens_per_s"], 1), us_per_step=round(r["ms_per_step"] * 1e3, 2),
+             n_active_mean=round(r["n_active_mean"], 1), layer_frac=round(r["layer_frac"], 4),
+             w13_frac=round(r["w13_GBs"] / PEAK_HBM_GBS, 4), experts_frac=round(r["experts_frac"], 4),
+             board_W=round(pw["board_W"], 1) if pw.get("board_W") else None,
+             tokens_per_J=round(pw["tokens_per_J"], 2) if pw.get("board_W") else None)
+    for n in ("route", "w13", "w2", "combine"):
+        v[n + "_us"] = round(r["stage_ms"][n] * 1e3, 1)
+    return [v[f] for f in fields]
+
+
+def sweep_json(results, fields=SWEEP_FIELDS):
+    out = {"fields": fields}
+    out.update({str(T): sweep_row(r, fields) for T, r in results.items()})
+    return out
 
 
 def main():
@@ -585,10 +602,9 @@ def main():
         ocfg = C.BY_NAME[name]
         ores, _, ocopies, osetup, _ = bench_layer(args, dev, ocfg, sorted(ocfg.tokens), max(ocfg.tokens))
         others[name] = dict(
-            workload=f"{ocfg.name} MoE decode layer: hidden {ocfg.hidden}, {ocfg.n_experts} experts, "
-                     f"top-{ocfg.topk}, SwiGLU intermediate {ocfg.inter}, {ocfg.wfmt} weights, {ocfg.act} activations",
-            cold_cache=f"{ocopies} weight copies x 16 token batches cycled", setup_s=round(osetup, 1),
-            sweep=sweep_json(ores))
+            layer=f"H {ocfg.hidden}, E {ocfg.n_experts}, top-{ocfg.topk}, I {ocfg.inter}, {ocfg.wfmt}"
+                  + (f", bias {ocfg.bias}" if ocfg.bias else ""),
+            copies=ocopies, **{str(T): sweep_row(r, OTHER_FIELDS) for T, r in ores.items()})
 
     # the fp64 oracle on this host's cores, on a bounded sample of the headline batch
     cpu = None
@@ -629,11 +645,10 @@ def main():
         stack = run_stack(args, dev)
     attention = None
     if not (args.no_attn or args.no_sweep):
-        attention = [dict(workload=a["config"]["workload"], us_per_step=round(a["ms_per_step"] * 1e3, 2),
-                          sequences_per_s=round(a["value"], 1), GBs=round(a["roofline"]["achieved"], 1),
-                          frac_of_peak=round(a["roofline"]["frac"], 4), bytes_per_step=a["roofline"]["bytes_per_step"],
-                          cold_cache=a["config"]["cold_cache"])
-                     for a in run_attn(args, dev, emit=False)]
+        attention = {"fields": ["us_per_step", "frac_of_peak"]}
+        attention.update({a["config"]["workload"].split(":")[0]: [round(a["ms_per_step"] * 1e3, 2),
+                                                                  round(a["roofline"]["frac"], 4)]
+                          for a in run_attn(args, dev, emit=False)})
     power = R.get("power")
     line = {
         "metric": METRIC,
@@ -683,7 +698,7 @@ def main():
             "bytes_per_launch": R["w13_bytes_per_launch"],
         },
         "sweep": sweep_json(results),
-        "other_layers": others or None,
+        "other_layers": {"fields": OTHER_FIELDS, **others} if others else None,
         "power": power,
         "cpu_baseline": cpu,
         "stack": stack,
