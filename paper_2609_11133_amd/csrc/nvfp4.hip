@@ -155,21 +155,22 @@ __device__ inline __amdgpu_buffer_rsrc_t uniform_rsrc(const void *p)
     return __builtin_amdgcn_make_buffer_rsrc((void *)(((uint64_t)hi << 32) | lo), (short)0, -1, kRawBufferWord3);
 }
 
-// The f16 form of dequant: E2M1 pairs to f16 with the power of two of the scale applied
-// by the conversion, then the scale's mantissa (exact in f16) by one packed multiply.
-__device__ inline void dequant16(const u32x4v &w, float s0, float s1, f16x8 (&a)[4])
+// The f16 form of dequant: E2M1 pairs to f16 (exact), times the block scale, which the
+// E4M3 conversion gave as f16 (s.x: the first 16 inputs, s.y: the next 16), by packed
+// multiplies whose operand selection broadcasts one half of s.  A product of an E2M1
+// value and an E4M3 scale has at most 6 significant bits and lies in [2^-10, 2688] or is
+// zero: exact in f16.
+__device__ inline void dequant16(const u32x4v &w, f16x2 s, f16x8 (&a)[4])
 {
+    const f16x2 m0 = {s.x, s.x}, m1 = {s.y, s.y};
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-        const uint32_t sb = __float_as_uint(q < 2 ? s0 : s1);
-        const float p2 = __uint_as_float(sb & 0xFF800000u);                      // 2^e (0 for a zero scale)
-        const _Float16 mh = (_Float16)__uint_as_float((sb & 0x007FFFFFu) | 0x3F800000u);  // 1 + j/8
-        const f16x2 m2 = {mh, mh};
+        const f16x2 m = q < 2 ? m0 : m1;
         f16x2 v[4];
-        v[0] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w[q], p2, 0) * m2;
-        v[1] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w[q], p2, 1) * m2;
-        v[2] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w[q], p2, 2) * m2;
-        v[3] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w[q], p2, 3) * m2;
+        v[0] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w[q], 1.0f, 0) * m;
+        v[1] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w[q], 1.0f, 1) * m;
+        v[2] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w[q], 1.0f, 2) * m;
+        v[3] = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(w[q], 1.0f, 3) * m;
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
             a[q][2 * b] = v[b].x;
@@ -222,8 +223,12 @@ __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__
     // the four scales of group q of a grouped layout
     auto load_group = [&](int q) { return __builtin_amdgcn_raw_buffer_load_b128(sr, 16u * lane, q * 1024, 0); };
     auto compute = [&](int slot, const Seg &sg, int kk, uint32_t sw) {
+        // the four E4M3 scales of this lane's 64 inputs, as fp32 for the bf16 path and
+        // as f16 pairs for the f16 one (the unused pair is dead code)
         const f32x2 s01 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(sw, 1.0f, false);
         const f32x2 s23 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(sw, 1.0f, true);
+        const f16x2 h01 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sw, 1.0f, false);
+        const f16x2 h23 = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(sw, 1.0f, true);
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             u32x4v b[4][NT];
@@ -237,7 +242,7 @@ __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__
             __builtin_amdgcn_sched_barrier(0);
             if constexpr (F16) {
                 f16x8 a[4];
-                dequant16(A[slot][h], h ? s23.x : s01.x, h ? s23.y : s01.y, a);
+                dequant16(A[slot][h], h ? h23 : h01, a);
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
 #pragma unroll
