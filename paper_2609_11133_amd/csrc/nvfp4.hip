@@ -72,9 +72,12 @@ struct alignas(16) Seg {
 };
 
 // Piece p (16 bytes) of token t's segment row is stored at piece swz(p, t): the low
-// four bits of the piece index (128 inputs) are XORed with the token, so the 16 token
-// columns of a fragment read fall on distinct banks.
-__device__ inline int swz(int p, int t) { return (p & ~15) | ((p ^ t) & 15); }
+// four bits of the piece index are XORed with the token's low three bits.  A fragment
+// read gives lane (token r, group g) piece 8g + q of a block.  Measured in an LDS probe
+// at eight waves per CU, cycles per 1 KB ds_read_b128: 5.2 for these reads (one or two
+// token tiles) and for contiguous ones; 8.1, two-way bank conflicts, when all four
+// token bits were XORed in.  The stager's row writes run at the same rate either way.
+__device__ inline int swz(int p, int t) { return (p & ~15) | ((p ^ (t & 7)) & 15); }
 
 __device__ inline void sync_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
