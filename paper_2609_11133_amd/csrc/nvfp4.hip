@@ -67,9 +67,12 @@ constexpr int kSegBlk = 2;                // K blocks per staged segment
 constexpr int kRowBytes = kSegBlk * kBlk * 2;  // bf16 bytes of one token row per segment
 constexpr int kTok = 32;                  // token rows of a chunk
 
-struct alignas(16) Seg {
-    uint8_t row[kTok][kRowBytes];
+// A staged segment of ROWS token rows.
+template <int ROWS>
+struct alignas(16) SegT {
+    uint8_t row[ROWS][kRowBytes];
 };
+using Seg = SegT<kTok>;
 
 // Piece p (16 bytes) of token t's segment row is stored at piece swz(p, t): the low
 // four bits of the piece index are XORed with the token's low three bits.  A fragment
@@ -119,7 +122,8 @@ struct Stager {
         for (int q = 0; q < Q; ++q)
             code[q] = __builtin_amdgcn_raw_buffer_load_b128(rs, voff[q] + (uint32_t)sg * kRowBytes, 0, 0);
     }
-    __device__ void store(Seg &S) const
+    template <class S_>
+    __device__ void store(S_ &S) const
     {
 #pragma unroll
         for (int q = 0; q < Q; ++q)
@@ -192,10 +196,10 @@ __device__ inline void dequant16(const u32x4v &w, f16x2 s, f16x8 (&a)[4])
 //   GS    packed scales in groups of four blocks (PK, KB a multiple of 4): one 16-byte
 //         load per lane and group, issued a group ahead, at a fixed place in the loop
 //         (a conditional load in the steady state would make every wait conservative)
-template <int NT, int W, bool PK, bool F16, bool GS>
+template <int NT, int W, bool PK, bool F16, bool GS, class S_>
 __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__ arow,
                                    const uint8_t *__restrict__ srow, int KB, __amdgpu_buffer_rsrc_t rs,
-                                   Stager<NT, W> &st, Seg (&seg)[2], int lane)
+                                   Stager<NT, W> &st, S_ (&seg)[2], int lane)
 {
     static_assert(!GS || PK, "grouped scales are a packed layout");
     const int r = lane & 15, g = lane >> 4;
@@ -225,7 +229,7 @@ __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__
     f32x4 acc2[2][NT];
     // the four scales of group q of a grouped layout
     auto load_group = [&](int q) { return __builtin_amdgcn_raw_buffer_load_b128(sr, 16u * lane, q * 1024, 0); };
-    auto compute = [&](int slot, const Seg &sg, int kk, uint32_t sw) {
+    auto compute = [&](int slot, const S_ &sg, int kk, uint32_t sw) {
         // the four E4M3 scales of this lane's 64 inputs, as fp32 for the bf16 path and
         // as f16 pairs for the f16 one (the unused pair is dead code)
         const f32x2 s01 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(sw, 1.0f, false);
@@ -329,10 +333,10 @@ __device__ inline void stream_tile(f32x4 (&acc)[NT], const uint8_t *__restrict__
 // gate waves through LDS (seg[1], free once stream_tile returns; the next item first
 // writes it after its first barrier), and the gate waves form h = silu(g) * u, round
 // it to bf16 and store it.
-template <int NT, int W, bool PK, bool GS>
+template <int NT, int W, bool PK, bool GS, class S_>
 __device__ inline void w13_item(const uint8_t *__restrict__ we, const uint8_t *__restrict__ se, int H, int I, int i0,
                                 int slot0, int mc, const int32_t *__restrict__ tok_of, __amdgpu_buffer_rsrc_t xr,
-                                const int32_t *__restrict__ xk, __bf16 *__restrict__ hb, Seg (&seg)[2], int wave,
+                                const int32_t *__restrict__ xk, __bf16 *__restrict__ hb, S_ (&seg)[2], int wave,
                                 int lane, int tid)
 {
     constexpr int HW = W / 2;
@@ -346,7 +350,7 @@ __device__ inline void w13_item(const uint8_t *__restrict__ we, const uint8_t *_
     f32x4 acc[NT];
     stream_tile<NT, W, PK, true, GS>(acc, arow, srow, H / kBlk, xr, st, seg, lane);
     f32x4 *red = reinterpret_cast<f32x4 *>(&seg[1].row[0][0]);
-    static_assert(sizeof(f32x4) * (W / 2) * 2 * 64 <= sizeof(Seg), "reduction buffer");
+    static_assert(sizeof(f32x4) * (W / 2) * 2 * 64 <= sizeof(S_), "reduction buffer");
     if (up) {
 #pragma unroll
         for (int j = 0; j < NT; ++j) red[((wave - HW) * 2 + j) * 64 + lane] = acc[j];
@@ -376,8 +380,11 @@ __device__ inline void w13_item(const uint8_t *__restrict__ we, const uint8_t *_
     }
 }
 
-template <int W, bool PK, bool GS>
-__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) void w13_nvfp4_kernel(const uint8_t *__restrict__ ew,
+// T16: every chunk in passes of at most 16 tokens (one token tile), staged in
+// 16-row segments: half the LDS and none of the two-tile registers, for three waves
+// per SIMD.  A chunk of more than 16 tokens streams its weights once per pass.
+template <int W, bool PK, bool GS, bool T16>
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(T16 ? 3 : 2))) void w13_nvfp4_kernel(const uint8_t *__restrict__ ew,
                                                            const uint8_t *__restrict__ es,
                                                            const int32_t *__restrict__ meta,
                                                            const int32_t *__restrict__ tok_of,
@@ -385,7 +392,7 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
                                                            const int32_t *__restrict__ xk, __bf16 *__restrict__ hb,
                                                            int T, int H, int I, int E, size_t ewb, size_t esb)
 {
-    __shared__ Seg seg[2];
+    __shared__ SegT<T16 ? 16 : kTok> seg[2];
     const MetaIdx mi{E};
     const int tiles = I / (8 * W);
     const int n_items = meta[mi.n_mfma_chunks()] * tiles;
@@ -398,17 +405,22 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
         const int i0 = (item % tiles) * 8 * W;
         const uint8_t *we = ew + (size_t)rec.x * ewb;
         const uint8_t *se = es + (size_t)rec.x * esb;
-        if (rec.z > 16)
+        if constexpr (T16) {
+            for (int s0 = 0; s0 < rec.z; s0 += 16)
+                w13_item<1, W, PK, GS>(we, se, H, I, i0, rec.y + s0, min(16, rec.z - s0), tok_of, xr, xk, hb, seg, wave,
+                                       lane, tid);
+        } else if (rec.z > 16) {
             w13_item<2, W, PK, GS>(we, se, H, I, i0, rec.y, rec.z, tok_of, xr, xk, hb, seg, wave, lane, tid);
-        else
+        } else {
             w13_item<1, W, PK, GS>(we, se, H, I, i0, rec.y, rec.z, tok_of, xr, xk, hb, seg, wave, lane, tid);
+        }
     }
 }
 
 // down: item = (chunk, rows [n0, n0 + 16W)); wave w streams rows n0 + 16w.
-template <int NT, int W, bool PK, bool GS>
+template <int NT, int W, bool PK, bool GS, class S_>
 __device__ inline void w2_item(const uint8_t *__restrict__ we, const uint8_t *__restrict__ se, int H, int I, int n0,
-                               int slot0, int mc, __amdgpu_buffer_rsrc_t hr, float *__restrict__ obuf, Seg (&seg)[2],
+                               int slot0, int mc, __amdgpu_buffer_rsrc_t hr, float *__restrict__ obuf, S_ (&seg)[2],
                                int wave, int lane, int tid)
 {
     const int r = lane & 15, g = lane >> 4;
@@ -426,14 +438,15 @@ __device__ inline void w2_item(const uint8_t *__restrict__ we, const uint8_t *__
             *reinterpret_cast<f32x4 *>(obuf + ((size_t)slot0 + 16 * j + r) * H + row0 + 4 * g) = td * acc[j];
 }
 
-template <int W, bool PK, bool GS>
-__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) void w2_nvfp4_kernel(const uint8_t *__restrict__ ew,
+// T16 as for the gate/up kernel.
+template <int W, bool PK, bool GS, bool T16>
+__global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(T16 ? 3 : 2))) void w2_nvfp4_kernel(const uint8_t *__restrict__ ew,
                                                           const uint8_t *__restrict__ es,
                                                           const int32_t *__restrict__ meta,
                                                           const __bf16 *__restrict__ hb, float *__restrict__ obuf,
                                                           int P, int H, int I, int E, size_t ewb, size_t esb)
 {
-    __shared__ Seg seg[2];
+    __shared__ SegT<T16 ? 16 : kTok> seg[2];
     const MetaIdx mi{E};
     const int tiles = H / (16 * W);
     const int n_items = meta[mi.n_mfma_chunks()] * tiles;
@@ -446,10 +459,14 @@ __global__ __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(2))) voi
         const int n0 = (item % tiles) * 16 * W;
         const uint8_t *we = ew + (size_t)rec.x * ewb;
         const uint8_t *se = es + (size_t)rec.x * esb;
-        if (rec.z > 16)
+        if constexpr (T16) {
+            for (int s0 = 0; s0 < rec.z; s0 += 16)
+                w2_item<1, W, PK, GS>(we, se, H, I, n0, rec.y + s0, min(16, rec.z - s0), hr, obuf, seg, wave, lane, tid);
+        } else if (rec.z > 16) {
             w2_item<2, W, PK, GS>(we, se, H, I, n0, rec.y, rec.z, hr, obuf, seg, wave, lane, tid);
-        else
+        } else {
             w2_item<1, W, PK, GS>(we, se, H, I, n0, rec.y, rec.z, hr, obuf, seg, wave, lane, tid);
+        }
     }
 }
 
@@ -480,21 +497,52 @@ bool grouped_scales(const Layer &L, int K) { return L.wlayout && (K / kBlk) % 4 
 // change.  The down projection keeps four (eight: 108.5 -> 121.0 us at Zipf T=256).
 constexpr int kWideBatchPairs = 1024;
 
-template <int W>
+// One-tile passes (T16) on packed weights up to this many (token, expert) pairs per
+// expert on average (T=128 at top-8 of 128 experts; the gate/up kernel takes its
+// eight-wave form from 1024 pairs first).  Three waves per SIMD against two,
+// 235B-shaped NVFP4 layer, gate/up and down us: T=8 66.7/43.4 -> 63.3/39.0, T=32
+// 132.0/87.8 -> 125.9/78.3, T=64 149.8/101.4 -> 142.2/93.0; T=96 155.6/104.3 ->
+// 147.3/96.4 and T=127 159.4/105.6 -> 152.0/99.2, where hot experts take several
+// passes.  Row-major weights keep the two-tile kernels (their T16 form spills at
+// three waves).
+constexpr long kTileOnlyPairsPerExpert = 8;
+
+static bool tile_only(const Layer &L, int T, int k) { return L.wlayout && (long)T * k <= kTileOnlyPairsPerExpert * (long)L.E; }
+
+template <int W, bool T16>
 hipError_t w13_nvfp4_launch(const Layer &L, const uint8_t *ew, const uint8_t *es, int T, int k, const int32_t *meta,
                             const int32_t *tok_of, const Workspace &ws, hipStream_t st)
 {
     dim3 grid(nvfp4_grid(L, T, k, L.I / (8 * W))), block(64 * W);
     __bf16 *hb = (__bf16 *)ws.hb;
     if (grouped_scales(L, L.H))
-        w13_nvfp4_kernel<W, true, true><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.x16, ws.xk, hb, T, L.H, L.I,
-                                                                L.E, L.expert_w_bytes, L.expert_s_bytes);
+        w13_nvfp4_kernel<W, true, true, T16><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.x16, ws.xk, hb, T, L.H,
+                                                                     L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
     else if (L.wlayout)
-        w13_nvfp4_kernel<W, true, false><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.x16, ws.xk, hb, T, L.H, L.I,
-                                                                 L.E, L.expert_w_bytes, L.expert_s_bytes);
+        w13_nvfp4_kernel<W, true, false, T16><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.x16, ws.xk, hb, T, L.H,
+                                                                      L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
     else
-        w13_nvfp4_kernel<W, false, false><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.x16, ws.xk, hb, T, L.H, L.I,
-                                                                  L.E, L.expert_w_bytes, L.expert_s_bytes);
+        w13_nvfp4_kernel<W, false, false, false><<<grid, block, 0, st>>>(ew, es, meta, tok_of, ws.x16, ws.xk, hb, T,
+                                                                         L.H, L.I, L.E, L.expert_w_bytes,
+                                                                         L.expert_s_bytes);
+    return hipGetLastError();
+}
+
+template <bool T16>
+hipError_t w2_nvfp4_launch(const Layer &L, const uint8_t *ew, const uint8_t *es, int T, int k, const int32_t *meta,
+                           const Workspace &ws, hipStream_t st)
+{
+    dim3 grid(nvfp4_grid(L, T, k, L.H / (16 * kWaves))), block(64 * kWaves);
+    const __bf16 *hb = (const __bf16 *)ws.hb;
+    if (grouped_scales(L, L.I))
+        w2_nvfp4_kernel<kWaves, true, true, T16><<<grid, block, 0, st>>>(ew, es, meta, hb, ws.o, T * k, L.H, L.I, L.E,
+                                                                         L.expert_w_bytes, L.expert_s_bytes);
+    else if (L.wlayout)
+        w2_nvfp4_kernel<kWaves, true, false, T16><<<grid, block, 0, st>>>(ew, es, meta, hb, ws.o, T * k, L.H, L.I, L.E,
+                                                                          L.expert_w_bytes, L.expert_s_bytes);
+    else
+        w2_nvfp4_kernel<kWaves, false, false, false><<<grid, block, 0, st>>>(ew, es, meta, hb, ws.o, T * k, L.H, L.I,
+                                                                             L.E, L.expert_w_bytes, L.expert_s_bytes);
     return hipGetLastError();
 }
 
@@ -503,25 +551,18 @@ hipError_t launch_w13_nvfp4(const Layer &L, const void *expert_w, const void *sc
 {
     const uint8_t *ew = (const uint8_t *)expert_w, *es = (const uint8_t *)scales;
     if ((long)T * k >= kWideBatchPairs && L.I % (8 * 8) == 0)
-        return w13_nvfp4_launch<8>(L, ew, es, T, k, meta, tok_of, ws, st);
-    return w13_nvfp4_launch<kWaves>(L, ew, es, T, k, meta, tok_of, ws, st);
+        return w13_nvfp4_launch<8, false>(L, ew, es, T, k, meta, tok_of, ws, st);
+    if (tile_only(L, T, k))
+        return w13_nvfp4_launch<kWaves, true>(L, ew, es, T, k, meta, tok_of, ws, st);
+    return w13_nvfp4_launch<kWaves, false>(L, ew, es, T, k, meta, tok_of, ws, st);
 }
 hipError_t launch_w2_nvfp4(const Layer &L, const void *expert_w, const void *scales, int T, int k,
                            const int32_t *meta, const Workspace &ws, hipStream_t st)
 {
-    dim3 grid(nvfp4_grid(L, T, k, L.H / (16 * kWaves))), block(64 * kWaves);
     const uint8_t *ew = (const uint8_t *)expert_w, *es = (const uint8_t *)scales;
-    const __bf16 *hb = (const __bf16 *)ws.hb;
-    if (grouped_scales(L, L.I))
-        w2_nvfp4_kernel<kWaves, true, true><<<grid, block, 0, st>>>(ew, es, meta, hb, ws.o, T * k, L.H, L.I, L.E,
-                                                                    L.expert_w_bytes, L.expert_s_bytes);
-    else if (L.wlayout)
-        w2_nvfp4_kernel<kWaves, true, false><<<grid, block, 0, st>>>(ew, es, meta, hb, ws.o, T * k, L.H, L.I, L.E,
-                                                                     L.expert_w_bytes, L.expert_s_bytes);
-    else
-        w2_nvfp4_kernel<kWaves, false, false><<<grid, block, 0, st>>>(ew, es, meta, hb, ws.o, T * k, L.H, L.I, L.E,
-                                                                      L.expert_w_bytes, L.expert_s_bytes);
-    return hipGetLastError();
+    if (tile_only(L, T, k))
+        return w2_nvfp4_launch<true>(L, ew, es, T, k, meta, ws, st);
+    return w2_nvfp4_launch<false>(L, ew, es, T, k, meta, ws, st);
 }
 
 }  // namespace moe

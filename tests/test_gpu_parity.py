@@ -504,6 +504,26 @@ def test_nvfp4_eight_wave_gate_up(dev, T):
     check_layer(run, W.host_x(PK_NV_WIDE, T, seed=591 + T), label=f"{PK_NV_WIDE.name} T={T}")
 
 
+PK_NV_T16 = LayerConfig("pk-nv-t16", 512, 32, 2, 256, "bf16", "bf16", "nvfp4", "zipf:1.1", [])
+
+
+@pytest.mark.parametrize("T", [1, 37, 100, 128, 129])
+def test_nvfp4_one_tile_passes(dev, T):
+    """Packed NVFP4 kernels in passes of one 16-token tile, used up to eight (token,
+    expert) pairs per expert on average (T <= 128 at top-2 of 32 experts), and the
+    two-tile kernels at T=129.  Zipf-skewed routing gives the hot expert 24 tokens at
+    T=37 (one chunk, two passes) and 70 at T=100 (chunks of 32, 32 and 6)."""
+    hl = W.host_layer(PK_NV_T16, seed=601)
+    run = Run(PK_NV_T16, hl, dev, max_tokens=129, weight_layout=1)
+    check_layer(run, W.host_x(PK_NV_T16, T, seed=601 + T), label=f"{PK_NV_T16.name} T={T}")
+    st, counts = run.m.stats()
+    say(f"[t16] {PK_NV_T16.name} T={T}: tokens per expert {sorted(counts, reverse=True)[:6]}")
+    if T == 37:
+        assert max(counts) > 16
+    if T >= 100:
+        assert max(counts) > 32
+
+
 @pytest.mark.parametrize("T", [1, 64])
 def test_full_235b_packed(dev, full_235b, T):
     """The 235B-shaped layer on packed weights (staged gate/up, the 12-block down)."""
