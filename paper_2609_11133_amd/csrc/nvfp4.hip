@@ -552,8 +552,17 @@ hipError_t launch_w13_nvfp4(const Layer &L, const void *expert_w, const void *sc
     const uint8_t *ew = (const uint8_t *)expert_w, *es = (const uint8_t *)scales;
     if ((long)T * k >= kWideBatchPairs && L.I % (8 * 8) == 0)
         return w13_nvfp4_launch<8, false>(L, ew, es, T, k, meta, tok_of, ws, st);
-    if (tile_only(L, T, k))
+    if (tile_only(L, T, k)) {
+        // Eight-wave one-tile workgroups (126 VGPRs, four waves per SIMD) where chunks
+        // are fuller, from four pairs per expert on average, or where the four-wave grid
+        // would leave most CUs with one workgroup (fewer than 512 items on 256 CUs).
+        // 235B-shaped layer, gate/up us (four -> eight waves): T=1 17.35 -> 16.4, T=127
+        // 152.6 -> 149.2; T=8 63.4 -> 64.3, T=32 125.7 -> 128.6, T=64 142.0 -> 142.9.
+        const long pairs = (long)T * k;
+        if ((pairs > 4L * L.E || pairs * (L.I / (8 * kWaves)) < 512) && L.I % (8 * 8) == 0)
+            return w13_nvfp4_launch<8, true>(L, ew, es, T, k, meta, tok_of, ws, st);
         return w13_nvfp4_launch<kWaves, true>(L, ew, es, T, k, meta, tok_of, ws, st);
+    }
     return w13_nvfp4_launch<kWaves, false>(L, ew, es, T, k, meta, tok_of, ws, st);
 }
 hipError_t launch_w2_nvfp4(const Layer &L, const void *expert_w, const void *scales, int T, int k,
