@@ -566,8 +566,8 @@ def sweep_json(results, fields=SWEEP_FIELDS):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU: the layer is measured at one GPU's share "
-                                   "(the TP4 shard configuration), and sharding across GPUs is a design note only",
+        print(json.dumps({"error": "the benchmark runs on one GPU: the layer is measured at one GPU's share "
+                                   "(the TP4 shard configuration); the library has no multi-GPU path",
                           "n_gpus": args.gpus}))
         sys.exit(2)
 
