@@ -528,21 +528,20 @@ hipError_t w13_nvfp4_launch(const Layer &L, const uint8_t *ew, const uint8_t *es
     return hipGetLastError();
 }
 
-template <bool T16>
+// Packed weights only: row-major ones take the four-wave two-tile kernel
+// (launch_w2_nvfp4).
+template <int W, bool T16>
 hipError_t w2_nvfp4_launch(const Layer &L, const uint8_t *ew, const uint8_t *es, int T, int k, const int32_t *meta,
                            const Workspace &ws, hipStream_t st)
 {
-    dim3 grid(nvfp4_grid(L, T, k, L.H / (16 * kWaves))), block(64 * kWaves);
+    dim3 grid(nvfp4_grid(L, T, k, L.H / (16 * W))), block(64 * W);
     const __bf16 *hb = (const __bf16 *)ws.hb;
     if (grouped_scales(L, L.I))
-        w2_nvfp4_kernel<kWaves, true, true, T16><<<grid, block, 0, st>>>(ew, es, meta, hb, ws.o, T * k, L.H, L.I, L.E,
-                                                                         L.expert_w_bytes, L.expert_s_bytes);
-    else if (L.wlayout)
-        w2_nvfp4_kernel<kWaves, true, false, T16><<<grid, block, 0, st>>>(ew, es, meta, hb, ws.o, T * k, L.H, L.I, L.E,
-                                                                          L.expert_w_bytes, L.expert_s_bytes);
+        w2_nvfp4_kernel<W, true, true, T16><<<grid, block, 0, st>>>(ew, es, meta, hb, ws.o, T * k, L.H, L.I, L.E,
+                                                                    L.expert_w_bytes, L.expert_s_bytes);
     else
-        w2_nvfp4_kernel<kWaves, false, false, false><<<grid, block, 0, st>>>(ew, es, meta, hb, ws.o, T * k, L.H, L.I,
-                                                                             L.E, L.expert_w_bytes, L.expert_s_bytes);
+        w2_nvfp4_kernel<W, true, false, T16><<<grid, block, 0, st>>>(ew, es, meta, hb, ws.o, T * k, L.H, L.I, L.E,
+                                                                     L.expert_w_bytes, L.expert_s_bytes);
     return hipGetLastError();
 }
 
@@ -569,9 +568,19 @@ hipError_t launch_w2_nvfp4(const Layer &L, const void *expert_w, const void *sca
                            const int32_t *meta, const Workspace &ws, hipStream_t st)
 {
     const uint8_t *ew = (const uint8_t *)expert_w, *es = (const uint8_t *)scales;
+    if (!L.wlayout) {
+        dim3 grid(nvfp4_grid(L, T, k, L.H / (16 * kWaves))), block(64 * kWaves);
+        w2_nvfp4_kernel<kWaves, false, false, false><<<grid, block, 0, st>>>(
+            ew, es, meta, (const __bf16 *)ws.hb, ws.o, T * k, L.H, L.I, L.E, L.expert_w_bytes, L.expert_s_bytes);
+        return hipGetLastError();
+    }
+    // One-tile passes in eight-wave workgroups (124-133 VGPRs, three or four waves per
+    // SIMD), 128 rows per item.  235B-shaped layer, down us (four -> eight waves): T=32
+    // 78.7 -> 77.9, T=64 92.8 -> 91.5, T=127 99.0 -> 97.4; T=1 and T=8 equal.
     if (tile_only(L, T, k))
-        return w2_nvfp4_launch<true>(L, ew, es, T, k, meta, ws, st);
-    return w2_nvfp4_launch<false>(L, ew, es, T, k, meta, ws, st);
+        return L.H % (16 * 8) == 0 ? w2_nvfp4_launch<8, true>(L, ew, es, T, k, meta, ws, st)
+                                   : w2_nvfp4_launch<kWaves, true>(L, ew, es, T, k, meta, ws, st);
+    return w2_nvfp4_launch<kWaves, false>(L, ew, es, T, k, meta, ws, st);
 }
 
 }  // namespace moe
