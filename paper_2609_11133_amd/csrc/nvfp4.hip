@@ -575,11 +575,10 @@ hipError_t launch_w2_nvfp4(const Layer &L, const void *expert_w, const void *sca
         return hipGetLastError();
     }
     // One-tile passes in eight-wave workgroups (124-133 VGPRs, three or four waves per
-    // SIMD), 128 rows per item.  235B-shaped layer, down us (four -> eight waves): T=32
-    // 78.7 -> 77.9, T=64 92.8 -> 91.5, T=127 99.0 -> 97.4; T=1 and T=8 equal.
-    if (tile_only(L, T, k))
-        return L.H % (16 * 8) == 0 ? w2_nvfp4_launch<8, true>(L, ew, es, T, k, meta, ws, st)
-                                   : w2_nvfp4_launch<kWaves, true>(L, ew, es, T, k, meta, ws, st);
+    // SIMD), 128 rows per item (H is a multiple of 256 for NVFP4 weights, checked at
+    // init).  235B-shaped layer, down us (four -> eight waves): T=32 78.7 -> 77.9, T=64
+    // 92.8 -> 91.5, T=127 99.0 -> 97.4; T=1 and T=8 equal.
+    if (tile_only(L, T, k)) return w2_nvfp4_launch<8, true>(L, ew, es, T, k, meta, ws, st);
     return w2_nvfp4_launch<kWaves, false>(L, ew, es, T, k, meta, ws, st);
 }
 
